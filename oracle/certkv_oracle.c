@@ -1,0 +1,520 @@
+/*
+ * certkv_oracle.c -- TEST INFRASTRUCTURE.  A plain, slow, fp64 CPU oracle of
+ * the CertKV one-shot compression pass.  Only the test suite, the smoke check
+ * and the CPU-baseline leg of the benchmark may call it; the product path
+ * (libcertkv.so) never does, and the two share no source.
+ *
+ * Source: "Beyond Sparse Weights: When Is Attention Compressible?"
+ * (arXiv 2608.21541).  Every function below names the passage it follows.
+ * Arithmetic is IEEE binary64, built with -ffp-contract=off so that every
+ * a*b+c is two roundings unless fma() is written out.
+ *
+ * Readings of points the paper leaves open (each is listed in the design doc):
+ *   - GQA: the scores of the query heads of one KV head are summed.
+ *   - Causal window rows: row q at position p sees keys j <= p.
+ *   - Sort key: the fp32 score s itself, descending; equal s keep ascending
+ *     position (the paper's tie rule for orderings).
+ *   - lambda_hi = 2 * max over every head and every b in [0, n-1] of c + 1.
+ *   - argmin ties go to the smallest b; c(b) + lambda*b is evaluated as the
+ *     single-rounding fma(lambda, b, c(b)) on the fp32 curve values.
+ *   - Repair adds one token to the head with the smallest marginal
+ *     c(b+1) - c(b) (ties: lowest head), or, should the bisection end above
+ *     the budget, removes one from the head with the smallest c(b-1) - c(b).
+ *   - The slot centroids are direct weighted sums over the evicted keys;
+ *     m = 0 gives zero vectors.
+ *
+ * Parity pins of each function are the tests in tests/test_oracle_pins.py.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORA_OK 0
+#define ORA_EINVAL -1
+#define ORA_EINFEASIBLE -3
+#define ORA_ENONFINITE -4
+#define ORA_ENOMEM -7
+
+/* ------------------------------------------------------------------------ */
+/* Scores.  Section 3, one-row setup: A_j = exp(l_j) / sum_t exp(l_t) with
+ * l_j = <q, k_j> / sqrt(d).  The window scorer sums the softmax weights of
+ * every window row (and here every query head of the group) per key.
+ *   q     [M][d]  the M = w*G window rows of one KV head
+ *   qpos  [M]     position of each row (causal: keys j <= qpos visible)
+ *   k     [n][d]
+ *   s     [n]     out, sum over rows of A_{row, j}
+ *   lse   [M]     out (may be NULL), natural-log partition function per row */
+int ora_scores(int64_t n, int32_t d, int32_t M, const double* q,
+               const int64_t* qpos, const double* k, double scale,
+               int32_t causal, double* s, double* lse) {
+  if (n <= 0 || d <= 0 || M <= 0) return ORA_EINVAL;
+  double* logit = (double*)malloc(sizeof(double) * (size_t)n);
+  if (!logit) return ORA_ENOMEM;
+  for (int64_t j = 0; j < n; ++j) s[j] = 0.0;
+  for (int32_t r = 0; r < M; ++r) {
+    int64_t visible = n;
+    if (causal) {
+      visible = qpos[r] + 1;
+      if (visible > n) visible = n;
+      if (visible < 1) visible = 1;
+    }
+    const double* qr = q + (size_t)r * d;
+    double mx = -INFINITY;
+    for (int64_t j = 0; j < visible; ++j) {
+      const double* kj = k + (size_t)j * d;
+      double dot = 0.0;
+      for (int32_t t = 0; t < d; ++t) dot += qr[t] * kj[t];
+      logit[j] = scale * dot;
+      if (logit[j] > mx) mx = logit[j];
+    }
+    double z = 0.0;
+    for (int64_t j = 0; j < visible; ++j) z += exp(logit[j] - mx);
+    for (int64_t j = 0; j < visible; ++j) s[j] += exp(logit[j] - mx) / z;
+    if (lse) lse[r] = mx + log(z);
+  }
+  free(logit);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Ordering.  Algorithm 1 sorts each head's keys by score descending; the
+ * paper orders ties by index (Section 3, the ordering pi of the gap profile).
+ * perm[r] = position of the key at rank r (rank 0 = highest score). */
+static const float* g_sort_keys; /* qsort has no context argument */
+
+static int cmp_desc_then_index(const void* pa, const void* pb) {
+  int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
+  float sa = g_sort_keys[a], sb = g_sort_keys[b];
+  if (sa > sb) return -1;
+  if (sa < sb) return 1;
+  return (a < b) ? -1 : (a > b);
+}
+
+int ora_order(int64_t n, const float* s32, int32_t* perm) {
+  if (n <= 0) return ORA_EINVAL;
+  for (int64_t j = 0; j < n; ++j) {
+    if (!isfinite(s32[j])) return ORA_ENONFINITE;
+    perm[j] = (int32_t)j;
+  }
+#pragma omp critical(ora_sort)
+  {
+    g_sort_keys = s32;
+    qsort(perm, (size_t)n, sizeof(int32_t), cmp_desc_then_index);
+  }
+  return ORA_OK;
+}
+
+/* Normalization, appendix "CertKV: implementation": a_j = (s_j)_+ /
+ * sum_i (s_i)_+, normalized directly (no second softmax).  The sum runs in
+ * position order.  An all-zero score vector gives the uniform a = 1/n. */
+int ora_normalize(int64_t n, const float* s32, double* a) {
+  double tot = 0.0;
+  for (int64_t j = 0; j < n; ++j) {
+    if (!isfinite(s32[j])) return ORA_ENONFINITE;
+    double sp = s32[j] > 0.0f ? (double)s32[j] : 0.0;
+    tot += sp;
+  }
+  for (int64_t j = 0; j < n; ++j) {
+    double sp = s32[j] > 0.0f ? (double)s32[j] : 0.0;
+    a[j] = tot > 0.0 ? sp / tot : 1.0 / (double)n;
+  }
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Dispersion curve.  Section 4.1 Eq. certkv-curve and the appendix's suffix
+ * moments: over the evicted suffix E(b) = ranks b..n-1 (0-based; the keys
+ * ranked after the b kept ones)
+ *   m(b) = sum a_j,  W(b) = sum a_j v_j,  Q(b) = sum a_j |v_j|^2,
+ *   c(b) = sqrt((m Q - |W|^2)_+),  b = 0..n-1.
+ * The sums are accumulated from rank n-1 down to rank 0, one key at a time.
+ *   v [n][d] (position-indexed), c [n] fp64 out, c32 [n] fp32 out (either
+ *   may be NULL). */
+int ora_curves(int64_t n, int32_t d, const float* s32, const int32_t* perm,
+               const double* v, double* c, float* c32) {
+  if (n <= 0 || d <= 0) return ORA_EINVAL;
+  double* a = (double*)malloc(sizeof(double) * (size_t)n);
+  double* W = (double*)calloc((size_t)d, sizeof(double));
+  if (!a || !W) {
+    free(a);
+    free(W);
+    return ORA_ENOMEM;
+  }
+  int st = ora_normalize(n, s32, a);
+  if (st != ORA_OK) {
+    free(a);
+    free(W);
+    return st;
+  }
+  double m = 0.0, Q = 0.0;
+  for (int64_t b = n - 1; b >= 0; --b) {
+    int32_t j = perm[b];
+    const double* vj = v + (size_t)j * d;
+    double vv = 0.0;
+    for (int32_t t = 0; t < d; ++t) vv += vj[t] * vj[t];
+    m += a[j];
+    Q += a[j] * vv;
+    for (int32_t t = 0; t < d; ++t) W[t] += a[j] * vj[t];
+    double w2 = 0.0;
+    for (int32_t t = 0; t < d; ++t) w2 += W[t] * W[t];
+    double c2 = m * Q - w2;
+    double cb = sqrt(c2 > 0.0 ? c2 : 0.0);
+    if (c) c[b] = cb;
+    if (c32) c32[b] = (float)cb;
+  }
+  free(a);
+  free(W);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exact slot accounting, Section 4.1 and the appendix: with n_keep live
+ * slots per head, B_live = H n_keep, B_real = B_live - H, b_min =
+ * max{1, floor(alpha B_real / H)}; feasible iff 2 <= n_keep <= n. */
+int ora_budget_params(int32_t H, int64_t n, int64_t n_keep, double alpha,
+                      int64_t* B_real, int64_t* b_min) {
+  if (H <= 0 || n <= 0) return ORA_EINVAL;
+  if (n_keep < 2 || n_keep > n) return ORA_EINFEASIBLE;
+  int64_t br = (int64_t)H * n_keep - H;
+  int64_t bm = (int64_t)floor(alpha * (double)br / (double)H);
+  if (bm < 1) bm = 1;
+  if (bm > n - 1 || (int64_t)H * bm > br) return ORA_EINFEASIBLE;
+  *B_real = br;
+  *b_min = bm;
+  return ORA_OK;
+}
+
+/* argmin over b in [lo, hi] of fma(lam, b, c(b)), smallest b on ties. */
+int64_t ora_argmin_penalized(const float* c32, int64_t lo, int64_t hi,
+                             double lam) {
+  int64_t best = lo;
+  double bestv = fma(lam, (double)lo, (double)c32[lo]);
+  for (int64_t b = lo + 1; b <= hi; ++b) {
+    double f = fma(lam, (double)b, (double)c32[b]);
+    if (f < bestv) {
+      bestv = f;
+      best = b;
+    }
+  }
+  return best;
+}
+
+/* Allocation, Algorithm 1: lambda bisection on the shared multiplier for T
+ * steps, b_h = b_h(lambda_hi), then one-token best-marginal repair until
+ * sum b_h = B_real.
+ *   c32 [H][n] fp32 curves; b [H] out; repairs (may be NULL) out;
+ *   lam (may be NULL) out: the final {lambda_lo, lambda_hi}. */
+int ora_allocate(int32_t H, int64_t n, const float* c32, int64_t n_keep,
+                 double alpha, int32_t T, int32_t* b, int64_t* repairs,
+                 double* lam) {
+  int64_t B_real, b_min;
+  int st = ora_budget_params(H, n, n_keep, alpha, &B_real, &b_min);
+  if (st != ORA_OK) return st;
+  double cmax = 0.0;
+  for (int32_t h = 0; h < H; ++h)
+    for (int64_t j = 0; j < n; ++j) {
+      double cj = (double)c32[(size_t)h * n + j];
+      if (!isfinite(cj)) return ORA_ENONFINITE;
+      if (cj > cmax) cmax = cj;
+    }
+  double lo = 0.0, hi = 2.0 * cmax + 1.0;
+  int64_t* bl = (int64_t*)malloc(sizeof(int64_t) * (size_t)H);
+  int64_t* bh = (int64_t*)malloc(sizeof(int64_t) * (size_t)H);
+  if (!bl || !bh) {
+    free(bl);
+    free(bh);
+    return ORA_ENOMEM;
+  }
+  for (int32_t h = 0; h < H; ++h)
+    bh[h] = ora_argmin_penalized(c32 + (size_t)h * n, b_min, n - 1, hi);
+  for (int32_t t = 0; t < T; ++t) {
+    double lam = (lo + hi) / 2.0;
+    int64_t sum = 0;
+    for (int32_t h = 0; h < H; ++h) {
+      bl[h] = ora_argmin_penalized(c32 + (size_t)h * n, b_min, n - 1, lam);
+      sum += bl[h];
+    }
+    if (sum > B_real) {
+      lo = lam;
+    } else {
+      hi = lam;
+      for (int32_t h = 0; h < H; ++h) bh[h] = bl[h];
+    }
+  }
+  int64_t sum = 0, nrep = 0;
+  for (int32_t h = 0; h < H; ++h) sum += bh[h];
+  while (sum < B_real) {
+    int32_t best = -1;
+    double bestd = 0.0;
+    for (int32_t h = 0; h < H; ++h) {
+      if (bh[h] >= n - 1) continue;
+      const float* ch = c32 + (size_t)h * n;
+      double dl = (double)ch[bh[h] + 1] - (double)ch[bh[h]];
+      if (best < 0 || dl < bestd) {
+        best = h;
+        bestd = dl;
+      }
+    }
+    if (best < 0) break; /* cannot happen: B_real <= H (n-1) */
+    bh[best] += 1;
+    sum += 1;
+    ++nrep;
+  }
+  while (sum > B_real) {
+    int32_t best = -1;
+    double bestd = 0.0;
+    for (int32_t h = 0; h < H; ++h) {
+      if (bh[h] <= b_min) continue;
+      const float* ch = c32 + (size_t)h * n;
+      double dl = (double)ch[bh[h] - 1] - (double)ch[bh[h]];
+      if (best < 0 || dl < bestd) {
+        best = h;
+        bestd = dl;
+      }
+    }
+    if (best < 0) break; /* cannot happen: H b_min <= B_real */
+    bh[best] -= 1;
+    sum -= 1;
+    ++nrep;
+  }
+  for (int32_t h = 0; h < H; ++h) b[h] = (int32_t)bh[h];
+  if (repairs) *repairs = nrep;
+  if (lam) {
+    lam[0] = lo;
+    lam[1] = hi;
+  }
+  free(bl);
+  free(bh);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Selection, Algorithm 1 return step: the b top-ranked keys, listed by
+ * ascending position.  kept [b] out. */
+int ora_select(int64_t n, const int32_t* perm, int64_t b, int32_t* kept) {
+  if (b < 0 || b > n) return ORA_EINVAL;
+  unsigned char* mark = (unsigned char*)calloc((size_t)n, 1);
+  if (!mark) return ORA_ENOMEM;
+  for (int64_t r = 0; r < b; ++r) mark[perm[r]] = 1;
+  int64_t o = 0;
+  for (int64_t j = 0; j < n; ++j)
+    if (mark[j]) kept[o++] = (int32_t)j;
+  free(mark);
+  return ORA_OK;
+}
+
+/* Coverage budget, Section 3 Eq. coverage-def with retained fraction
+ * retain = 1 - eta: the smallest k >= 1 whose top-k mass sum_{r<=k} a_(r),
+ * summed in rank order, reaches retain; n if it never does. */
+int ora_coverage(int64_t n, const float* s32, const int32_t* perm,
+                 double retain, int64_t* k_eta) {
+  double* a = (double*)malloc(sizeof(double) * (size_t)n);
+  if (!a) return ORA_ENOMEM;
+  int st = ora_normalize(n, s32, a);
+  if (st != ORA_OK) {
+    free(a);
+    return st;
+  }
+  double p = 0.0;
+  int64_t k = n;
+  for (int64_t r = 0; r < n; ++r) {
+    p += a[perm[r]];
+    if (p >= retain) {
+      k = r + 1;
+      break;
+    }
+  }
+  *k_eta = k;
+  free(a);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Tail summary, Section 4.1: with r_j = a_j / m over the evicted set E,
+ * (k*, v*) = E_{j~r}[(k_j, v_j)] and m = sum_E a_j; m = 0 gives zero
+ * vectors (appendix, centered-moment envelope: v* = 0 when m = 0).
+ *   kept [b] ascending positions; k, v [n][d]; kstar, vstar [d] out. */
+int ora_tail(int64_t n, int32_t d, const float* s32, const int32_t* kept,
+             int64_t b, const double* k, const double* v, double* kstar,
+             double* vstar, double* m_out) {
+  double* a = (double*)malloc(sizeof(double) * (size_t)n);
+  unsigned char* mark = (unsigned char*)calloc((size_t)n, 1);
+  if (!a || !mark) {
+    free(a);
+    free(mark);
+    return ORA_ENOMEM;
+  }
+  int st = ora_normalize(n, s32, a);
+  if (st != ORA_OK) {
+    free(a);
+    free(mark);
+    return st;
+  }
+  for (int64_t i = 0; i < b; ++i) mark[kept[i]] = 1;
+  double m = 0.0;
+  for (int32_t t = 0; t < d; ++t) kstar[t] = vstar[t] = 0.0;
+  for (int64_t j = 0; j < n; ++j) {
+    if (mark[j]) continue;
+    m += a[j];
+    for (int32_t t = 0; t < d; ++t) {
+      kstar[t] += a[j] * k[(size_t)j * d + t];
+      vstar[t] += a[j] * v[(size_t)j * d + t];
+    }
+  }
+  for (int32_t t = 0; t < d; ++t) {
+    kstar[t] = m > 0.0 ? kstar[t] / m : 0.0;
+    vstar[t] = m > 0.0 ? vstar[t] / m : 0.0;
+  }
+  *m_out = m;
+  free(a);
+  free(mark);
+  return ORA_OK;
+}
+
+/* Round an fp32 value to bfloat16, round-to-nearest-even (IEEE 754
+ * binary32 -> the upper 16 bits), NaN kept quiet. */
+uint16_t ora_f32_to_bf16(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
+    return (uint16_t)((u >> 16) | 0x0040u);
+  uint32_t lsb = (u >> 16) & 1u;
+  u += 0x7fffu + lsb;
+  return (uint16_t)(u >> 16);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Output-error helpers (Section 3.2, Theorem "fixed-row tail
+ * factorization"; the worked examples of the oracle-subset and proxy
+ * sections of the appendix use the same quantities).
+ * For one realized row with weights A [n] and values V [n][d], a kept mask,
+ * and a compensation vector u [d] (NULL = none):
+ *   err = | sum_{j kept} A_j V_j + u - sum_j A_j V_j |_2.               */
+double ora_row_error(int64_t n, int32_t d, const double* A, const double* V,
+                     const unsigned char* kept, const double* u) {
+  double acc2 = 0.0;
+  for (int32_t t = 0; t < d; ++t) {
+    double full = 0.0, part = 0.0;
+    for (int64_t j = 0; j < n; ++j) {
+      full += A[j] * V[(size_t)j * d + t];
+      if (kept[j]) part += A[j] * V[(size_t)j * d + t];
+    }
+    double e = part + (u ? u[t] : 0.0) - full;
+    acc2 += e * e;
+  }
+  return sqrt(acc2);
+}
+
+/* ------------------------------------------------------------------------ */
+/* One (layer, sequence) block end to end: every KV head through score, order,
+ * curves, allocation, selection and tail, heads in parallel (OpenMP) where a
+ * stage is per head.  Inputs already in fp64.
+ *   q      [w][H*G][d]   window rows of this sequence
+ *   k, v   [n][H][d]
+ *   s      [H][n] fp64 out; s32 [H][n] fp32 out (the shared scores)
+ *   perm   [H][n] out; c32 [H][n] out; b [H] out
+ *   kept   [H*n] out, unit h's run at kept_off[h]; kept_off [H+1] out
+ *   kstar, vstar [H][d] out; m [H] out
+ * When s32_in is not NULL the scoring step is skipped and those fp32 scores
+ * are used instead (stage parity: the oracle fed the GPU's scores). */
+int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
+                       const double* q, const double* k, const double* v,
+                       double scale, int32_t causal, int64_t n_keep,
+                       double alpha, int32_t T, const float* s32_in,
+                       double* s, float* s32, int32_t* perm, float* c32,
+                       int32_t* b, int32_t* kept, int64_t* kept_off,
+                       double* kstar, double* vstar, double* m,
+                       int64_t* repairs) {
+  if (w > n || w <= 0) return ORA_EINVAL;
+  int32_t M = w * G;
+  int err = ORA_OK;
+  int64_t B_real, b_min;
+  int st = ora_budget_params(H, n, n_keep, alpha, &B_real, &b_min);
+  if (st != ORA_OK) return st;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t h = 0; h < H; ++h) {
+    int lerr = ORA_OK;
+    double* kh = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* vh = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* qh = (double*)malloc(sizeof(double) * (size_t)M * d);
+    int64_t* qpos = (int64_t*)malloc(sizeof(int64_t) * (size_t)M);
+    if (!kh || !vh || !qh || !qpos) lerr = ORA_ENOMEM;
+    if (lerr == ORA_OK) {
+      for (int64_t j = 0; j < n; ++j)
+        for (int32_t t = 0; t < d; ++t) {
+          kh[(size_t)j * d + t] = k[((size_t)j * H + h) * d + t];
+          vh[(size_t)j * d + t] = v[((size_t)j * H + h) * d + t];
+        }
+      for (int32_t r = 0; r < w; ++r)
+        for (int32_t g = 0; g < G; ++g) {
+          int32_t row = r * G + g;
+          qpos[row] = n - w + r;
+          for (int32_t t = 0; t < d; ++t)
+            qh[(size_t)row * d + t] =
+                q[((size_t)r * H * G + (size_t)h * G + g) * d + t];
+        }
+      if (s32_in) {
+        for (int64_t j = 0; j < n; ++j) {
+          s32[(size_t)h * n + j] = s32_in[(size_t)h * n + j];
+          s[(size_t)h * n + j] = (double)s32_in[(size_t)h * n + j];
+        }
+      } else {
+        lerr = ora_scores(n, d, M, qh, qpos, kh, scale, causal,
+                          s + (size_t)h * n, NULL);
+        for (int64_t j = 0; j < n; ++j)
+          s32[(size_t)h * n + j] = (float)s[(size_t)h * n + j];
+      }
+    }
+    if (lerr == ORA_OK)
+      lerr = ora_order(n, s32 + (size_t)h * n, perm + (size_t)h * n);
+    if (lerr == ORA_OK)
+      lerr = ora_curves(n, d, s32 + (size_t)h * n, perm + (size_t)h * n, vh,
+                        NULL, c32 + (size_t)h * n);
+    free(kh);
+    free(vh);
+    free(qh);
+    free(qpos);
+    if (lerr != ORA_OK) {
+#pragma omp critical(ora_err)
+      err = lerr;
+    }
+  }
+  if (err != ORA_OK) return err;
+  err = ora_allocate(H, n, c32, n_keep, alpha, T, b, repairs, NULL);
+  if (err != ORA_OK) return err;
+  kept_off[0] = 0;
+  for (int32_t h = 0; h < H; ++h) kept_off[h + 1] = kept_off[h] + b[h];
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int32_t h = 0; h < H; ++h) {
+    int lerr = ora_select(n, perm + (size_t)h * n, b[h], kept + kept_off[h]);
+    double* kh = (double*)malloc(sizeof(double) * (size_t)n * d);
+    double* vh = (double*)malloc(sizeof(double) * (size_t)n * d);
+    if (!kh || !vh) lerr = ORA_ENOMEM;
+    if (lerr == ORA_OK) {
+      for (int64_t j = 0; j < n; ++j)
+        for (int32_t t = 0; t < d; ++t) {
+          kh[(size_t)j * d + t] = k[((size_t)j * H + h) * d + t];
+          vh[(size_t)j * d + t] = v[((size_t)j * H + h) * d + t];
+        }
+      lerr = ora_tail(n, d, s32 + (size_t)h * n, kept + kept_off[h], b[h], kh,
+                      vh, kstar + (size_t)h * d, vstar + (size_t)h * d, m + h);
+    }
+    free(kh);
+    free(vh);
+    if (lerr != ORA_OK) {
+#pragma omp critical(ora_err)
+      err = lerr;
+    }
+  }
+  return err;
+}
+
+int ora_num_threads(void) {
+#ifdef _OPENMP
+  extern int omp_get_max_threads(void);
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
