@@ -186,7 +186,7 @@ certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win,
  * smallest b among equal minima. */
 certkv_status certkv_allocate(const certkv_problem* p, const float* scores,
                               certkv_tensor v, const int32_t* n_keep_host,
-                              float alpha, int32_t steps, int32_t* budgets,
+                              double alpha, int32_t steps, int32_t* budgets,
                               int32_t* perm, float* curves, double* vsum,
                               void* ws, size_t ws_bytes, void* stream);
 
@@ -196,7 +196,7 @@ certkv_status certkv_allocate(const certkv_problem* p, const float* scores,
  * very same curves. */
 certkv_status certkv_allocate_curves(const certkv_problem* p,
                                      const float* curves,
-                                     const int32_t* n_keep_host, float alpha,
+                                     const int32_t* n_keep_host, double alpha,
                                      int32_t steps, int32_t* budgets, void* ws,
                                      size_t ws_bytes, void* stream);
 
@@ -253,7 +253,7 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k,
  * with one workspace of certkv_workspace_size(p, CERTKV_STAGE_COMPRESS). */
 certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
                               certkv_tensor k, certkv_tensor v,
-                              const int32_t* n_keep_host, float alpha,
+                              const int32_t* n_keep_host, double alpha,
                               int32_t steps, const certkv_outputs* out,
                               void* ws, size_t ws_bytes, void* stream);
 

@@ -1,0 +1,212 @@
+// Kept-key selection: threshold on the score order plus ballot compaction.
+//
+// The top-b keys of a unit (score descending, ties by position) are exactly
+// the keys whose (radix key, position) pair is lexicographically <= the pair
+// at rank b-1 of the sort.  One workgroup streams the unit's scores in
+// position order, tests each key against that threshold, and compacts the
+// kept positions with wave ballots and a 4-wave prefix, so kept indices come
+// out ascending without a scatter.  The same pass sums (s)_+ over the evicted
+// keys and over all keys in fp64 (the tail mass and its normalizer).
+#include "stages.h"
+
+namespace certkv {
+
+// budgets clamped to [0, n_b] (caller-supplied budgets in selection mode)
+__global__ void clamp_budgets_kernel(Geo g, SeqTab st, int32_t* __restrict__ budgets) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int per_layer = st.count * g.H;
+  if (i >= per_layer * g.L) return;
+  const int l = i / per_layer, r = i % per_layer;
+  const int bl = r / g.H, h = r % g.H;
+  const int64_t u = unit_index(g, l, st.first + bl, h);
+  int32_t b = budgets[u];
+  b = b < 0 ? 0 : (b > st.len[bl] ? st.len[bl] : b);
+  budgets[u] = b;
+}
+
+// Exclusive prefix over all units of the budgets -> kept_offsets[U+1];
+// packed_offsets[u] = kept_offsets[u] + u (one slot row per unit).
+__global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, const int32_t* __restrict__ budgets,
+                                                       int64_t* __restrict__ kept_offsets,
+                                                       int64_t* __restrict__ packed_offsets) {
+  __shared__ int64_t wsum[16];
+  __shared__ int64_t carry;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int64_t base = 0; base < U; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    int64_t v = i < U ? (int64_t)budgets[i] : 0;
+    int64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      int64_t y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int64_t before = carry;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    if (i < U) {
+      kept_offsets[i] = before + incl - v;
+      if (packed_offsets) packed_offsets[i] = before + incl - v + i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 1023) carry = before + incl;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    kept_offsets[U] = carry;
+    if (packed_offsets) packed_offsets[U] = carry + U;
+  }
+}
+
+__global__ __launch_bounds__(256) void select_kernel(
+    Geo g, SeqTab st, const float* __restrict__ scores, const uint32_t* __restrict__ sorted_keys,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ budgets,
+    const int64_t* __restrict__ kept_offsets, int32_t* __restrict__ kept_idx, int64_t capacity,
+    double* __restrict__ evicted_sum, double* __restrict__ total_sum) {
+  __shared__ int32_t wcount[4];
+  __shared__ double dsum[2][4];
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int n = st.len[bl];
+  const int64_t base = lht_base(g, l, h, st.start[bl]);
+  const int64_t u = unit_index(g, l, b, h);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int bb = budgets[u];
+  uint32_t kthr = 0u;
+  int32_t ithr = -1;  // keep nothing when bb == 0
+  if (bb > 0 && bb <= n) {
+    kthr = sorted_keys[base + bb - 1];
+    ithr = perm[base + bb - 1];
+  }
+  const int64_t off = kept_offsets[u];
+  int64_t run = 0;
+  double se = 0.0, sa = 0.0;
+  for (int j0 = 0; j0 < n; j0 += 256) {
+    const int j = j0 + threadIdx.x;
+    const bool valid = j < n;
+    const float s = valid ? scores[base + j] : 0.f;
+    const uint32_t key = desc_key(s);
+    const bool keep = valid && (key < kthr || (key == kthr && j <= ithr));
+    if (valid) {
+      const double sp = s > 0.f ? (double)s : 0.0;
+      sa += sp;
+      if (!keep) se += sp;
+    }
+    const uint64_t bal = __ballot(keep);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    if (lane == 0) wcount[wave] = __popcll(bal);
+    __syncthreads();
+    int64_t pre = run;
+    for (int w = 0; w < wave; ++w) pre += wcount[w];
+    const int64_t dst = off + pre + below;
+    if (keep && dst < capacity) kept_idx[dst] = j;
+    run += wcount[0] + wcount[1] + wcount[2] + wcount[3];
+    __syncthreads();
+  }
+  se = wave_sum(se);
+  sa = wave_sum(sa);
+  if (lane == 0) {
+    dsum[0][wave] = se;
+    dsum[1][wave] = sa;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (evicted_sum) evicted_sum[u] = dsum[0][0] + dsum[0][1] + dsum[0][2] + dsum[0][3];
+    if (total_sum) total_sum[u] = dsum[1][0] + dsum[1][1] + dsum[1][2] + dsum[1][3];
+  }
+}
+
+// Coverage budget k_eta: the normalizer sum (s)_+ in position order, then the
+// rank-order prefix of a = (s)_+ / sum until it reaches retain, both summed
+// one term at a time in fp64 (one wave per unit, uniform accumulators).
+__global__ __launch_bounds__(64) void coverage_kernel(Geo g, SeqTab st, const float* __restrict__ scores,
+                                                      const uint32_t* __restrict__ sorted_keys,
+                                                      double retain, int32_t* __restrict__ budgets) {
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int n = st.len[bl];
+  const int64_t base = lht_base(g, l, h, st.start[bl]);
+  const int lane = threadIdx.x;
+  double tot = 0.0;
+  for (int j0 = 0; j0 < n; j0 += 64) {
+    const int j = j0 + lane;
+    const float s = j < n ? scores[base + j] : 0.f;
+    const double sp = s > 0.f ? (double)s : 0.0;
+    const int cnt = min(64, n - j0);
+    for (int i = 0; i < cnt; ++i) tot += __shfl(sp, i, 64);
+  }
+  const double inv_n = 1.0 / (double)n;
+  double p = 0.0;
+  int k = n;
+  bool done = false;
+  for (int r0 = 0; r0 < n && !done; r0 += 64) {
+    const int r = r0 + lane;
+    const float s = r < n ? desc_key_value(sorted_keys[base + r]) : 0.f;
+    const double a = tot > 0.0 ? (s > 0.f ? (double)s / tot : 0.0) : inv_n;
+    const int cnt = min(64, n - r0);
+    for (int i = 0; i < cnt; ++i) {
+      p += __shfl(a, i, 64);
+      if (p >= retain) {
+        k = r0 + i + 1;
+        done = true;
+        break;
+      }
+    }
+  }
+  if (lane == 0) budgets[unit_index(g, l, b, h)] = k;
+}
+
+
+certkv_status run_coverage(const Geo& g, const SeqTab& st, const float* scores,
+                           const uint32_t* sorted_keys, double retain, int32_t* budgets,
+                           hipStream_t s) {
+  CERTKV_LAUNCH("coverage_budget", coverage_kernel, dim3(g.H * st.count, g.L), dim3(64), 0, s, g, st,
+                scores, sorted_keys, retain, budgets);
+  return CERTKV_OK;
+}
+
+certkv_status run_clamp(const Geo& g, const SeqTab& st, int32_t* budgets, hipStream_t s) {
+  const int total = st.count * g.H * g.L;
+  CERTKV_LAUNCH("clamp_budgets", clamp_budgets_kernel, dim3((total + 255) / 256), dim3(256), 0, s, g,
+                st, budgets);
+  return CERTKV_OK;
+}
+
+certkv_status run_offsets(int64_t U, const int32_t* budgets, int64_t* kept_offsets,
+                          int64_t* packed_offsets, hipStream_t s) {
+  CERTKV_LAUNCH("kept_offsets", offsets_kernel, dim3(1), dim3(1024), 0, s, U, budgets, kept_offsets,
+                packed_offsets);
+  return CERTKV_OK;
+}
+
+__global__ void packed_from_kept_kernel(int64_t U, const int64_t* __restrict__ kept_offsets,
+                                        int64_t* __restrict__ packed_offsets) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= U) packed_offsets[i] = kept_offsets[i] + i;
+}
+
+certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64_t* packed_offsets,
+                                   hipStream_t s) {
+  CERTKV_LAUNCH("packed_offsets", packed_from_kept_kernel, dim3((unsigned)((U + 256) / 256)),
+                dim3(256), 0, s, U, kept_offsets, packed_offsets);
+  return CERTKV_OK;
+}
+
+certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s) {
+  CERTKV_LAUNCH("select", select_kernel, dim3(a.g.H * st.count, a.g.L), dim3(256), 0, s, a.g, st,
+                a.scores, a.sorted_keys, a.perm, (const int32_t*)a.budgets,
+                (const int64_t*)a.kept_offsets, a.kept_idx, a.capacity, a.evicted_sum, a.total_sum);
+  return CERTKV_OK;
+}
+
+}  // namespace certkv

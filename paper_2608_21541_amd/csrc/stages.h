@@ -1,0 +1,107 @@
+// Argument blocks and host launchers of the kernel stages (internal).
+#pragma once
+
+#include "common.h"
+
+namespace certkv {
+
+struct ScoreArgs {
+  Geo g;
+  certkv_tensor q, k;
+  int32_t dtype;
+  float* scores;
+  double* ksum;
+  float2* part;
+  float* lse2;
+  float* kpart;
+  int32_t keys_per_block;
+  int32_t nkb_max;
+};
+certkv_status run_score(const ScoreArgs& a, const SeqTab& st, int max_len, hipStream_t s);
+
+struct SortArgs {
+  Geo g;
+  const float* scores;
+  uint32_t *keysA, *keysB, *keys_out;
+  int32_t *valsA, *valsB, *perm_out;
+  double* ssum;
+};
+certkv_status run_sort(const SortArgs& a, const SeqTab& st, hipStream_t s);
+
+struct CurveArgs {
+  Geo g;
+  const uint32_t* sorted_keys;
+  const int32_t* perm;
+  const double* ssum;
+  certkv_tensor v;
+  int32_t dtype;
+  float* curves;
+  float* cmin;
+  int32_t cmin_stride;
+  float* cmax;
+  double* vsum;
+};
+certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s);
+
+struct AllocArgs {
+  Geo g;
+  const float* curves;
+  float* cmin;
+  int32_t cmin_stride;
+  float* cmax;
+  int32_t steps;
+  int32_t* budgets;
+  int64_t* repairs;
+  bool need_minmax;
+};
+certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s);
+
+struct SelectArgs {
+  Geo g;
+  const float* scores;
+  const uint32_t* sorted_keys;
+  const int32_t* perm;
+  int32_t* budgets;
+  int64_t* kept_offsets;
+  int64_t* packed_offsets;
+  int32_t* kept_idx;
+  int64_t capacity;
+  double* evicted_sum;
+  double* total_sum;
+};
+certkv_status run_coverage(const Geo& g, const SeqTab& st, const float* scores,
+                           const uint32_t* sorted_keys, double retain, int32_t* budgets,
+                           hipStream_t s);
+certkv_status run_clamp(const Geo& g, const SeqTab& st, int32_t* budgets, hipStream_t s);
+certkv_status run_offsets(int64_t U, const int32_t* budgets, int64_t* kept_offsets,
+                          int64_t* packed_offsets, hipStream_t s);
+certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s);
+
+struct TailArgs {
+  Geo g;
+  int32_t dtype;
+  const float* scores;
+  certkv_tensor k, v;
+  const int64_t* kept_offsets;
+  const int32_t* kept_idx;
+  uint64_t* bitmap;
+  int32_t bm_stride;
+  bool build_bitmap;
+  const double* ksum;
+  const double* vsum;
+  float* k_star;
+  float* v_star;
+  double* tail_mass;
+  void* k_packed;
+  void* v_packed;
+  int32_t* pos_packed;
+  bool do_tail, do_compact;
+};
+certkv_status run_bitmap(const TailArgs& a, const SeqTab& st, int64_t words_total, bool clear,
+                         hipStream_t s);
+certkv_status run_tail(const TailArgs& a, const SeqTab& st, hipStream_t s);
+size_t score_smem_bytes(const Geo& g, int32_t dtype);
+
+certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64_t* packed_offsets,
+                                   hipStream_t s);
+}  // namespace certkv

@@ -1,0 +1,254 @@
+// Tail-summary slot and packed-cache compaction.
+//
+// Per unit (one workgroup) the evicted set E is the complement of the kept
+// positions (a bitmap).  The slot is the (s)_+-weighted key and value centroid
+// of E; the weights' normalizer cancels, so
+//   k* = sum_E s_j k_j / sum_E s_j,  v* likewise,  m = sum_E s_j / sum_j s_j.
+// When the totals sum_j s_j k_j and sum_j s_j v_j are already known (from the
+// scoring and curve kernels), the evicted sums are formed as total minus kept,
+// so only the ~f*n kept rows are read; if the evicted mass is below 1/64 of
+// the total the kernel sums the evicted rows directly instead (cancellation
+// guard).  Compaction copies the kept rows (already being read) to the packed
+// cache in ascending position and appends the slot row.
+#include "stages.h"
+
+namespace certkv {
+
+constexpr int kTailThreads = 256;
+constexpr double kComplementMinMass = 1.0 / 64.0;
+
+template <typename T>
+__device__ __forceinline__ float elem_f32(const uint4& q, int e);
+template <>
+__device__ __forceinline__ float elem_f32<uint16_t>(const uint4& q, int e) {
+  const uint32_t w = (&q.x)[e >> 1];
+  return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+}
+template <>
+__device__ __forceinline__ float elem_f32<float>(const uint4& q, int e) {
+  return __uint_as_float((&q.x)[e]);
+}
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f32_to_bf16_rne(x); }
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+
+// Clear the per-unit kept bitmaps, then set one bit per kept position.
+__global__ void bitmap_clear_kernel(uint64_t* __restrict__ bm, int64_t words) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < words) bm[i] = 0ull;
+}
+
+__global__ void bitmap_set_kernel(Geo g, SeqTab st, const int64_t* __restrict__ kept_offsets,
+                                  const int32_t* __restrict__ kept_idx, uint64_t* __restrict__ bm,
+                                  int32_t bm_stride) {
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int n = st.len[bl];
+  const int64_t u = unit_index(g, l, st.first + bl, h);
+  const int64_t o0 = kept_offsets[u], o1 = kept_offsets[u + 1];
+  for (int64_t i = o0 + threadIdx.x; i < o1; i += blockDim.x) {
+    const int j = kept_idx[i];
+    if (j >= 0 && j < n)
+      atomicOr(reinterpret_cast<unsigned long long*>(&bm[u * bm_stride + (j >> 6)]),
+               1ull << (j & 63));
+  }
+}
+
+template <int D, typename T, bool DO_TAIL, bool DO_COMPACT>
+__global__ __launch_bounds__(kTailThreads) void tail_compact_kernel(
+    Geo g, SeqTab st, const float* __restrict__ scores, const T* __restrict__ kc, int64_t k_sl,
+    int64_t k_st, int64_t k_sh, const T* __restrict__ vc, int64_t v_sl, int64_t v_st, int64_t v_sh,
+    const int64_t* __restrict__ kept_offsets, const int32_t* __restrict__ kept_idx,
+    const uint64_t* __restrict__ bm, int32_t bm_stride, const double* __restrict__ ksum,
+    const double* __restrict__ vsum, float* __restrict__ k_star, float* __restrict__ v_star,
+    double* __restrict__ tail_mass, T* __restrict__ k_packed, T* __restrict__ v_packed,
+    int32_t* __restrict__ pos_packed) {
+  constexpr int EPL = 16 / sizeof(T);          // elements per 16-byte lane chunk
+  constexpr int LPR = D / EPL;                 // lanes per row
+  constexpr int RPS = kTailThreads / LPR;      // rows per workgroup step
+  __shared__ double redk[RPS][D];
+  __shared__ double redv[RPS][D];
+  __shared__ double dsum[2][kTailThreads / 64];
+  __shared__ float slot_k[D], slot_v[D];
+  __shared__ int use_direct;
+
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int n = st.len[bl];
+  const int64_t tok0 = st.start[bl];
+  const int64_t sbase = lht_base(g, l, h, tok0);
+  const int64_t u = unit_index(g, l, b, h);
+  const int tid = threadIdx.x;
+  const int ri = tid / LPR, ci = tid % LPR;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int64_t off = kept_offsets[u];
+  const int nk = (int)(kept_offsets[u + 1] - off);
+  const int64_t poff = off + u;  // packed segment start
+  const T* kb = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
+  const T* vb = vc + (int64_t)l * v_sl + tok0 * v_st + (int64_t)h * v_sh;
+  const uint64_t* bmu = bm + u * bm_stride;
+
+  // Evicted and total mass, in fp64.
+  double S_all = 0.0, S_E = 0.0;
+  bool uniform_w = false;
+  if (DO_TAIL) {
+    double sa = 0.0, se = 0.0, ne = 0.0;
+    for (int j = tid; j < n; j += kTailThreads) {
+      const float s = scores[sbase + j];
+      const double sp = s > 0.f ? (double)s : 0.0;
+      const bool ev = !((bmu[j >> 6] >> (j & 63)) & 1ull);
+      sa += sp;
+      if (ev) {
+        se += sp;
+        ne += 1.0;
+      }
+    }
+    sa = wave_sum(sa);
+    se = wave_sum(se);
+    ne = wave_sum(ne);
+    if (lane == 0) {
+      dsum[0][wave] = sa;
+      dsum[1][wave] = se;
+      redk[0][wave] = ne;  // scratch (overwritten below)
+    }
+    __syncthreads();
+    S_all = dsum[0][0] + dsum[0][1] + dsum[0][2] + dsum[0][3];
+    S_E = dsum[1][0] + dsum[1][1] + dsum[1][2] + dsum[1][3];
+    uniform_w = S_all <= 0.0;
+    if (uniform_w) {  // every score zero: uniform weights
+      S_all = (double)n;
+      S_E = redk[0][0] + redk[0][1] + redk[0][2] + redk[0][3];
+    }
+    if (tid == 0)
+      use_direct = uniform_w || !(ksum && vsum && S_E >= kComplementMinMass * S_all);
+    __syncthreads();
+  }
+
+  // Kept rows: copy (compaction) and accumulate (complement form).
+  double ak[EPL], av[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) ak[e] = av[e] = 0.0;
+  const bool comp_acc = DO_TAIL && !use_direct;
+  for (int i = ri; i < nk; i += RPS) {
+    const int j = min(max(kept_idx[off + i], 0), n - 1);  // caller-supplied indices clamped
+    const uint4 kq = *reinterpret_cast<const uint4*>(kb + (int64_t)j * k_st + ci * EPL);
+    const uint4 vq = *reinterpret_cast<const uint4*>(vb + (int64_t)j * v_st + ci * EPL);
+    if (DO_COMPACT) {
+      *reinterpret_cast<uint4*>(k_packed + (poff + i) * D + ci * EPL) = kq;
+      *reinterpret_cast<uint4*>(v_packed + (poff + i) * D + ci * EPL) = vq;
+      if (ci == 0) pos_packed[poff + i] = j;
+    }
+    if (comp_acc) {
+      const float s = scores[sbase + j];
+      const double w = uniform_w ? 1.0 : (s > 0.f ? (double)s : 0.0);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        ak[e] = fma(w, (double)elem_f32<T>(kq, e), ak[e]);
+        av[e] = fma(w, (double)elem_f32<T>(vq, e), av[e]);
+      }
+    }
+  }
+  if (DO_TAIL && use_direct) {
+    // Direct weighted sums over the evicted rows.
+    for (int j = ri; j < n; j += RPS) {
+      if ((bmu[j >> 6] >> (j & 63)) & 1ull) continue;
+      const float s = scores[sbase + j];
+      const double w = uniform_w ? 1.0 : (s > 0.f ? (double)s : 0.0);
+      if (w == 0.0) continue;
+      const uint4 kq = *reinterpret_cast<const uint4*>(kb + (int64_t)j * k_st + ci * EPL);
+      const uint4 vq = *reinterpret_cast<const uint4*>(vb + (int64_t)j * v_st + ci * EPL);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        ak[e] = fma(w, (double)elem_f32<T>(kq, e), ak[e]);
+        av[e] = fma(w, (double)elem_f32<T>(vq, e), av[e]);
+      }
+    }
+  }
+  if (DO_TAIL) {
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      redk[ri][ci * EPL + e] = ak[e];
+      redv[ri][ci * EPL + e] = av[e];
+    }
+    __syncthreads();
+    for (int d = tid; d < D; d += kTailThreads) {
+      double sk = 0.0, sv = 0.0;
+      for (int r = 0; r < RPS; ++r) {
+        sk += redk[r][d];
+        sv += redv[r][d];
+      }
+      double nk_ = use_direct ? sk : ksum[u * D + d] - sk;
+      double nv_ = use_direct ? sv : vsum[u * D + d] - sv;
+      const float ks = S_E > 0.0 ? (float)(nk_ / S_E) : 0.f;
+      const float vs = S_E > 0.0 ? (float)(nv_ / S_E) : 0.f;
+      k_star[u * D + d] = ks;
+      v_star[u * D + d] = vs;
+      slot_k[d] = ks;
+      slot_v[d] = vs;
+    }
+    if (tid == 0) tail_mass[u] = S_E / S_all;
+    __syncthreads();
+  } else if (DO_COMPACT) {
+    for (int d = tid; d < D; d += kTailThreads) {
+      slot_k[d] = k_star[u * D + d];
+      slot_v[d] = v_star[u * D + d];
+    }
+    __syncthreads();
+  }
+  if (DO_COMPACT) {
+    const int64_t prow = poff + nk;
+    for (int d = tid; d < D; d += kTailThreads) {
+      k_packed[prow * D + d] = from_f32<T>(slot_k[d]);
+      v_packed[prow * D + d] = from_f32<T>(slot_v[d]);
+    }
+    if (tid == 0) pos_packed[prow] = -1;
+  }
+}
+
+
+template <int D, typename T, bool DT, bool DC>
+static certkv_status launch_tail(const TailArgs& a, const SeqTab& st, hipStream_t s) {
+  const char* nm = DT ? (DC ? "tail_compact" : "tail_summary") : "compact";
+  CERTKV_LAUNCH(nm, (tail_compact_kernel<D, T, DT, DC>), dim3(a.g.H * st.count, a.g.L),
+                dim3(kTailThreads), 0, s, a.g, st, a.scores, static_cast<const T*>(a.k.ptr),
+                a.k.s_layer, a.k.s_token, a.k.s_head, static_cast<const T*>(a.v.ptr), a.v.s_layer,
+                a.v.s_token, a.v.s_head, a.kept_offsets, a.kept_idx, (const uint64_t*)a.bitmap,
+                a.bm_stride, a.ksum, a.vsum, a.k_star, a.v_star, a.tail_mass,
+                static_cast<T*>(a.k_packed), static_cast<T*>(a.v_packed), a.pos_packed);
+  return CERTKV_OK;
+}
+
+template <int D, typename T>
+static certkv_status dispatch_tail(const TailArgs& a, const SeqTab& st, hipStream_t s) {
+  if (a.do_tail && a.do_compact) return launch_tail<D, T, true, true>(a, st, s);
+  if (a.do_tail) return launch_tail<D, T, true, false>(a, st, s);
+  return launch_tail<D, T, false, true>(a, st, s);
+}
+
+certkv_status run_bitmap(const TailArgs& a, const SeqTab& st, int64_t words_total, bool clear,
+                         hipStream_t s) {
+  if (clear)
+    CERTKV_LAUNCH("kept_bitmap_clear", bitmap_clear_kernel, dim3((unsigned)((words_total + 255) / 256)),
+                  dim3(256), 0, s, a.bitmap, words_total);
+  CERTKV_LAUNCH("kept_bitmap_set", bitmap_set_kernel, dim3(a.g.H * st.count, a.g.L), dim3(256), 0, s,
+                a.g, st, a.kept_offsets, a.kept_idx, a.bitmap, a.bm_stride);
+  return CERTKV_OK;
+}
+
+certkv_status run_tail(const TailArgs& a, const SeqTab& st, hipStream_t s) {
+  if (a.dtype == CERTKV_BF16)
+    return a.g.D == 128 ? dispatch_tail<128, uint16_t>(a, st, s) : dispatch_tail<64, uint16_t>(a, st, s);
+  return a.g.D == 128 ? dispatch_tail<128, float>(a, st, s) : dispatch_tail<64, float>(a, st, s);
+}
+
+}  // namespace certkv

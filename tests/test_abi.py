@@ -1,0 +1,152 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+the header declares, and validates arguments (CERTKV_DRY_RUN: nothing is
+launched, so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_21541_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "certkv.h")
+
+FAKE = 1 << 20  # aligned non-null stand-in pointer (never dereferenced in dry runs)
+
+
+def declared_entry_points():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(certkv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.lib()
+    names = declared_entry_points()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(_lib.EXPORTS)
+
+
+def problem(L=2, seqlens=(1000, 700), H=4, G=2, d=128, w=16, dtype=_lib.CERTKV_BF16, flags=None):
+    cu = [0]
+    for n in seqlens:
+        cu.append(cu[-1] + n)
+    arr = (ctypes.c_int64 * len(cu))(*cu)
+    fl = (_lib.CERTKV_CAUSAL | _lib.CERTKV_DRY_RUN) if flags is None else flags
+    p = _lib.Problem(L, len(seqlens), H, G, d, w, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int64)),
+                     dtype, dtype, 0.0, fl)
+    p._keep = arr
+    return p
+
+
+def tensor(ptr=FAKE, sl=8 * 4 * 128 * 1700, st=4 * 128, sh=128):
+    return _lib.Tensor(ptr, sl, st, sh)
+
+
+def ws_for(p, stage):
+    n = _lib.lib().certkv_workspace_size(ctypes.byref(p), stage)
+    return (FAKE if n else None), n
+
+
+def status_name(st):
+    return _lib.lib().certkv_status_string(st).decode()
+
+
+def test_status_strings():
+    for st in [0, -1, -2, -3, -5, -6, -99]:
+        assert isinstance(status_name(st), str) and status_name(st)
+
+
+def test_dry_run_score_validation():
+    L = _lib.lib()
+    p = problem()
+    ws, n = ws_for(p, _lib.STAGE_SCORE)
+    assert n > 0
+    ok = L.certkv_score(ctypes.byref(p), tensor(), tensor(), FAKE, None, ws, n, None)
+    assert ok == _lib.CERTKV_OK
+    assert L.certkv_score(ctypes.byref(p), tensor(), tensor(), FAKE, None, ws, n - 256, None) == \
+        _lib.CERTKV_EWORKSPACE
+    assert L.certkv_score(ctypes.byref(p), tensor(ptr=FAKE + 4), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EINVAL
+    assert L.certkv_score(ctypes.byref(p), tensor(st=4 * 128 + 4), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EINVAL
+    assert L.certkv_score(ctypes.byref(problem(d=96)), tensor(), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EUNSUPPORTED
+    assert L.certkv_score(ctypes.byref(problem(w=701)), tensor(), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EINVAL
+    assert L.certkv_score(ctypes.byref(problem(H=65)), tensor(), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EUNSUPPORTED
+    assert L.certkv_score(ctypes.byref(problem(w=64, G=9)), tensor(), tensor(), FAKE, None, ws, n,
+                          None) == _lib.CERTKV_EUNSUPPORTED  # 576 window rows > 512
+    assert L.certkv_score(ctypes.byref(problem(flags=_lib.CERTKV_DRY_RUN | 64)), tensor(),
+                          tensor(), FAKE, None, ws, n, None) == _lib.CERTKV_EINVAL
+
+
+def test_dry_run_allocate_budget_checks():
+    L = _lib.lib()
+    p = problem()
+    ws, n = ws_for(p, _lib.STAGE_ALLOCATE)
+
+    def call(nk, alpha=0.2, steps=40):
+        arr = (ctypes.c_int32 * 2)(*nk)
+        return L.certkv_allocate(ctypes.byref(p), FAKE, tensor(), arr, alpha, steps, FAKE, None,
+                                 None, None, ws, n, None)
+
+    assert call([101, 71]) == _lib.CERTKV_OK
+    assert call([1, 71]) == _lib.CERTKV_EINFEASIBLE       # n_keep >= 2
+    assert call([1001, 71]) == _lib.CERTKV_EINFEASIBLE    # n_keep <= n
+    assert call([700, 700]) == _lib.CERTKV_OK             # keep all of sequence 2
+    assert call([101, 71], alpha=1.5) == _lib.CERTKV_EINVAL
+    assert call([101, 71], steps=-1) == _lib.CERTKV_EINVAL
+    assert L.certkv_allocate(ctypes.byref(p), FAKE, tensor(), None, 0.2, 40, FAKE, None, None,
+                             None, ws, n, None) == _lib.CERTKV_EINVAL
+
+
+def test_dry_run_compress_and_select():
+    L = _lib.lib()
+    p = problem()
+    ws, n = ws_for(p, _lib.STAGE_COMPRESS)
+    out = _lib.Outputs(*([FAKE] * 11 + [None, None]))
+    nk = (ctypes.c_int32 * 2)(101, 71)
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), nk, 0.2, 40,
+                             ctypes.byref(out), ws, n, None) == _lib.CERTKV_OK
+    out.kept_idx = None
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), nk, 0.2, 40,
+                             ctypes.byref(out), ws, n, None) == _lib.CERTKV_EINVAL
+    ws2, n2 = ws_for(p, _lib.STAGE_SELECT)
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, 5, 0.9, FAKE, FAKE, 10, ws2, n2, None) == \
+        _lib.CERTKV_EINVAL  # bad mode
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_COVERAGE, 1.5, FAKE,
+                           FAKE, 1 << 30, ws2, n2, None) == _lib.CERTKV_EINVAL
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_COVERAGE, 0.9, FAKE,
+                           FAKE, 1 << 30, ws2, n2, None) == _lib.CERTKV_OK
+
+
+def test_fp32_values_need_head_dim_64():
+    L = _lib.lib()
+    p = problem(dtype=_lib.CERTKV_F32, d=128, w=8, G=1)
+    ws, n = ws_for(p, _lib.STAGE_ALLOCATE)
+    nk = (ctypes.c_int32 * 2)(101, 71)
+    assert L.certkv_allocate(ctypes.byref(p), FAKE, tensor(), nk, 0.2, 40, FAKE, None, None, None,
+                             ws, n, None) == _lib.CERTKV_EUNSUPPORTED
+    p64 = problem(dtype=_lib.CERTKV_F32, d=64, w=8, G=1)
+    ws, n = ws_for(p64, _lib.STAGE_ALLOCATE)
+    assert L.certkv_allocate(ctypes.byref(p64), FAKE, tensor(sl=0, st=256, sh=64), nk, 0.2, 40,
+                             FAKE, None, None, None, ws, n, None) == _lib.CERTKV_OK
+
+
+def test_workspace_size_zero_on_invalid():
+    L = _lib.lib()
+    assert L.certkv_workspace_size(ctypes.byref(problem(d=96)), _lib.STAGE_COMPRESS) == 0
+    assert L.certkv_workspace_size(ctypes.byref(problem()), 99) == 0
+
+
+def test_profile_api_without_launches():
+    L = _lib.lib()
+    assert L.certkv_profile_enable(1) == 0
+    names = (ctypes.c_char * 64 * 8)()
+    assert L.certkv_profile_read(names, None, None, 8) == 0
+    L.certkv_profile_reset()
+    assert L.certkv_profile_enable(0) == 0

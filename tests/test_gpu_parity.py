@@ -1,0 +1,213 @@
+"""GPU parity of the HIP path against the fp64 CPU oracle, through the C ABI.
+
+Integer stages are bit-exact against the oracle fed the GPU's own upstream
+arrays; floating outputs meet the workload tolerances (per-key mass 1e-4
+relative; slot vectors and reconstructed window outputs 2e-3 relative L2).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_21541_amd as ck
+import synth
+from _parity import check_block_stages, run_gpu, spec_of, unit_id
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+
+
+# --------------------------------------------------------------------------
+# Small configurations, every block checked.
+
+def test_c1_tiny_fp32_full():
+    cfg = synth.config("C1")
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    check_block_stages(spec, cfg, cache, out, 0, 0, log=log)
+
+
+@pytest.mark.parametrize("n", [4096 + 77, 1000])
+def test_c2_shape_ragged_tail(n):
+    # Llama-3-8B head shapes (GQA 4, d 128, window 64) at a length that is not
+    # a multiple of any tile, so partial key tiles and partial rank chunks run.
+    cfg = synth.config("C2", seqlens=[n])
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    check_block_stages(spec, cfg, cache, out, 0, 0, log=log)
+
+
+def test_c2_full_length():
+    cfg = synth.config("C2")
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    check_block_stages(spec, cfg, cache, out, 0, 0, log=log)
+
+
+def test_c4_ragged_batch_two_layers():
+    # ragged batch with two layers: per-sequence offsets and budgets
+    cfg = synth.config("C4", seqlens=[3000, 8192 + 5, 1024, 4500], layers=2)
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    for li in range(2):
+        for b in range(cfg.batch):
+            check_block_stages(spec, cfg, cache, out, li, b, check_scores=(li == 1), log=log)
+
+
+def test_keep_all_and_minimal_budgets():
+    # n_keep = n: every head keeps n-1 tokens and the slot is the last-ranked
+    # key; n_keep = 2: B_real = H, every head keeps exactly b_min = 1.
+    cfg = synth.config("C2", seqlens=[640, 700])
+    cache = synth.make_cache(cfg, "cpu")
+    cache["n_keep"] = [640, 2]
+    spec, out, _, _ = run_gpu(cfg, cache)
+    bud = out["budgets"].numpy()
+    H = cfg.kv_heads
+    assert (bud[:H] == 639).all() and (bud[H:] == 1).all()
+    for b in range(2):
+        check_block_stages(spec, cfg, cache, out, 0, b, check_scores=False, log=log)
+    for h in range(H):
+        u = unit_id(spec, 0, 0, h)
+        last = out["perm"][0, h, 639].item()
+        np.testing.assert_allclose(out["v_star"][u].numpy(),
+                                   cache["v"][0, last, h].float().numpy(), rtol=1e-6, atol=1e-7)
+
+
+def test_determinism_bitwise():
+    cfg = synth.config("C2", seqlens=[5000, 3333])
+    cache = synth.make_cache(cfg, "cpu")
+    _, out1, _, _ = run_gpu(cfg, cache)
+    _, out2, _, _ = run_gpu(cfg, cache)
+    for name, t in out1.items():
+        if t is not None:
+            assert torch.equal(t, out2[name]), name
+
+
+# --------------------------------------------------------------------------
+# Stage entry points agree with the fused pass.
+
+def test_stage_entry_points_match_fused():
+    cfg = synth.config("C2", seqlens=[3000, 2049])
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, (q, k, v), _ = run_gpu(cfg, cache)
+    s, ksum = ck.score(spec, q, k, with_ksum=True)
+    assert torch.equal(s.cpu(), out["scores"])
+    al = ck.allocate(spec, s, v, cache["n_keep"], with_perm=True, with_curves=True, with_vsum=True)
+    assert torch.equal(al["budgets"].cpu(), out["budgets"])
+    assert torch.equal(al["perm"].cpu(), out["perm"])
+    assert torch.equal(al["curves"].cpu(), out["curves"])
+    b2 = ck.allocate_curves(spec, al["curves"], cache["n_keep"])
+    assert torch.equal(b2.cpu(), out["budgets"])
+    bsel, ko, ki = ck.select(spec, s, al["budgets"])
+    assert torch.equal(ko.cpu(), out["kept_offsets"])
+    nk = int(out["kept_offsets"][-1])
+    assert torch.equal(ki[:nk].cpu(), out["kept_idx"][:nk])
+    # complement form (totals given) and direct form agree within tolerance
+    ks1, vs1, m1 = ck.tail_summary(spec, s, k, v, ko, ki, ksum, al["vsum"])
+    ks2, vs2, m2 = ck.tail_summary(spec, s, k, v, ko, ki)
+    assert torch.equal(m1, m2)
+    torch.testing.assert_close(ks1, ks2, rtol=1e-4, atol=1e-5)
+    torch.testing.assert_close(vs1, vs2, rtol=1e-4, atol=1e-5)
+    torch.testing.assert_close(ks1.cpu(), out["k_star"], rtol=1e-5, atol=1e-6)
+    kp, vp, pp, po = ck.compact(spec, k, v, ko, ki, ks1, vs1)
+    assert torch.equal(po.cpu(), out["packed_offsets"])
+    assert torch.equal(pp.cpu(), out["pos_packed"])
+    kp_c, vp_c = kp.cpu(), vp.cpu()
+    real = out["pos_packed"] >= 0
+    assert torch.equal(kp_c[real], out["k_packed"][real])
+    assert torch.equal(vp_c[real], out["v_packed"][real])
+
+
+def test_coverage_mode_matches_oracle():
+    cfg = synth.config("C1")
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg)
+    dev = torch.device("cuda:0")
+    q, k = cache["q_win"].to(dev), cache["k"].to(dev)
+    s = ck.score(spec, q, k)
+    for retain in [0.5, 0.9, 0.99]:
+        kb, ko, ki = ck.select(spec, s, mode="coverage", retain_mass=retain)
+        torch.cuda.synchronize()
+        s_np = s.cpu().numpy()
+        for h in range(cfg.kv_heads):
+            perm = oracle.order(s_np[0, h])
+            k_eta = oracle.coverage(s_np[0, h], perm, retain)
+            assert kb[h].item() == k_eta, (retain, h)
+            kept = ki[ko[h].item():ko[h + 1].item()].cpu().numpy()
+            assert np.array_equal(kept, oracle.select(perm, k_eta))
+            a = oracle.normalize(s_np[0, h])
+            assert a[kept].sum() >= retain - 1e-12
+
+
+def test_allocate_from_supplied_curves_matches_oracle():
+    # allocation stage alone on adversarial curves: flat, linear, step shapes
+    rng = np.random.default_rng(7)
+    H, n = 8, 2000
+    x = np.arange(n, dtype=np.float64)
+    cases = [
+        np.zeros((H, n)),                                               # all ties
+        np.stack([(h + 1) * (n - 1 - x) for h in range(H)]),            # linear
+        np.stack([np.where(x < 50 * (h + 1), 10.0, 1.0) for h in range(H)]),  # steps
+        np.abs(np.cumsum(rng.standard_normal((H, n)), 1))[:, ::-1],     # rough
+    ]
+    cfg = synth.config("C2", seqlens=[n])
+    spec = spec_of(cfg)
+    for c in cases:
+        c32 = np.ascontiguousarray(c, np.float32)
+        for n_keep in [2, 3, 201, n // 2, n]:
+            t = torch.from_numpy(c32).reshape(1, H, n).cuda()
+            got = ck.allocate_curves(spec, t, [n_keep]).cpu().numpy()
+            want, _ = oracle.allocate(c32, n_keep)
+            assert np.array_equal(got, want), (n_keep, got, want)
+
+
+# --------------------------------------------------------------------------
+# Full-size workloads in the launch configuration the benchmark times:
+# sampled blocks against the oracle, invariants everywhere.
+
+def _global_invariants(spec, cfg, cache, out):
+    L, H = spec.layers, cfg.kv_heads
+    w, G = cfg.window, cfg.group
+    s = out["scores"].to(torch.float64)
+    cu = cache["cu_seqlens"]
+    for b in range(cfg.batch):
+        tot = s[:, :, cu[b]:cu[b + 1]].sum(-1)
+        assert torch.all((tot - w * G).abs() <= 1e-3 * w * G)
+    bud = out["budgets"].numpy().reshape(L, cfg.batch, H)
+    for b in range(cfg.batch):
+        br, bm = oracle.budget_params(H, cu[b + 1] - cu[b], cache["n_keep"][b])
+        assert (bud[:, b].sum(-1) == br).all() and bud[:, b].min() >= bm
+    po = out["packed_offsets"].numpy()
+    ko = out["kept_offsets"].numpy()
+    assert (po - ko == np.arange(len(po))).all()
+    assert (np.diff(ko) == out["budgets"].numpy()).all()
+    assert (out["tail_mass"].numpy() > 0).all()
+
+
+@pytest.mark.parametrize("name", ["C3", "C5"])
+def test_full_size_sampled(name):
+    cfg = synth.config(name)
+    log(f"{name}: generating {cfg.layers} layers on the GPU")
+    cache = synth.make_cache(cfg, "cuda:0")
+    spec = spec_of(cfg)
+    bufs = ck.compress(spec, cache["q_win"], cache["k"], cache["v"], cache["n_keep"],
+                       with_curves=True, with_perm=True)
+    torch.cuda.synchronize()
+    out = {k: (t.cpu() if t is not None else None) for k, t in bufs.as_dict().items()}
+    del bufs
+    _global_invariants(spec, cfg, cache, out)
+    log(f"{name}: invariants hold; oracle on sampled layers")
+    for li in [0, cfg.layers - 1]:
+        check_block_stages(spec, cfg, cache, out, li, 0, check_scores=(li == 0), log=log)
