@@ -133,6 +133,11 @@ def main():
     prof = ck.profile_read()
     ck.profile_enable(False)
     ck.profile_reset()
+    st = bufs.alloc_stats.cpu()
+    alloc_diag = {"repairs_mean": float(st[:, 0].float().mean()), "repairs_max": int(st[:, 0].max()),
+                  "bisect_us_mean": float(st[:, 1].float().mean()) / 100.0,
+                  "repair_us_mean": float(st[:, 2].float().mean()) / 100.0}
+    log(f"allocation: {alloc_diag}")
     model, ht = algorithmic_model(cfg, n_keep)
     kernels = {}
     for name, (cnt, tot) in prof.items():
@@ -187,6 +192,7 @@ def main():
         "roofline": roof,
         "kernels": kernels,
         "cpu_baseline": cpu,
+        "allocation": alloc_diag,
     }
     print(json.dumps(rec), flush=True)
 

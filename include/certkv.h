@@ -126,6 +126,9 @@ typedef struct certkv_problem {
  *   packed_offsets[L*B*H+1] int64, start of each unit's packed segment
  *   curves        optional [L][H][T] fp32, c_h(b) for b = 0..n_b-1
  *   perm          optional [L][H][T] int32, key position at each rank
+ *   alloc_stats   optional [L*B][3] int64 diagnostics of the allocation per
+ *                 (layer, sequence): one-token repairs performed, and the
+ *                 bisection and repair durations in 100 MHz clock ticks
  * Every (layer, sequence) block of the packed cache holds exactly
  * H * n_keep_b rows (the matched live-slot budget). */
 typedef struct certkv_outputs {
@@ -142,6 +145,7 @@ typedef struct certkv_outputs {
   int64_t* packed_offsets;
   float* curves;
   int32_t* perm;
+  int64_t* alloc_stats;
 } certkv_outputs;
 
 /* Human-readable name of a status code (static storage). */

@@ -66,7 +66,7 @@ class Tensor(ctypes.Structure):
 class Outputs(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "scores", "budgets", "kept_offsets", "kept_idx", "k_star", "v_star", "tail_mass",
-        "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm")]
+        "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm", "alloc_stats")]
 
 
 class CertKVError(RuntimeError):

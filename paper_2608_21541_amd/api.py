@@ -238,6 +238,8 @@ class CompressBuffers:
         self.packed_offsets = torch.empty(U + 1, dtype=torch.int64, device=device)
         self.curves = torch.empty(shape, dtype=torch.float32, device=device) if with_curves else None
         self.perm = torch.empty(shape, dtype=torch.int32, device=device) if with_perm else None
+        self.alloc_stats = torch.zeros((spec.layers * spec.batch, 3), dtype=torch.int64,
+                                       device=device)
         self.ws, self.ws_bytes = _workspace(spec, _lib.STAGE_COMPRESS, device)
         self._nk = (ctypes.c_int32 * spec.batch)(*self.n_keep)
         self._p = spec.c_problem()
@@ -245,12 +247,13 @@ class CompressBuffers:
             (t.data_ptr() if t is not None else None) for t in (
                 self.scores, self.budgets, self.kept_offsets, self.kept_idx, self.k_star,
                 self.v_star, self.tail_mass, self.k_packed, self.v_packed, self.pos_packed,
-                self.packed_offsets, self.curves, self.perm)])
+                self.packed_offsets, self.curves, self.perm, self.alloc_stats)])
 
     def as_dict(self):
         return {k: getattr(self, k) for k in (
             "scores", "budgets", "kept_offsets", "kept_idx", "k_star", "v_star", "tail_mass",
-            "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm")}
+            "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm",
+            "alloc_stats")}
 
 
 def compress(spec: ProblemSpec, q_win, k, v, n_keep, alpha=0.2, steps=40, bufs=None,

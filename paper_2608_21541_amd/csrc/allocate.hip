@@ -1,44 +1,54 @@
 // Budget allocation (multiplier bisection + one-token repair) on gfx950.
 //
-// One workgroup per (layer, sequence).  Each bisection step needs, for every
-// head, the smallest b in [b_min, n-1] minimizing f(b) = fma(lambda, b, c(b))
-// in fp64 on the fp32 curve.  Scanning all H*n candidates 40 times would
-// re-read the curves from L2 40 times, so the scan is pruned exactly:
-// for a block of 256 ranks starting at b0 (clamped to b_min) with block
-// minimum cmin, every candidate b >= b0 has lambda*b + c(b) >= lambda*b0 +
-// cmin, and round-to-nearest is monotone, so LB = fma(lambda, b0, cmin) <=
-// f(b) for the whole block.  A block whose (LB, b0) is lexicographically above
-// the current best (f*, b*) cannot hold the answer (ties favour smaller b), so
-// only the block with the smallest LB and the blocks whose LB undercuts the
-// best found in it are evaluated candidate by candidate.  The result is
-// identical to the full scan.
+// One workgroup per (layer, sequence).
 //
-// Repair runs on one wave, lane h owning head h, with each head's next curve
-// values cached in LDS.
+// Bisection.  Each step needs, per head, the smallest b in [b_min, n-1]
+// minimizing f(b) = fma(lambda, b, c(b)) in fp64 on the fp32 curve.  The scan
+// is pruned exactly: for a block of 256 ranks starting at b0 (clamped to
+// b_min) with block minimum cmin, every candidate has lambda*b + c(b) >=
+// lambda*b0 + cmin, and round-to-nearest is monotone, so LB = fma(lambda, b0,
+// cmin) <= f(b) on the block.  The block with the smallest bound is evaluated
+// first (32 threads per head); every block whose (LB, b0) undercuts the best
+// (f*, b*) lexicographically is then put on a candidate list and evaluated
+// by the whole workgroup, one coalesced 256-wide row per block.  Blocks left
+// out cannot hold the answer (ties favour smaller b), so the result equals the
+// full scan.
+//
+// Repair.  Starting from b_h = b_h(lambda_hi), the method adds one token at a
+// time to the head with the smallest marginal d_h(i) = c_h(i+1) - c_h(i)
+// (ties: lowest head).  That greedy consumes the candidate increments in
+// increasing order of the key (P_h(i), h, i), where P_h(i) is the running
+// maximum of d_h over [b_h, i]: all increments keyed below a level are taken
+// before any keyed at or above it, and within a level the lowest head runs
+// first.  So the final budgets follow from the R-th smallest key, R = B_real -
+// sum b_h: a bisection over the ordered bit patterns of fp64 keys finds it,
+// counting per head with block-level running maxima (LDS) and one scan of the
+// block where the running maximum crosses the threshold.
 #include "stages.h"
 
 namespace certkv {
 
 constexpr int kAllocThreads = 256;
-constexpr int kHeadGroup = 8;     // heads evaluated concurrently (32 threads each)
-constexpr int kBlk = 256;         // ranks per pruning block
-constexpr int kRepairWin = 64;    // cached curve values per head during repair
+constexpr int kHeadGroup = 8;      // heads evaluated concurrently (32 threads each)
+constexpr int kBlk = 256;          // ranks per pruning block
+constexpr int kLdsItems = 8192;    // H * blocks handled from LDS
+constexpr int kRepairWin = 64;     // cached curve values per head (fallback repair)
+
+__device__ __forceinline__ bool lex_less(double f1, int b1, double f2, int b2) {
+  return f1 < f2 || (f1 == f2 && b1 < b2);
+}
 
 struct BestFB {
   double f;
   int b;
 };
 
-__device__ __forceinline__ bool lex_less(double f1, int b1, double f2, int b2) {
-  return f1 < f2 || (f1 == f2 && b1 < b2);
-}
-
 // Lexicographic (f, b) minimum over the 32 lanes of a half-wave.
 __device__ __forceinline__ BestFB half_wave_min(double f, int b) {
 #pragma unroll
   for (int m = 16; m >= 1; m >>= 1) {
-    double fo = __shfl_xor(f, m, 64);
-    int bo = __shfl_xor(b, m, 64);
+    const double fo = __shfl_xor(f, m, 64);
+    const int bo = __shfl_xor(b, m, 64);
     if (lex_less(fo, bo, f, b)) {
       f = fo;
       b = bo;
@@ -47,66 +57,91 @@ __device__ __forceinline__ BestFB half_wave_min(double f, int b) {
   return BestFB{f, b};
 }
 
-// argmin_b fma(lam, b, c(b)) over [bmin, n-1] for one head, by the 32 threads
-// with sub = 0..31.  Returns the same value in all 32 threads.
-__device__ int head_argmin(const float* __restrict__ ch, const float* __restrict__ mh, int n,
-                           int bmin, double lam, int sub) {
+__device__ __forceinline__ BestFB wave_lexmin(double f, int b) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const double fo = __shfl_xor(f, m, 64);
+    const int bo = __shfl_xor(b, m, 64);
+    if (lex_less(fo, bo, f, b)) {
+      f = fo;
+      b = bo;
+    }
+  }
+  return BestFB{f, b};
+}
+
+// Monotone map between fp64 values and unsigned keys (total order of doubles).
+__device__ __forceinline__ uint64_t dkey(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  return (u & 0x8000000000000000ull) ? ~u : (u | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double dval(uint64_t k) {
+  const uint64_t u = (k & 0x8000000000000000ull) ? (k & 0x7fffffffffffffffull) : ~k;
+  return __longlong_as_double((long long)u);
+}
+
+// Per-block statistics of the curves: minimum and maximum of c over each
+// 256-rank block, and the maximum marginal d(i) = c(i+1) - c(i) (fp64) over
+// the i of the block with i <= n-2.  One wave per block.
+__global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st, int32_t nblk_max,
+                                                               const float* __restrict__ curves,
+                                                               float* __restrict__ cmin,
+                                                               float* __restrict__ cmaxb,
+                                                               double* __restrict__ dmax) {
+  const int per_unit = (nblk_max + 3) / 4;
+  const int wb = blockIdx.x % per_unit;
+  const int hb = blockIdx.x / per_unit;
+  const int h = hb % g.H;
+  const int bl = hb / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int n = st.len[bl];
   const int nblk = (n + kBlk - 1) / kBlk;
-  const int kfirst = bmin / kBlk;
-  // (a) block with the smallest lower bound
-  double lbest = INFINITY;
-  int kbest = 0x7fffffff;
-  for (int k = kfirst + sub; k < nblk; k += 32) {
-    const int b0 = max(k * kBlk, bmin);
-    const double lb = fma(lam, (double)b0, (double)mh[k]);
-    if (lex_less(lb, k, lbest, kbest)) {
-      lbest = lb;
-      kbest = k;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int k = wb * 4 + wave;
+  if (k >= nblk) return;
+  const int64_t u = unit_index(g, l, st.first + bl, h);
+  const float* ch = curves + lht_base(g, l, h, st.start[bl]);
+  const int i0 = k * kBlk + lane * 4;
+  float c[5];
+#pragma unroll
+  for (int e = 0; e < 5; ++e) c[e] = (i0 + e < n) ? ch[i0 + e] : 0.f;
+  float mn = INFINITY, mx = -INFINITY;
+  double dm = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (i0 + e < n) {
+      mn = fminf(mn, c[e]);
+      mx = fmaxf(mx, c[e]);
     }
+    if (i0 + e <= n - 2) dm = fmax(dm, (double)c[e + 1] - (double)c[e]);
   }
-  BestFB kb = half_wave_min(lbest, kbest);
-  const int kstar = kb.b;
-  // (b) exact minimum inside that block
-  double fbest = INFINITY;
-  int bbest = 0x7fffffff;
-  {
-    const int lo = max(kstar * kBlk, bmin), hi = min(kstar * kBlk + kBlk - 1, n - 1);
-    for (int bb = lo + sub; bb <= hi; bb += 32) {
-      const double f = fma(lam, (double)bb, (double)ch[bb]);
-      if (lex_less(f, bb, fbest, bbest)) {
-        fbest = f;
-        bbest = bb;
-      }
-    }
+  mn = wave_min_f(mn);
+  mx = wave_max(mx);
+  dm = wave_max(dm);
+  if (lane == 0) {
+    cmin[u * nblk_max + k] = mn;
+    cmaxb[u * nblk_max + k] = mx;
+    dmax[u * nblk_max + k] = dm;
   }
-  BestFB fb = half_wave_min(fbest, bbest);
-  // (c) every other block whose bound undercuts (f*, b*)
-  double f2 = fb.f;
-  int b2 = fb.b;
-  for (int k = kfirst + sub; k < nblk; k += 32) {
-    if (k == kstar) continue;
-    const int b0 = max(k * kBlk, bmin);
-    const double lb = fma(lam, (double)b0, (double)mh[k]);
-    if (lex_less(lb, b0, fb.f, fb.b)) {
-      const int hi = min(k * kBlk + kBlk - 1, n - 1);
-      for (int bb = b0; bb <= hi; ++bb) {
-        const double f = fma(lam, (double)bb, (double)ch[bb]);
-        if (lex_less(f, bb, f2, b2)) {
-          f2 = f;
-          b2 = bb;
-        }
-      }
-    }
-  }
-  return half_wave_min(f2, b2).b;
 }
 
 __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     Geo g, SeqTab st, const float* __restrict__ curves, const float* __restrict__ cmin,
-    int32_t cmin_stride, const float* __restrict__ cmax, int32_t steps,
-    int32_t* __restrict__ budgets, int64_t* __restrict__ repairs) {
-  __shared__ int32_t bcur[64];
-  __shared__ int32_t bhi[64];
+    const float* __restrict__ cmaxb, const double* __restrict__ dmax, int32_t nblk_max,
+    int32_t steps, int32_t* __restrict__ budgets, int64_t* __restrict__ stats) {
+  // 64 KB of LDS: block minima + candidate lists during the bisection, the
+  // block-level running maxima of the marginals during the repair.
+  __shared__ __align__(16) unsigned char pool[kLdsItems * 8];
+  float* mcache = reinterpret_cast<float*>(pool);
+  int32_t* cand = reinterpret_cast<int32_t*>(pool + kLdsItems * 4);
+  double* pbm = reinterpret_cast<double*>(pool);
+  __shared__ double fbest[64];
+  __shared__ int32_t bbest[64], kstar[64], ccount[64], coff[65], cfill[64];
+  __shared__ int32_t bcur[64], bhi[64];
+  __shared__ double redf[4];
+  __shared__ int32_t redb[4];
+  __shared__ int64_t cnt_lt[64], cnt_le[64];
   __shared__ float win[64][kRepairWin + 1];
 
   const int bl = blockIdx.x;
@@ -119,31 +154,206 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   const int bmin = st.b_min[bl];
   const int H = g.H;
   const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int sub = tid & 31;
   const int hg = tid >> 5;
+  const int nblk = (n + kBlk - 1) / kBlk;
+  const int kfirst = bmin / kBlk;
+  const bool fast = H * nblk <= kLdsItems;
+  const uint64_t t_start = wall_clock64();
 
+  // lambda_hi = 2 max c + 1 over every head and b in [0, n-1]
   double cm = 0.0;
-  for (int h = 0; h < H; ++h) cm = fmax(cm, (double)cmax[unit_index(g, l, b, h)]);
+  for (int i = tid; i < H * nblk; i += kAllocThreads) {
+    const int h = i / nblk, k = i % nblk;
+    cm = fmax(cm, (double)cmaxb[unit_index(g, l, b, h) * nblk_max + k]);
+  }
+  cm = wave_max(cm);
+  if (lane == 0) redf[wave] = cm;
+  if (fast) {
+    for (int i = tid; i < H * nblk; i += kAllocThreads) {
+      const int h = i / nblk, k = i % nblk;
+      mcache[i] = cmin[unit_index(g, l, b, h) * nblk_max + k];
+    }
+  }
+  __syncthreads();
+  cm = fmax(fmax(redf[0], redf[1]), fmax(redf[2], redf[3]));
   double lo = 0.0, hi = 2.0 * cm + 1.0;
 
+  auto mh_at = [&](int h, int k) -> float {
+    return fast ? mcache[h * nblk + k] : cmin[unit_index(g, l, b, h) * nblk_max + k];
+  };
+
+  // argmin over [bmin, n-1] of fma(lam, b, c_h(b)) for every head -> out[h]
   auto evaluate = [&](double lam, int32_t* out) {
+    // (a) + (b): per head, best-bound block evaluated exactly (32 threads)
     for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
       const int h = h0 + hg;
       if (h < H) {
         const float* ch = curves + lht_base(g, l, h, tok0);
-        const float* mh = cmin + unit_index(g, l, b, h) * cmin_stride;
-        const int bh = head_argmin(ch, mh, n, bmin, lam, sub);
-        if (sub == 0) out[h] = bh;
+        double lbest = INFINITY;
+        int kb_ = 0x7fffffff;
+        for (int k = kfirst + sub; k < nblk; k += 32) {
+          const int b0 = max(k * kBlk, bmin);
+          const double lb = fma(lam, (double)b0, (double)mh_at(h, k));
+          if (lex_less(lb, k, lbest, kb_)) {
+            lbest = lb;
+            kb_ = k;
+          }
+        }
+        const int ks = half_wave_min(lbest, kb_).b;
+        double f = INFINITY;
+        int bb = 0x7fffffff;
+        const int lo_b = max(ks * kBlk, bmin), hi_b = min(ks * kBlk + kBlk - 1, n - 1);
+        float cv[kBlk / 32];
+#pragma unroll
+        for (int i = 0; i < kBlk / 32; ++i) {
+          const int x = ks * kBlk + sub + 32 * i;
+          cv[i] = (x >= lo_b && x <= hi_b) ? ch[x] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < kBlk / 32; ++i) {
+          const int x = ks * kBlk + sub + 32 * i;
+          if (x >= lo_b && x <= hi_b) {
+            const double v = fma(lam, (double)x, (double)cv[i]);
+            if (lex_less(v, x, f, bb)) {
+              f = v;
+              bb = x;
+            }
+          }
+        }
+        const BestFB r = half_wave_min(f, bb);
+        if (sub == 0) {
+          fbest[h] = r.f;
+          bbest[h] = r.b;
+          kstar[h] = ks;
+          ccount[h] = 0;
+        }
       }
     }
+    __syncthreads();
+    if (fast) {
+      // (c) candidate blocks grouped by head, then evaluated by all threads
+      for (int i = tid; i < H * nblk; i += kAllocThreads) {
+        const int h = i / nblk, k = i % nblk;
+        if (k < kfirst || k == kstar[h]) continue;
+        const int b0 = max(k * kBlk, bmin);
+        const double lb = fma(lam, (double)b0, (double)mcache[i]);
+        if (lex_less(lb, b0, fbest[h], bbest[h])) atomicAdd(&ccount[h], 1);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int run = 0;
+        for (int h = 0; h < H; ++h) {
+          coff[h] = run;
+          cfill[h] = run;
+          run += ccount[h];
+        }
+        coff[H] = run;
+      }
+      __syncthreads();
+      for (int i = tid; i < H * nblk; i += kAllocThreads) {
+        const int h = i / nblk, k = i % nblk;
+        if (k < kfirst || k == kstar[h]) continue;
+        const int b0 = max(k * kBlk, bmin);
+        const double lb = fma(lam, (double)b0, (double)mcache[i]);
+        if (lex_less(lb, b0, fbest[h], bbest[h])) cand[atomicAdd(&cfill[h], 1)] = k;
+      }
+      __syncthreads();
+      for (int h = 0; h < H; ++h) {
+        const int c0 = coff[h], c1 = coff[h + 1];
+        if (c0 == c1) continue;
+        const float* ch = curves + lht_base(g, l, h, tok0);
+        double f = INFINITY;
+        int bb = 0x7fffffff;
+        int c = c0;
+        for (; c + 4 <= c1; c += 4) {
+          float cv[4];
+          int xs[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            xs[e] = cand[c + e] * kBlk + tid;
+            cv[e] = (xs[e] >= bmin && xs[e] <= n - 1) ? ch[xs[e]] : 0.f;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (xs[e] >= bmin && xs[e] <= n - 1) {
+              const double v = fma(lam, (double)xs[e], (double)cv[e]);
+              if (lex_less(v, xs[e], f, bb)) {
+                f = v;
+                bb = xs[e];
+              }
+            }
+          }
+        }
+        for (; c < c1; ++c) {
+          const int x = cand[c] * kBlk + tid;
+          if (x >= bmin && x <= n - 1) {
+            const double v = fma(lam, (double)x, (double)ch[x]);
+            if (lex_less(v, x, f, bb)) {
+              f = v;
+              bb = x;
+            }
+          }
+        }
+        const BestFB r = wave_lexmin(f, bb);
+        if (lane == 0) {
+          redf[wave] = r.f;
+          redb[wave] = r.b;
+        }
+        __syncthreads();
+        if (tid == 0) {
+          double ff = fbest[h];
+          int b2 = bbest[h];
+          for (int w = 0; w < 4; ++w)
+            if (lex_less(redf[w], redb[w], ff, b2)) {
+              ff = redf[w];
+              b2 = redb[w];
+            }
+          fbest[h] = ff;
+          bbest[h] = b2;
+        }
+        __syncthreads();
+      }
+    } else {
+      // large problems: every other block re-checked by its head's 32 threads
+      for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+        const int h = h0 + hg;
+        if (h < H) {
+          const float* ch = curves + lht_base(g, l, h, tok0);
+          double f = fbest[h];
+          int bb = bbest[h];
+          for (int k = kfirst + sub; k < nblk; k += 32) {
+            if (k == kstar[h]) continue;
+            const int b0 = max(k * kBlk, bmin);
+            const double lb = fma(lam, (double)b0, (double)mh_at(h, k));
+            if (!lex_less(lb, b0, f, bb)) continue;
+            const int hi_b = min(k * kBlk + kBlk - 1, n - 1);
+            for (int x = b0; x <= hi_b; ++x) {
+              const double v = fma(lam, (double)x, (double)ch[x]);
+              if (lex_less(v, x, f, bb)) {
+                f = v;
+                bb = x;
+              }
+            }
+          }
+          const BestFB r = half_wave_min(f, bb);
+          if (sub == 0) {
+            fbest[h] = r.f;
+            bbest[h] = r.b;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (tid < H) out[tid] = bbest[tid];
+    __syncthreads();
   };
 
   evaluate(hi, bhi);
-  __syncthreads();
   for (int t = 0; t < steps; ++t) {
     const double lam = (lo + hi) / 2.0;
     evaluate(lam, bcur);
-    __syncthreads();
     int64_t sum = 0;
     for (int h = 0; h < H; ++h) sum += bcur[h];
     if (sum > B_real) {
@@ -154,16 +364,110 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     }
     __syncthreads();
   }
+  const uint64_t t_bisect = wall_clock64();
 
-  // Repair to the exact budget: one wave, lane h = head h.
-  if (tid < 64) {
-    const int lane = tid;
+  int64_t sum0 = 0;
+  for (int h = 0; h < H; ++h) sum0 += bhi[h];
+  const int64_t R = B_real - sum0;
+  const int64_t nrep = R >= 0 ? R : -R;
+  const int kmax = (n - 2) / kBlk;  // last block holding an increment i <= n-2
+
+  // Number of increments of head h whose key P is < p (le = false) or <= p
+  // (le = true); computed by the 32 threads of a half-wave.
+  auto count_head = [&](int h, double p, bool le) -> int64_t {
+    const int s = bhi[h];
+    if (s > n - 2) return 0;
+    const int ks = s / kBlk;
+    int lo_k = ks, hi_k = kmax + 1;  // first block whose running max crosses p
+    while (lo_k < hi_k) {
+      const int mid = (lo_k + hi_k) >> 1;
+      const double v = pbm[h * nblk + mid];
+      if (le ? (v > p) : (v >= p)) hi_k = mid;
+      else lo_k = mid + 1;
+    }
+    if (lo_k > kmax) return (int64_t)(n - 1 - s);
+    const float* ch = curves + lht_base(g, l, h, tok0);
+    const int i0 = max(lo_k * kBlk, s), i1 = min(lo_k * kBlk + kBlk - 1, n - 2);
+    int first = 0x7fffffff;
+    for (int i = i0 + sub; i <= i1; i += 32) {
+      const double d = (double)ch[i + 1] - (double)ch[i];
+      if ((le ? (d > p) : (d >= p)) && i < first) first = i;
+    }
+#pragma unroll
+    for (int m = 16; m >= 1; m >>= 1) first = min(first, __shfl_xor(first, m, 64));
+    return (int64_t)(first - s);
+  };
+  auto total_count = [&](double p, bool le, int64_t* per_head) -> int64_t {
+    for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+      const int h = h0 + hg;
+      if (h < H) {
+        const int64_t c = count_head(h, p, le);
+        if (sub == 0) per_head[h] = c;
+      }
+    }
+    __syncthreads();
+    int64_t tot = 0;
+    for (int h = 0; h < H; ++h) tot += per_head[h];
+    __syncthreads();
+    return tot;
+  };
+
+  if (R > 0 && fast) {
+    // pbm[h*nblk + k] = running max of d_h over [s_h, end of block k] for the
+    // blocks k >= block of s_h (s_h = bhi[h]); -inf before it.
+    for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+      const int h = h0 + hg;
+      if (h < H) {
+        const float* ch = curves + lht_base(g, l, h, tok0);
+        const int s = bhi[h];
+        const int ks = s / kBlk;
+        double dm = -INFINITY;
+        if (s <= n - 2) {
+          const int e1 = min(ks * kBlk + kBlk - 1, n - 2);
+          for (int i = s + sub; i <= e1; i += 32) dm = fmax(dm, (double)ch[i + 1] - (double)ch[i]);
+        }
+#pragma unroll
+        for (int m = 16; m >= 1; m >>= 1) dm = fmax(dm, __shfl_xor(dm, m, 64));
+        if (sub == 0) {
+          double run = dm;
+          for (int k = 0; k < nblk; ++k) {
+            if (k > ks && k <= kmax) run = fmax(run, dmax[unit_index(g, l, b, h) * nblk_max + k]);
+            pbm[h * nblk + k] = (k < ks || s > n - 2) ? -INFINITY : run;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // smallest key x in [-inf, +inf] with count(P <= x) >= R, by bisection
+    // over the ordered bit patterns (count(P <= +inf) covers every increment)
+    uint64_t klo = dkey(-INFINITY), khi = dkey(INFINITY);
+    while (klo < khi) {
+      const uint64_t mid = klo + ((khi - klo) >> 1);
+      const int64_t c = total_count(dval(mid), true, cnt_le);
+      if (c >= R) khi = mid;
+      else klo = mid + 1;
+    }
+    const double pstar = dval(klo);
+    total_count(pstar, false, cnt_lt);
+    total_count(pstar, true, cnt_le);
+    if (tid == 0) {
+      int64_t rem = R;
+      for (int h = 0; h < H; ++h) rem -= cnt_lt[h];
+      for (int h = 0; h < H; ++h) {
+        const int64_t eq = cnt_le[h] - cnt_lt[h];
+        const int64_t take = rem < eq ? rem : eq;
+        rem -= take;
+        bhi[h] = bhi[h] + (int32_t)(cnt_lt[h] + take);
+      }
+    }
+    __syncthreads();
+    if (tid < H) budgets[unit_index(g, l, b, tid)] = bhi[tid];
+  } else if (tid < 64) {
+    // Sequential repair (large problems, or the unreachable removal case).
     const bool act = lane < H;
     int bh = act ? bhi[lane] : 0;
     const float* ch = act ? curves + lht_base(g, l, lane, tok0) : curves;
-    int64_t sum = 0;
-    for (int h = 0; h < H; ++h) sum += bhi[h];
-    int64_t nrep = 0;
+    int64_t sum = sum0;
     int wbase = bh;  // win[lane][i] = c(wbase + i)
     if (act)
       for (int i = 0; i <= kRepairWin && wbase + i < n; ++i) win[lane][i] = ch[wbase + i];
@@ -176,90 +480,35 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         }
         d = (double)win[lane][bh + 1 - wbase] - (double)win[lane][bh - wbase];
       }
-      double dm = d;
-      int hm = act ? lane : 0x7fffffff;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        double dof = __shfl_xor(dm, m, 64);
-        int ho = __shfl_xor(hm, m, 64);
-        if (lex_less(dof, ho, dm, hm)) {
-          dm = dof;
-          hm = ho;
-        }
-      }
-      if (dm == INFINITY) break;  // unreachable: B_real <= H (n - 1)
-      if (lane == hm) ++bh;
+      const BestFB r = wave_lexmin(d, act ? lane : 0x7fffffff);
+      if (r.f == INFINITY) break;  // unreachable: B_real <= H (n - 1)
+      if (lane == r.b) ++bh;
       ++sum;
-      ++nrep;
     }
     while (sum > B_real) {
       double d = INFINITY;
       if (act && bh > bmin) d = (double)ch[bh - 1] - (double)ch[bh];
-      double dm = d;
-      int hm = act ? lane : 0x7fffffff;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        double dof = __shfl_xor(dm, m, 64);
-        int ho = __shfl_xor(hm, m, 64);
-        if (lex_less(dof, ho, dm, hm)) {
-          dm = dof;
-          hm = ho;
-        }
-      }
-      if (dm == INFINITY) break;  // unreachable: H b_min <= B_real
-      if (lane == hm) --bh;
+      const BestFB r = wave_lexmin(d, act ? lane : 0x7fffffff);
+      if (r.f == INFINITY) break;  // unreachable: H b_min <= B_real
+      if (lane == r.b) --bh;
       --sum;
-      ++nrep;
     }
     if (act) budgets[unit_index(g, l, b, lane)] = bh;
-    if (repairs && lane == 0) repairs[(int64_t)l * g.B + b] = nrep;
+  }
+  if (stats && tid == 0) {
+    stats[((int64_t)l * g.B + b) * 3 + 0] = nrep;
+    stats[((int64_t)l * g.B + b) * 3 + 1] = (int64_t)(t_bisect - t_start);
+    stats[((int64_t)l * g.B + b) * 3 + 2] = (int64_t)(wall_clock64() - t_bisect);
   }
 }
-
-// Block minima and maximum of caller-supplied curves (the allocation-only path).
-__global__ __launch_bounds__(256) void block_minmax_kernel(Geo g, SeqTab st,
-                                                            const float* __restrict__ curves,
-                                                            float* __restrict__ cmin,
-                                                            int32_t cmin_stride,
-                                                            float* __restrict__ cmax) {
-  __shared__ float wmx[4];
-  const int h = blockIdx.x % g.H;
-  const int bl = blockIdx.x / g.H;
-  const int l = blockIdx.y;
-  if (bl >= st.count) return;
-  const int b = st.first + bl;
-  const int n = st.len[bl];
-  const int64_t u = unit_index(g, l, b, h);
-  const float* ch = curves + lht_base(g, l, h, st.start[bl]);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float mx = -INFINITY;
-  const int nblk = (n + kBlk - 1) / kBlk;
-  for (int k = wave; k < nblk; k += 4) {
-    float mn = INFINITY;
-    for (int i = lane; i < kBlk; i += 64) {
-      const int bb = k * kBlk + i;
-      if (bb < n) {
-        mn = fminf(mn, ch[bb]);
-        mx = fmaxf(mx, ch[bb]);
-      }
-    }
-    mn = wave_min_f(mn);
-    if (lane == 0) cmin[u * cmin_stride + k] = mn;
-  }
-  mx = wave_max(mx);
-  if (lane == 0) wmx[wave] = mx;
-  __syncthreads();
-  if (threadIdx.x == 0) cmax[u] = fmaxf(fmaxf(wmx[0], wmx[1]), fmaxf(wmx[2], wmx[3]));
-}
-
 
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) {
-  if (a.need_minmax)
-    CERTKV_LAUNCH("curve_block_minmax", block_minmax_kernel, dim3(a.g.H * st.count, a.g.L),
-                  dim3(256), 0, s, a.g, st, a.curves, a.cmin, a.cmin_stride, a.cmax);
+  const int per_unit = (a.nblk_max + 3) / 4;
+  CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
+                dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.dmax);
   CERTKV_LAUNCH("allocate", allocate_kernel, dim3(st.count, a.g.L), dim3(kAllocThreads), 0, s, a.g,
-                st, a.curves, (const float*)a.cmin, a.cmin_stride, (const float*)a.cmax, a.steps,
-                a.budgets, a.repairs);
+                st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb, (const double*)a.dmax,
+                a.nblk_max, a.steps, a.budgets, a.repairs);
   return CERTKV_OK;
 }
 

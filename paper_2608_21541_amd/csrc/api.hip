@@ -57,7 +57,9 @@ struct Plan {
   int kpb;           // keys per scoring block
   int nkb_max;       // scoring blocks per unit (max over sequences)
   int nblk_max;      // 256-rank allocation blocks per unit
+  int nsub_max;      // 16-rank allocation sub-blocks per unit
   int bm_words;      // 64-bit bitmap words per unit
+  int nsplit;        // tail gather workgroups per unit
   const int64_t* cu;
 };
 
@@ -105,7 +107,10 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.kpb = kpb;
   P.nkb_max = (max_len + kpb - 1) / kpb;
   P.nblk_max = (max_len + 255) / 256;
+  P.nsub_max = (max_len + 15) / 16;
   P.bm_words = (max_len + 63) / 64;
+  P.nsplit = (max_len + 8191) / 8192;
+  if (P.nsplit > 64) P.nsplit = 64;
   return CERTKV_OK;
 }
 
@@ -185,12 +190,17 @@ struct Bufs {
   double* ssum = nullptr;
   float* curves = nullptr;
   float* cmin = nullptr;
-  float* cmax = nullptr;
+  float* cmaxb = nullptr;
+  double* dmax = nullptr;
   double* vsum = nullptr;
   int64_t* repairs = nullptr;
   // select / tail
   uint64_t* bitmap = nullptr;
   int64_t* kept_offsets = nullptr;
+  double* tpart = nullptr;
+  double* mpart = nullptr;
+  double* evicted_sum = nullptr;
+  double* total_sum = nullptr;
 };
 
 enum : uint32_t {
@@ -229,10 +239,17 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
   if (need & NEED_CURVEBUF) b->curves = w.take<float>(LHT);
   if (need & (NEED_CURVES | NEED_MINMAX)) {
     b->cmin = w.take<float>((size_t)P.U * P.nblk_max);
-    b->cmax = w.take<float>((size_t)P.U);
-    b->repairs = w.take<int64_t>((size_t)P.g.L * P.g.B);
+    b->cmaxb = w.take<float>((size_t)P.U * P.nblk_max);
+    b->dmax = w.take<double>((size_t)P.U * P.nblk_max);
+    b->repairs = w.take<int64_t>((size_t)P.g.L * P.g.B * 3);
   }
-  if (need & NEED_BITMAP) b->bitmap = w.take<uint64_t>((size_t)P.U * P.bm_words);
+  if (need & NEED_BITMAP) {
+    b->bitmap = w.take<uint64_t>((size_t)P.U * P.bm_words);
+    b->tpart = w.take<double>((size_t)P.U * P.nsplit * 2 * P.g.D);
+    b->mpart = w.take<double>((size_t)P.U * P.nsplit * 3);
+    b->evicted_sum = w.take<double>((size_t)P.U);
+    b->total_sum = w.take<double>((size_t)P.U);
+  }
   if (need & NEED_OFFSETS) b->kept_offsets = w.take<int64_t>((size_t)P.U + 1);
   return (w.off + 255) & ~(size_t)255;
 }
@@ -324,9 +341,6 @@ static certkv_status do_curves(const Plan& P, certkv_tensor v, const int32_t* pe
   a.v = v;
   a.dtype = P.dtype;
   a.curves = curves;
-  a.cmin = w.cmin;
-  a.cmin_stride = P.nblk_max;
-  a.cmax = w.cmax;
   a.vsum = vsum;
   for (const SeqTab& t : make_tabs(P, nullptr, 0.f)) TRY(run_curves(a, t, s));
   return CERTKV_OK;
@@ -334,17 +348,18 @@ static certkv_status do_curves(const Plan& P, certkv_tensor v, const int32_t* pe
 
 static certkv_status do_allocate(const Plan& P, const float* curves, const int32_t* n_keep,
                                  double alpha, int steps, int32_t* budgets, bool minmax,
-                                 const Bufs& w, hipStream_t s) {
+                                 const Bufs& w, hipStream_t s, int64_t* stats = nullptr) {
   AllocArgs a;
   a.g = P.g;
   a.curves = curves;
   a.cmin = w.cmin;
-  a.cmin_stride = P.nblk_max;
-  a.cmax = w.cmax;
+  a.cmaxb = w.cmaxb;
+  a.dmax = w.dmax;
+  a.nblk_max = P.nblk_max;
   a.steps = steps;
   a.budgets = budgets;
-  a.repairs = w.repairs;
-  a.need_minmax = minmax;
+  a.repairs = stats ? stats : w.repairs;
+  (void)minmax;
   for (const SeqTab& t : make_tabs(P, n_keep, alpha)) TRY(run_allocate(a, t, s));
   return CERTKV_OK;
 }
@@ -352,7 +367,7 @@ static certkv_status do_allocate(const Plan& P, const float* curves, const int32
 static certkv_status do_select(const Plan& P, const float* scores, const uint32_t* sorted_keys,
                                const int32_t* perm, int32_t* budgets, int mode, double retain,
                                int64_t* kept_offsets, int64_t* packed_offsets, int32_t* kept_idx,
-                               int64_t capacity, hipStream_t s) {
+                               int64_t capacity, const Bufs* fused, hipStream_t s) {
   const auto tabs = make_tabs(P, nullptr, 0.f);
   for (const SeqTab& t : tabs) {
     if (mode == CERTKV_SELECT_COVERAGE)
@@ -371,8 +386,10 @@ static certkv_status do_select(const Plan& P, const float* scores, const uint32_
   a.packed_offsets = packed_offsets;
   a.kept_idx = kept_idx;
   a.capacity = capacity;
-  a.evicted_sum = nullptr;
-  a.total_sum = nullptr;
+  a.evicted_sum = fused ? fused->evicted_sum : nullptr;
+  a.total_sum = fused ? fused->total_sum : nullptr;
+  a.bitmap = fused ? fused->bitmap : nullptr;
+  a.bm_stride = P.bm_words;
   for (const SeqTab& t : tabs) TRY(run_select(a, t, s));
   return CERTKV_OK;
 }
@@ -381,8 +398,8 @@ static certkv_status do_tail(const Plan& P, const float* scores, certkv_tensor k
                              const int64_t* kept_offsets, const int32_t* kept_idx,
                              const double* ksum, const double* vsum, float* k_star, float* v_star,
                              double* tail_mass, void* k_packed, void* v_packed,
-                             int32_t* pos_packed, bool do_tail, bool do_compact, const Bufs& w,
-                             hipStream_t s) {
+                             int32_t* pos_packed, bool do_tail, bool do_compact, bool fused,
+                             const Bufs& w, hipStream_t s) {
   TailArgs a;
   a.g = P.g;
   a.dtype = P.dtype;
@@ -393,7 +410,11 @@ static certkv_status do_tail(const Plan& P, const float* scores, certkv_tensor k
   a.kept_idx = kept_idx;
   a.bitmap = w.bitmap;
   a.bm_stride = P.bm_words;
-  a.build_bitmap = do_tail;
+  a.nsplit = P.nsplit;
+  a.kpart = w.tpart;
+  a.mpart = w.mpart;
+  a.evicted_sum = fused ? w.evicted_sum : nullptr;
+  a.total_sum = fused ? w.total_sum : nullptr;
   a.ksum = ksum;
   a.vsum = vsum;
   a.k_star = k_star;
@@ -405,7 +426,7 @@ static certkv_status do_tail(const Plan& P, const float* scores, certkv_tensor k
   a.do_tail = do_tail;
   a.do_compact = do_compact;
   const auto tabs = make_tabs(P, nullptr, 0.f);
-  if (do_tail) {
+  if (do_tail && !fused) {
     bool first = true;
     for (const SeqTab& t : tabs) {
       TRY(run_bitmap(a, t, P.U * (int64_t)P.bm_words, first, s));
@@ -516,7 +537,7 @@ certkv_status certkv_select(const certkv_problem* p, const float* scores, int32_
   hipStream_t s = (hipStream_t)stream;
   TRY(do_sort(P, scores, w.perm, w, s));
   return do_select(P, scores, w.keysA, w.perm, budgets_io, mode, retain_mass, kept_offsets,
-                   nullptr, kept_idx, kept_capacity, s);
+                   nullptr, kept_idx, kept_capacity, nullptr, s);
 }
 
 certkv_status certkv_tail_summary(const certkv_problem* p, const float* scores, certkv_tensor k,
@@ -536,7 +557,7 @@ certkv_status certkv_tail_summary(const certkv_problem* p, const float* scores, 
   const bool comp = ksum && vsum;
   return do_tail(P, scores, k, v, kept_offsets, kept_idx, comp ? ksum : nullptr,
                  comp ? vsum : nullptr, k_star, v_star, tail_mass, nullptr, nullptr, nullptr, true,
-                 false, w, (hipStream_t)stream);
+                 false, false, w, (hipStream_t)stream);
 }
 
 certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k, certkv_tensor v,
@@ -558,8 +579,8 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k, certkv_te
   Bufs w;
   TRY(run_packed_from_kept(P.U, kept_offsets, packed_offsets, s));
   TRY(do_tail(P, nullptr, k, v, kept_offsets, kept_idx, nullptr, nullptr, const_cast<float*>(k_star),
-              const_cast<float*>(v_star), nullptr, k_packed, v_packed, pos_packed, false, true, w,
-              s));
+              const_cast<float*>(v_star), nullptr, k_packed, v_packed, pos_packed, false, true,
+              false, w, s));
   return CERTKV_OK;
 }
 
@@ -591,12 +612,12 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, cert
   TRY(do_score(P, q_win, k, out->scores, w.ksum, w, s));
   TRY(do_sort(P, out->scores, pm, w, s));
   TRY(do_curves(P, v, pm, cv, w.vsum, w, s));
-  TRY(do_allocate(P, cv, n_keep_host, alpha, steps, out->budgets, false, w, s));
+  TRY(do_allocate(P, cv, n_keep_host, alpha, steps, out->budgets, false, w, s, out->alloc_stats));
   TRY(do_select(P, out->scores, w.keysA, pm, out->budgets, CERTKV_SELECT_BUDGET, 0.0,
-                out->kept_offsets, out->packed_offsets, out->kept_idx, cap, s));
+                out->kept_offsets, out->packed_offsets, out->kept_idx, cap, &w, s));
   return do_tail(P, out->scores, k, v, out->kept_offsets, out->kept_idx, w.ksum, w.vsum,
                  out->k_star, out->v_star, out->tail_mass, out->k_packed, out->v_packed,
-                 out->pos_packed, true, true, w, s);
+                 out->pos_packed, true, true, true, w, s);
 }
 
 certkv_status certkv_profile_enable(int32_t enable) {

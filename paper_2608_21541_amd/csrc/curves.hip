@@ -14,8 +14,8 @@
 //              x = m * (local Q of its dims) - |its W dims|^2,
 //            lane 0 adds m * Q_carry, and a transpose-reduce over the 64
 //            lanes yields c^2 for 16 ranks at a time.
-// Besides c (fp32), the kernel emits per-256-rank block minima and the unit
-// maximum of c (used by the allocation), and sum_j (s_j)_+ v_j.
+// Besides c (fp32), the kernel emits sum_j (s_j)_+ v_j (the value total of the
+// tail summary).
 #include "stages.h"
 
 namespace certkv {
@@ -24,8 +24,6 @@ constexpr int kCurveThreads = 512;
 constexpr int kCurveWaves = kCurveThreads / 64;
 constexpr int kRPW = 32;                          // ranks per wave and chunk
 constexpr int kCurveChunk = kCurveWaves * kRPW;   // 256 ranks
-constexpr int kCurveBlock = 256;                  // allocation block
-constexpr int kWavesPerBlock = kCurveBlock / kRPW;
 
 template <int DP>
 __device__ __forceinline__ void unpack_dims(uint32_t raw, float (&v)[DP]) {
@@ -41,14 +39,11 @@ template <int D, bool BF16>
 __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     Geo g, SeqTab st, const uint32_t* __restrict__ sorted_keys, const int32_t* __restrict__ perm,
     const double* __restrict__ ssum, const void* __restrict__ vc, int64_t v_sl, int64_t v_st,
-    int64_t v_sh, float* __restrict__ curves, float* __restrict__ cmin, int32_t cmin_stride,
-    float* __restrict__ cmax, double* __restrict__ vsum) {
+    int64_t v_sh, float* __restrict__ curves, double* __restrict__ vsum) {
   constexpr int DP = D / 64;
   __shared__ double tW[kCurveWaves][D];
   __shared__ double tQ[kCurveWaves];
   __shared__ double tM[kCurveWaves];
-  __shared__ float wmin[kCurveWaves];
-  __shared__ float wmax[kCurveWaves];
   __shared__ double a_lds[kCurveWaves][kRPW];
   __shared__ int32_t pos_lds[kCurveWaves][kRPW];
 
@@ -70,7 +65,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   double cW[DP], cQ = 0.0, cM = 0.0;
 #pragma unroll
   for (int t = 0; t < DP; ++t) cW[t] = 0.0;
-  float umax = -INFINITY;
 
   const int nch = (n + kCurveChunk - 1) / kCurveChunk;
   for (int k = nch - 1; k >= 0; --k) {
@@ -154,7 +148,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     double PL[DP];
 #pragma unroll
     for (int t = 0; t < DP; ++t) PL[t] = 0.0;
-    float lmin = INFINITY, lmax = -INFINITY;
 #pragma unroll
     for (int q4 = 0; q4 < kRPW / 16; ++q4) {
       double x[16];
@@ -200,32 +193,9 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       const int j = lane >> 2;
       const int rk = lo + kRPW - 1 - (q4 * 16 + j);
       const float c = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
-      if ((lane & 3) == 0 && rk < n) {
-        curves[base + rk] = c;
-        lmin = fminf(lmin, c);
-        lmax = fmaxf(lmax, c);
-      }
-    }
-    lmin = wave_min_f(lmin);
-    lmax = wave_max(lmax);
-    if (lane == 0) {
-      wmin[wave] = lmin;
-      wmax[wave] = lmax;
+      if ((lane & 3) == 0 && rk < n) curves[base + rk] = c;
     }
     __syncthreads();
-    // block minima of this chunk: block j is waves W-1-8j-7..W-1-8j
-    if (cmin && threadIdx.x < kCurveChunk / kCurveBlock) {
-      const int j = threadIdx.x;
-      const int blk = (k * kCurveChunk) / kCurveBlock + j;
-      if (blk * kCurveBlock < n) {
-        float mn = INFINITY;
-        for (int q = 0; q < kWavesPerBlock; ++q)
-          mn = fminf(mn, wmin[kCurveWaves - 1 - (kWavesPerBlock * j + q)]);
-        cmin[u * (int64_t)cmin_stride + blk] = mn;
-      }
-    }
-#pragma unroll
-    for (int w2 = 0; w2 < kCurveWaves; ++w2) umax = fmaxf(umax, wmax[w2]);
     // advance the chunk carry by every wave's totals, in wave order
     for (int w2 = 0; w2 < kCurveWaves; ++w2) {
 #pragma unroll
@@ -235,7 +205,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0 && cmax) cmax[u] = umax;
   if (vsum && wave == 0) {
 #pragma unroll
     for (int t = 0; t < DP; ++t) vsum[u * D + lane * DP + t] = cW[t] * tot;
@@ -249,16 +218,16 @@ certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
     if (a.g.D == 128)
       CERTKV_LAUNCH("curves", (curves_kernel<128, true>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.cmin, a.cmin_stride, a.cmax, a.vsum);
+                    a.curves, a.vsum);
     else
       CERTKV_LAUNCH("curves", (curves_kernel<64, true>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.cmin, a.cmin_stride, a.cmax, a.vsum);
+                    a.curves, a.vsum);
   } else {
     if (a.g.D != 64) return CERTKV_EUNSUPPORTED;
     CERTKV_LAUNCH("curves", (curves_kernel<64, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                   a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                  a.curves, a.cmin, a.cmin_stride, a.cmax, a.vsum);
+                  a.curves, a.vsum);
   }
   return CERTKV_OK;
 }

@@ -65,7 +65,8 @@ __global__ __launch_bounds__(256) void select_kernel(
     Geo g, SeqTab st, const float* __restrict__ scores, const uint32_t* __restrict__ sorted_keys,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ budgets,
     const int64_t* __restrict__ kept_offsets, int32_t* __restrict__ kept_idx, int64_t capacity,
-    double* __restrict__ evicted_sum, double* __restrict__ total_sum) {
+    double* __restrict__ evicted_sum, double* __restrict__ total_sum, uint64_t* __restrict__ bm,
+    int32_t bm_stride) {
   __shared__ int32_t wcount[4];
   __shared__ double dsum[2][4];
   const int h = blockIdx.x % g.H;
@@ -101,7 +102,11 @@ __global__ __launch_bounds__(256) void select_kernel(
     const uint64_t bal = __ballot(keep);
     const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-    if (lane == 0) wcount[wave] = __popcll(bal);
+    if (lane == 0) {
+      wcount[wave] = __popcll(bal);
+      const int word = (j0 >> 6) + wave;
+      if (bm && word < bm_stride) bm[u * bm_stride + word] = bal;
+    }
     __syncthreads();
     int64_t pre = run;
     for (int w = 0; w < wave; ++w) pre += wcount[w];
@@ -205,7 +210,8 @@ certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64
 certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s) {
   CERTKV_LAUNCH("select", select_kernel, dim3(a.g.H * st.count, a.g.L), dim3(256), 0, s, a.g, st,
                 a.scores, a.sorted_keys, a.perm, (const int32_t*)a.budgets,
-                (const int64_t*)a.kept_offsets, a.kept_idx, a.capacity, a.evicted_sum, a.total_sum);
+                (const int64_t*)a.kept_offsets, a.kept_idx, a.capacity, a.evicted_sum, a.total_sum,
+                a.bitmap, a.bm_stride);
   return CERTKV_OK;
 }
 

@@ -36,9 +36,6 @@ struct CurveArgs {
   certkv_tensor v;
   int32_t dtype;
   float* curves;
-  float* cmin;
-  int32_t cmin_stride;
-  float* cmax;
   double* vsum;
 };
 certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s);
@@ -46,13 +43,13 @@ certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s);
 struct AllocArgs {
   Geo g;
   const float* curves;
-  float* cmin;
-  int32_t cmin_stride;
-  float* cmax;
+  float* cmin;      // [U][nblk_max] block minima of c
+  float* cmaxb;     // [U][nblk_max] block maxima of c
+  double* dmax;     // [U][nblk_max] block maxima of c(i+1) - c(i)
+  int32_t nblk_max;
   int32_t steps;
   int32_t* budgets;
   int64_t* repairs;
-  bool need_minmax;
 };
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s);
 
@@ -68,6 +65,8 @@ struct SelectArgs {
   int64_t capacity;
   double* evicted_sum;
   double* total_sum;
+  uint64_t* bitmap;
+  int32_t bm_stride;
 };
 certkv_status run_coverage(const Geo& g, const SeqTab& st, const float* scores,
                            const uint32_t* sorted_keys, double retain, int32_t* budgets,
@@ -86,7 +85,11 @@ struct TailArgs {
   const int32_t* kept_idx;
   uint64_t* bitmap;
   int32_t bm_stride;
-  bool build_bitmap;
+  int32_t nsplit;            // gather workgroups per unit
+  double* kpart;             // [U][nsplit][2][D] partial kept sums
+  double* mpart;             // [U][nsplit][3] partial masses (standalone path)
+  const double* evicted_sum; // [U] from the selection pass, or NULL
+  const double* total_sum;   // [U] from the selection pass, or NULL
   const double* ksum;
   const double* vsum;
   float* k_star;

@@ -108,7 +108,7 @@ def test_dry_run_compress_and_select():
     L = _lib.lib()
     p = problem()
     ws, n = ws_for(p, _lib.STAGE_COMPRESS)
-    out = _lib.Outputs(*([FAKE] * 11 + [None, None]))
+    out = _lib.Outputs(*([FAKE] * 11 + [None, None, None]))
     nk = (ctypes.c_int32 * 2)(101, 71)
     assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), nk, 0.2, 40,
                              ctypes.byref(out), ws, n, None) == _lib.CERTKV_OK

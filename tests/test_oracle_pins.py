@@ -588,3 +588,43 @@ def test_compress_block_invariants():
         qpos = np.repeat(n - w + np.arange(w), G)
         np.testing.assert_allclose(out["s"][h], oracle.scores(qh, qpos, k[:, h], 1 / math.sqrt(d)),
                                    rtol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# The one-token repair (Algorithm 1: "repair one token at a time") as a
+# selection problem.  Greedy: repeatedly take the head whose next marginal
+# d = c(b+1) - c(b) is smallest, ties to the lowest head.  Claim used by the
+# GPU allocator: the greedy consumes elements in increasing order of the key
+# (running max of the head's marginals up to that element, head, position).
+# Checked here against the oracle's sequential repair on random curves.
+
+def _keyed_repair(c, start, R):
+    H, n = c.shape
+    keys = []
+    for h in range(H):
+        run = -math.inf
+        for i in range(int(start[h]), n - 1):
+            run = max(run, float(c[h, i + 1]) - float(c[h, i]))
+            keys.append((run, h, i))
+    keys.sort()
+    b = np.array(start, dtype=np.int64)
+    for _, h, _ in keys[:R]:
+        b[h] += 1
+    return b
+
+
+def test_repair_equals_running_max_key_order():
+    rng = np.random.default_rng(18)
+    for trial in range(300):
+        H, n = int(rng.integers(1, 6)), int(rng.integers(3, 30))
+        n_keep = int(rng.integers(2, n + 1))
+        # few distinct levels so that ties between heads and within runs occur
+        c = rng.integers(0, 4, (H, n)).astype(np.float32) * 0.5
+        if trial % 3 == 0:
+            c = np.sort(c, axis=1)[:, ::-1].copy()
+        br, bm = oracle.budget_params(H, n, n_keep)
+        b_seq, rep = oracle.allocate(c, n_keep, steps=0)  # start = b_min everywhere
+        start = np.full(H, bm)
+        R = br - H * bm
+        assert rep == R
+        assert _keyed_repair(c, start, R).tolist() == b_seq.tolist()
