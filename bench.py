@@ -31,14 +31,18 @@ def algorithmic_model(cfg, n_keep):
 
     Per (KV head, token) unit with d = head_dim, e = element bytes, keep
     fraction f = (n_keep - 1) / n:
-      score pass 1       K read                                  d*e
-      score pass 2       K read + score write                    d*e + 4
-      sort               score read + order write                4 + 4
-      curves             V gathered + order + key + curve write  d*e + 12
-      allocate           curve read                              4
-      select             score read + kept index write           4 + 4f
-      tail + compact     score read + kept K,V read and written  4 + f*(4*d*e + 4)
+      score pass 1          K read                                   d*e
+      score pass 2          K read + score write                     d*e + 4
+      sort                  score read + order write                 4 + 4
+      curves                V gathered + order + key + curve write   d*e + 12
+      curve block stats     curve read                               4
+      allocate              curve read                               4
+      select                score read + kept index write + bitmap   4 + 4f + 1/8
+      tail+compact gather   kept index, score, K, V read; K, V and
+                            position written                          f*(4*d*e + 12)
     MFMA flops of each scoring pass: 2 * M * d per (head, token), M = w*G.
+    Small per-unit kernels (row combines, offsets, slot finalize) are
+    modelled by their per-unit traffic only.
     """
     L, H, D = cfg.layers, cfg.kv_heads, cfg.head_dim
     e = 2 if cfg.dtype_name == "bf16" else 4
@@ -50,9 +54,10 @@ def algorithmic_model(cfg, n_keep):
         "score_pass2_mfma": (D * e + 4, 2 * M * D),
         "sort_segments": (8, 0),
         "curves": (D * e + 12, 0),
+        "curve_blockstats": (4, 0),
         "allocate": (4, 0),
-        "select": (4 + 4 * f, 0),
-        "tail_compact": (4 + f * (4 * D * e + 4), 0),
+        "select": (4 + 4 * f + 0.125, 0),
+        "tail_compact_gather": (f * (4 * D * e + 12), 0),
     }
     return {k: (b * ht, fl * ht) for k, (b, fl) in per.items()}, ht
 

@@ -57,7 +57,8 @@ typedef int32_t certkv_status;
 enum {
   CERTKV_OK = 0,
   CERTKV_EINVAL = -1,       /* null pointer, bad size, stride or flag      */
-  CERTKV_EUNSUPPORTED = -2, /* head_dim not 64/128, or dtype not built     */
+  CERTKV_EUNSUPPORTED = -2, /* head_dim not 64/128, dtype not built, or a  */
+                            /* per-head slice spanning 4 GiB or more      */
   CERTKV_EINFEASIBLE = -3,  /* n_keep < 2 or n_keep > n_b (budget algebra) */
   CERTKV_EWORKSPACE = -5,   /* workspace smaller than required             */
   CERTKV_EHIP = -6          /* a HIP runtime call or launch failed         */
@@ -88,7 +89,9 @@ enum {
 
 /* A strided [L][tokens][heads][head_dim] tensor.  Strides are in ELEMENTS;
  * the head_dim axis is contiguous.  The pointer must be 16-byte aligned and
- * every stride a multiple of 8 elements. */
+ * every stride a multiple of 8 elements.  The rows of one (layer, head,
+ * sequence) must span less than 4 GiB ((n_max - 1) * s_token + head_dim
+ * elements), else CERTKV_EUNSUPPORTED. */
 typedef struct certkv_tensor {
   const void* ptr;
   int64_t s_layer;

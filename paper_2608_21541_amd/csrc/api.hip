@@ -102,6 +102,7 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.cu = cu;
   int kpb = 256;
   if (P.dtype == CERTKV_BF16) {
+    kpb = 512;
     while (kpb < 4096 && P.U * ((max_len + 2 * kpb - 1) / (2 * kpb)) >= 2048) kpb *= 2;
   }
   P.kpb = kpb;
@@ -119,7 +120,11 @@ static certkv_status check_tensor(const certkv_tensor& t, const Plan& P) {
   if (((uintptr_t)t.ptr & 15u) != 0) return CERTKV_EINVAL;
   if ((t.s_layer % 8) || (t.s_token % 8) || (t.s_head % 8)) return CERTKV_EINVAL;
   if (t.s_layer < 0 || t.s_token < 0 || t.s_head < 0) return CERTKV_EINVAL;
-  (void)P;
+  // the rows of one (layer, head, sequence) are addressed with 32-bit byte
+  // offsets from the slice start
+  const int64_t esz = P.dtype == CERTKV_BF16 ? 2 : 4;
+  if (((int64_t)(P.max_len - 1) * t.s_token + P.g.D) * esz > (int64_t)0xFFFFFFFFLL)
+    return CERTKV_EUNSUPPORTED;
   return CERTKV_OK;
 }
 
@@ -182,6 +187,7 @@ struct Bufs {
   float2* part = nullptr;
   float* lse2 = nullptr;
   float* kpart = nullptr;
+  int32_t* flag = nullptr;
   double* ksum = nullptr;
   // order / curves / allocation
   uint32_t *keysA = nullptr, *keysB = nullptr;
@@ -223,6 +229,7 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
     b->part = w.take<float2>((size_t)P.U * P.nkb_max * P.M);
     b->lse2 = w.take<float>((size_t)P.U * P.M);
     b->kpart = w.take<float>((size_t)P.U * P.nkb_max * P.g.D);
+    b->flag = w.take<int32_t>((size_t)P.U);
   }
   if (need & NEED_KSUM) {
     b->ksum = w.take<double>((size_t)P.U * P.g.D);
@@ -305,6 +312,7 @@ static certkv_status do_score(const Plan& P, certkv_tensor q, certkv_tensor k, f
   a.part = w.part;
   a.lse2 = w.lse2;
   a.kpart = w.kpart;
+  a.flag = w.flag;
   a.keys_per_block = P.dtype == CERTKV_BF16 ? P.kpb : 256;
   a.nkb_max = P.dtype == CERTKV_BF16 ? P.nkb_max : (P.max_len + 255) / 256;
   for (const SeqTab& t : make_tabs(P, nullptr, 0.f)) {

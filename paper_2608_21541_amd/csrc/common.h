@@ -39,6 +39,24 @@ __device__ __forceinline__ int64_t lht_base(const Geo& g, int l, int h, int64_t 
   return ((int64_t)l * g.H + h) * g.T + tok0;
 }
 
+// Raw buffer resource over [base, base + bytes): loads through it take a
+// uniform 64-bit base and a 32-bit per-lane byte offset, and return zero for
+// offsets at or beyond `bytes` (hardware range check).
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t buf_load_u32(BufRsrc r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint32_t buf_load_u16(BufRsrc r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint2 buf_load_u64(BufRsrc r, uint32_t off) {
+  auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+  return make_uint2(v[0], v[1]);
+}
+
 // bf16 <-> fp32.  bf16 is the upper half of an IEEE binary32.
 __device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t packed) { return __uint_as_float(packed & 0xffff0000u); }

@@ -1,37 +1,46 @@
 // Dispersion curves c(b) = sqrt((m Q - |W|^2)_+) over the evicted suffix of
-// the score order (the keys at ranks b..n-1), for b = 0..n-1, in fp64.
+// the score order (the keys at ranks b..n-1), for b = 0..n-1, in fp64, with
+// m, W and Q the suffix sums of a, a v and a |v|^2.
 //
-// One workgroup (8 waves) per unit walks the ranks from the top (rank n-1)
-// down in chunks of 256.  Wave w owns the 32 ranks
-// [256k + 32(7-w), 256k + 32(8-w)) of chunk k and lane i owns dims
-// DP*i..DP*i+DP-1 (DP = d/64):
-//   phase 1  each wave gathers its 32 value rows (by perm) into VGPRs and
-//            forms its totals m, W (per dim) and Q;
+// One workgroup (16 waves) per unit walks the ranks from the top (rank n-1)
+// down in chunks of 256.  Wave w owns the 16 ranks [256k + 16(15-w),
+// 256k + 16(16-w)) of chunk k and lane i owns dims DP*i..DP*i+DP-1
+// (DP = d/64).  Per chunk:
+//   phase 1  each wave forms the totals of its 16 rows: m, W (per dim) and
+//            Q (sum of a |v|^2);
 //   carry    wave w starts from the chunk carry plus the totals of waves
-//            0..w-1 (higher ranks), summed in that fixed order;
-//   phase 2  the wave walks its ranks top-down extending m and W and the
-//            local part of Q; per rank each lane forms
-//              x = m * (local Q of its dims) - |its W dims|^2,
-//            lane 0 adds m * Q_carry, and a transpose-reduce over the 64
-//            lanes yields c^2 for 16 ranks at a time.
-// Besides c (fp32), the kernel emits sum_j (s_j)_+ v_j (the value total of the
+//            0..w-1 (higher ranks), added in that fixed order (deterministic);
+//   phase 2  the wave walks its ranks top-down extending m, W and the
+//            lane-local part q of Q; per rank each lane forms
+//            x = m q - |W|^2 over its dims (lane 0 adds m * Q_carry) and a
+//            transpose-reduce over the 64 lanes, folded in as the ranks are
+//            produced, yields c^2 of all 16 ranks.  The last wave's final
+//            state is the carry of the next chunk.
+// The gathers are software-pipelined: while chunk k is computed, the value
+// rows of chunk k-1 are in flight and the order/score entries of chunk k-2
+// are being fetched.  Also emitted: sum_j (s_j)_+ v_j (the value total of the
 // tail summary).
 #include "stages.h"
 
 namespace certkv {
 
-constexpr int kCurveThreads = 512;
+constexpr int kCurveThreads = 1024;
 constexpr int kCurveWaves = kCurveThreads / 64;
-constexpr int kRPW = 32;                          // ranks per wave and chunk
+constexpr int kRPW = 16;                          // ranks per wave and chunk
 constexpr int kCurveChunk = kCurveWaves * kRPW;   // 256 ranks
 
-template <int DP>
-__device__ __forceinline__ void unpack_dims(uint32_t raw, float (&v)[DP]) {
-  if (DP == 2) {
-    v[0] = bf16_lo(raw);
-    v[DP - 1] = bf16_hi(raw);
+template <int DP, bool BF16>
+__device__ __forceinline__ void unpack_dims(uint32_t raw0, uint32_t raw1, float (&v)[DP]) {
+  if (BF16) {
+    if (DP == 2) {
+      v[0] = bf16_lo(raw0);
+      v[DP - 1] = bf16_hi(raw0);
+    } else {
+      v[0] = bf16_lo(raw0);
+    }
   } else {
-    v[0] = bf16_lo(raw);
+    v[0] = __uint_as_float(raw0);
+    if (DP == 2) v[DP - 1] = __uint_as_float(raw1);
   }
 }
 
@@ -41,11 +50,16 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     const double* __restrict__ ssum, const void* __restrict__ vc, int64_t v_sl, int64_t v_st,
     int64_t v_sh, float* __restrict__ curves, double* __restrict__ vsum) {
   constexpr int DP = D / 64;
-  __shared__ double tW[kCurveWaves][D];
+  constexpr int RAW = (BF16 || DP == 1) ? 1 : 2;  // 32-bit words per lane per row
+  __shared__ double tW[kCurveWaves][D];   // phase-1 totals per wave
   __shared__ double tQ[kCurveWaves];
   __shared__ double tM[kCurveWaves];
   __shared__ double a_lds[kCurveWaves][kRPW];
-  __shared__ int32_t pos_lds[kCurveWaves][kRPW];
+  // chunk carry (suffix sums above the chunk), double-buffered by chunk
+  // parity: the last wave writes the next carry while others may still read
+  // the current one
+  __shared__ double cW[2][D];
+  __shared__ double cQM[2][2];
 
   const int h = blockIdx.x % g.H;
   const int bl = blockIdx.x / g.H;
@@ -60,157 +74,203 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   const int wave = threadIdx.x >> 6;
   const double tot = ssum[u];
   const double inv_n = 1.0 / (double)n;
+  // Value slice of this (layer, head, sequence): rows of d elements, token
+  // stride v_st; the host guarantees it spans less than 4 GiB.
+  constexpr int E = BF16 ? 2 : 4;
+  const BufRsrc vrs = make_rsrc(
+      static_cast<const char*>(vc) + ((int64_t)l * v_sl + tok0 * v_st + (int64_t)h * v_sh) * E,
+      (uint32_t)(((int64_t)(n - 1) * v_st + D) * E));
+  const uint32_t vrow_bytes = (uint32_t)(v_st * E);
+  const uint32_t vlane = (uint32_t)(lane * DP * E);
+  const BufRsrc krs = make_rsrc(sorted_keys + base, (uint32_t)n * 4u);
+  const BufRsrc prs = make_rsrc(perm + base, (uint32_t)n * 4u);
 
-  // chunk carry (identical in every wave)
-  double cW[DP], cQ = 0.0, cM = 0.0;
+  // rank of lane r (< kRPW) of this wave in chunk k; lane 0 = highest rank
+  auto rank_of = [&](int k, int r) {
+    return k * kCurveChunk + (kCurveWaves - 1 - wave) * kRPW + kRPW - 1 - r;
+  };
+  // Order entry and radix key of lane r of chunk k.  Every lane loads (from a
+  // clamped, in-bounds rank) so that no branch splits the pipelined loads;
+  // `valid` marks the lanes that hold a real rank of this wave.  The weight
+  // is formed one iteration later, when the loads have landed.
+  auto fetch_meta = [&](int k, uint32_t& key, int& pos, bool& valid) {
+    const int rk = rank_of(k, lane);
+    valid = k >= 0 && lane < kRPW && rk < n;
+    const uint32_t idx = (uint32_t)min(max(rk, 0), n - 1) * 4u;
+    key = buf_load_u32(krs, idx);
+    pos = (int)buf_load_u32(prs, idx);
+  };
+  // weight a = (s)_+ / sum (s)_+ (uniform when every score is zero); zero for
+  // absent ranks, whose rows then add nothing
+  auto weight = [&](uint32_t key, bool valid) -> double {
+    if (!valid) return 0.0;
+    const float s = desc_key_value(key);
+    return tot > 0.0 ? (s > 0.f ? (double)s / tot : 0.0) : inv_n;
+  };
+  auto row_of = [&](int pos, bool valid) { return valid ? min(max(pos, 0), n - 1) : 0; };
+  // Value rows of the 16 ranks of chunk k (row 0 stands in for absent ranks,
+  // whose weight is zero).
+  auto fetch_rows = [&](int pos, uint32_t (&raw)[kRPW][RAW]) {
 #pragma unroll
-  for (int t = 0; t < DP; ++t) cW[t] = 0.0;
+    for (int r = 0; r < kRPW; ++r) {
+      const int pr = __shfl(pos, r, 64);
+      const uint32_t off = (uint32_t)pr * vrow_bytes + vlane;
+      if (RAW == 2) {
+        const uint2 w2 = buf_load_u64(vrs, off);
+        raw[r][0] = w2.x;
+        raw[r][RAW - 1] = w2.y;
+      } else if (BF16 && DP == 1) {
+        raw[r][0] = buf_load_u16(vrs, off);
+      } else {
+        raw[r][0] = buf_load_u32(vrs, off);
+      }
+    }
+  };
 
   const int nch = (n + kCurveChunk - 1) / kCurveChunk;
+  for (int i = threadIdx.x; i < D; i += kCurveThreads) cW[(nch - 1) & 1][i] = 0.0;
+  if (threadIdx.x < 2) cQM[(nch - 1) & 1][threadIdx.x] = 0.0;
+
+  double a_cur, a_n1;
+  int p_cur, p_n1, p_n2;
+  uint32_t k_cur, k_n1, k_n2;
+  bool ok_cur, ok_n1, ok_n2;
+  uint32_t vcur[kRPW][RAW], vnext[kRPW][RAW];
+  fetch_meta(nch - 1, k_cur, p_cur, ok_cur);
+  fetch_meta(nch - 2, k_n1, p_n1, ok_n1);
+  a_cur = weight(k_cur, ok_cur);
+  a_n1 = weight(k_n1, ok_n1);
+  p_cur = row_of(p_cur, ok_cur);
+  p_n1 = row_of(p_n1, ok_n1);
+  fetch_rows(p_cur, vcur);
+
   for (int k = nch - 1; k >= 0; --k) {
-    const int lo = k * kCurveChunk + (kCurveWaves - 1 - wave) * kRPW;  // lowest rank of wave
-    const int rank = lo + kRPW - 1 - lane;  // lane 0 = highest rank of the sub-chunk
-    const bool live = lane < kRPW && rank < n;
-    // weights a = (s)_+ / sum (s)_+ (uniform when every score is zero)
-    double a = 0.0;
-    int32_t pos = 0;
-    if (live) {
-      const float s = desc_key_value(sorted_keys[base + rank]);
-      pos = min(max(perm[base + rank], 0), n - 1);
-      a = tot > 0.0 ? (s > 0.f ? (double)s / tot : 0.0) : inv_n;
-    }
-    if (lane < kRPW) {
-      a_lds[wave][lane] = a;
-      pos_lds[wave][lane] = pos;
-    }
-    // gather the value rows, lane i holding dims DP*i..
-    uint32_t vraw[kRPW];
+    // pipeline: order entries two chunks ahead, value rows one chunk ahead
+    fetch_meta(k - 2, k_n2, p_n2, ok_n2);
+    fetch_rows(p_n1, vnext);
+    if (lane < kRPW) a_lds[wave][lane] = a_cur;
+    __builtin_amdgcn_wave_barrier();
+
+    // phase 1: totals of the wave's rows
+    {
+      double sW[DP], sQ = 0.0, sM = 0.0;
 #pragma unroll
-    for (int r = 0; r < kRPW; ++r) {
-      const int pr = pos_lds[wave][r];
-      const bool lr = (lo + kRPW - 1 - r) < n;
-      vraw[r] = 0u;
-      if (lr) {
-        const int64_t off = (int64_t)l * v_sl + (tok0 + pr) * v_st + (int64_t)h * v_sh + lane * DP;
-        if (BF16) {
-          const uint16_t* vp = static_cast<const uint16_t*>(vc) + off;
-          vraw[r] = DP == 2 ? *reinterpret_cast<const uint32_t*>(vp) : (uint32_t)vp[0];
-        } else {
-          const float* vp = static_cast<const float*>(vc) + off;
-          vraw[r] = __float_as_uint(vp[0]);  // fp32 values: one dim per lane (d = 64)
+      for (int t = 0; t < DP; ++t) sW[t] = 0.0;
+#pragma unroll
+      for (int r = 0; r < kRPW; ++r) {
+        const double ar = a_lds[wave][r];
+        float v[DP];
+        unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
+        double vv = 0.0;
+#pragma unroll
+        for (int t = 0; t < DP; ++t) {
+          const double vd = (double)v[t];
+          sW[t] = fma(ar, vd, sW[t]);
+          vv = fma(vd, vd, vv);
         }
+        sQ = fma(ar, vv, sQ);
+        sM += ar;
       }
-    }
-    // phase 1: sub-chunk totals
-    double sW[DP], sP = 0.0, sM = 0.0;
+      sQ = wave_sum(sQ);
 #pragma unroll
-    for (int t = 0; t < DP; ++t) sW[t] = 0.0;
-#pragma unroll
-    for (int r = 0; r < kRPW; ++r) {
-      const double ar = a_lds[wave][r];
-      float v[DP];
-      if (BF16) {
-        unpack_dims<DP>(vraw[r], v);
-      } else {
-        v[0] = __uint_as_float(vraw[r]);
+      for (int t = 0; t < DP; ++t) tW[wave][lane * DP + t] = sW[t];
+      if (lane == 0) {
+        tQ[wave] = sQ;
+        tM[wave] = sM;
       }
-      sM += ar;
-#pragma unroll
-      for (int t = 0; t < DP; ++t) {
-        const double p = ar * (double)v[t];
-        sW[t] += p;
-        sP += p * (double)v[t];
-      }
-    }
-    sP = wave_sum(sP);
-#pragma unroll
-    for (int t = 0; t < DP; ++t) tW[wave][lane * DP + t] = sW[t];
-    if (lane == 0) {
-      tQ[wave] = sP;
-      tM[wave] = sM;
     }
     __syncthreads();
     // carry of this wave: chunk carry + totals of the waves above it
-    double W[DP], m = cM, Qc = cQ;
+    const int par = k & 1;
+    double W[DP], m = cQM[par][1], Qc = cQM[par][0];
 #pragma unroll
-    for (int t = 0; t < DP; ++t) W[t] = cW[t];
+    for (int t = 0; t < DP; ++t) W[t] = cW[par][lane * DP + t];
     for (int w2 = 0; w2 < wave; ++w2) {
 #pragma unroll
       for (int t = 0; t < DP; ++t) W[t] += tW[w2][lane * DP + t];
       Qc += tQ[w2];
       m += tM[w2];
     }
-    // Opaque to the optimizer: keeps the rows packed in 32-bit registers
-    // between the phases instead of holding 2*kRPW converted doubles.
+    // Opaque to the optimizer: keeps the rows packed between the phases
+    // instead of holding their converted doubles.
 #pragma unroll
-    for (int r = 0; r < kRPW; ++r) __asm__ volatile("" : "+v"(vraw[r]));
-    // phase 2: walk the wave's ranks top-down, 16 at a time
-    double PL[DP];
+    for (int r = 0; r < kRPW; ++r) {
+      __asm__ volatile("" : "+v"(vcur[r][0]));
+      if (RAW == 2) __asm__ volatile("" : "+v"(vcur[r][RAW - 1]));
+    }
+    // phase 2: walk the ranks top-down.  Streaming transpose-reduce of the
+    // per-lane values over lane bits 5..2: ranks 2i and 2i+1 combine over
+    // lane bit 5 as soon as both exist, pairs of those over bit 4, and so on,
+    // so at most one pending value per level is live.  Lane bits (5, 4, 3, 2)
+    // end up naming rank bits (0, 1, 2, 3).
+    double q = 0.0;
+    double pend[4];
+    double c2 = 0.0;
 #pragma unroll
-    for (int t = 0; t < DP; ++t) PL[t] = 0.0;
+    for (int r = 0; r < kRPW; ++r) {
+      const double ar = a_lds[wave][r];
+      float v[DP];
+      unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
+      double vv = 0.0, w2 = 0.0;
 #pragma unroll
-    for (int q4 = 0; q4 < kRPW / 16; ++q4) {
-      double x[16];
+      for (int t = 0; t < DP; ++t) {
+        const double vd = (double)v[t];
+        W[t] = fma(ar, vd, W[t]);
+        w2 = fma(W[t], W[t], w2);
+        vv = fma(vd, vd, vv);
+      }
+      m += ar;
+      q = fma(ar, vv, q);
+      double cur = fma(m, q, -w2);
+      if (lane == 0) cur = fma(m, Qc, cur);
+      bool placed = false;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int r = q4 * 16 + j;
-        const double ar = a_lds[wave][r];
-        float v[DP];
-        if (BF16) {
-          unpack_dims<DP>(vraw[r], v);
+      for (int lev = 0; lev < 4; ++lev) {
+        if (placed) continue;
+        if (((r >> lev) & 1) == 0) {
+          pend[lev] = cur;
+          placed = true;
         } else {
-          v[0] = __uint_as_float(vraw[r]);
-        }
-        m += ar;
-        double xl = 0.0, pl = 0.0;
-#pragma unroll
-        for (int t = 0; t < DP; ++t) {
-          const double p = ar * (double)v[t];
-          W[t] += p;
-          PL[t] += p * (double)v[t];
-          pl += PL[t];
-          xl -= W[t] * W[t];
-        }
-        xl += m * pl;
-        if (lane == 0) xl += m * Qc;
-        x[j] = xl;
-      }
-      // transpose-reduce 16 values over lane bits 5..2, then sum lane bits 1..0
-#pragma unroll
-      for (int msk = 32, half = 8; msk >= 4; msk >>= 1, half >>= 1) {
-        const bool up = (lane & msk) != 0;
-#pragma unroll
-        for (int i = 0; i < half; ++i) {
-          double keep = up ? x[half + i] : x[i];
-          double send = up ? x[i] : x[half + i];
-          x[i] = keep + __shfl_xor(send, msk, 64);
+          const int msk = 32 >> lev;
+          const bool up = (lane & msk) != 0;
+          const double keep = up ? cur : pend[lev];
+          const double send = up ? pend[lev] : cur;
+          cur = keep + __shfl_xor(send, msk, 64);
         }
       }
-      double c2 = x[0];
-      c2 += __shfl_xor(c2, 1, 64);
-      c2 += __shfl_xor(c2, 2, 64);
-      // value index held = lane bits 5..2 -> j = lane >> 2 within this group of 16
-      const int j = lane >> 2;
-      const int rk = lo + kRPW - 1 - (q4 * 16 + j);
-      const float c = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
-      if ((lane & 3) == 0 && rk < n) curves[base + rk] = c;
+      if (!placed) c2 = cur;
     }
-    __syncthreads();
-    // advance the chunk carry by every wave's totals, in wave order
-    for (int w2 = 0; w2 < kCurveWaves; ++w2) {
+    c2 += __shfl_xor(c2, 1, 64);
+    c2 += __shfl_xor(c2, 2, 64);
+    const int r_mine = ((lane >> 5) & 1) | (((lane >> 4) & 1) << 1) | (((lane >> 3) & 1) << 2) |
+                       (((lane >> 2) & 1) << 3);
+    const int rk = rank_of(k, r_mine);
+    if ((lane & 3) == 0 && rk < n) curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
+    // the last wave's final state carries into the next chunk
+    if (wave == kCurveWaves - 1) {
 #pragma unroll
-      for (int t = 0; t < DP; ++t) cW[t] += tW[w2][lane * DP + t];
-      cQ += tQ[w2];
-      cM += tM[w2];
+      for (int t = 0; t < DP; ++t) cW[par ^ 1][lane * DP + t] = W[t];
+      if (lane == 0) {
+        cQM[par ^ 1][0] = Qc + tQ[wave];
+        cQM[par ^ 1][1] = m;
+      }
     }
     __syncthreads();
+    // rotate the pipeline
+#pragma unroll
+    for (int r = 0; r < kRPW; ++r) {
+      vcur[r][0] = vnext[r][0];
+      if (RAW == 2) vcur[r][RAW - 1] = vnext[r][RAW - 1];
+    }
+    a_cur = a_n1;
+    a_n1 = weight(k_n2, ok_n2);
+    p_n1 = row_of(p_n2, ok_n2);
   }
   if (vsum && wave == 0) {
 #pragma unroll
-    for (int t = 0; t < DP; ++t) vsum[u * D + lane * DP + t] = cW[t] * tot;
+    for (int t = 0; t < DP; ++t) vsum[u * D + lane * DP + t] = cW[1][lane * DP + t] * tot;
   }
 }
-
 
 certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
   dim3 grid(a.g.H * st.count, a.g.L);
@@ -224,10 +284,14 @@ certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
                     a.curves, a.vsum);
   } else {
-    if (a.g.D != 64) return CERTKV_EUNSUPPORTED;
-    CERTKV_LAUNCH("curves", (curves_kernel<64, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                  a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                  a.curves, a.vsum);
+    if (a.g.D == 128)
+      CERTKV_LAUNCH("curves", (curves_kernel<128, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
+                    a.curves, a.vsum);
+    else
+      CERTKV_LAUNCH("curves", (curves_kernel<64, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
+                    a.curves, a.vsum);
   }
   return CERTKV_OK;
 }

@@ -3,16 +3,22 @@
 // For KV head h the M = w*G window rows (query head g of the group, window
 // position q) give logits l = scale * <q_row, k_j>; the score of key j is the
 // sum over rows of the row-softmax weight of key j.  Two passes over K:
-//   pass 1  per key block: running (max, sum of exp) of every row -> partials
-//   combine per row: log-sum-exp over blocks
-//   pass 2  per key block: s_j = sum_rows exp(l_row,j - lse_row), written out,
-//           plus (optionally) the block's sum_j s_j k_j for the tail summary.
+//   pass 1   per key block: sum over the block of exp2(l * log2 e) per row;
+//   combine  per row: log2 of the sum over blocks;
+//   pass 2   per key block: s_j = sum_rows exp2(l_row,j * log2 e - lse2_row),
+//            written out, plus (optionally) the block's sum_j s_j k_j.
+// Pass 1 sums exponentials without a running maximum, so partial sums of
+// different blocks add directly.  A row whose total falls outside
+// [2^-60, 2^120] (where fp32 exponentials could under- or overflow) flags its
+// unit, and a fallback pass recomputes that unit's partials with a running
+// maximum; it returns immediately for units that are not flagged.
 // The contraction runs on MFMA v_mfma_f32_16x16x32_bf16 with key tiles as the
 // A operand (rows = 16 keys, held in VGPRs straight from HBM) and the window
 // queries as the B operand (columns = 16 queries, staged once per workgroup in
-// LDS).  Each lane then owns one query column, so row statistics
-// are lane-local and per-key sums are one cross-lane reduction per key tile.
-// Exponentials use v_exp_f32 on log2-domain logits.
+// LDS).  Each lane owns one query column, so row sums are lane-local and
+// per-key sums are one transposed reduction per 64 keys.
+#include <type_traits>
+
 #include "stages.h"
 
 namespace certkv {
@@ -21,9 +27,10 @@ typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kScoreThreads = 256;     // 4 waves
-constexpr int kKeysPerWaveIter = 64;   // two 32-key tiles per wave
-constexpr int kKeysPerIter = 256;      // per workgroup iteration
+constexpr int kScoreThreads = 512;  // 8 waves
+constexpr int kScoreKT = 2;         // 16-key tiles per wave iteration
+constexpr float kSumLo = 8.673617379884035e-19f;  // 2^-60
+constexpr float kSumHi = 1.329227995784916e+36f;  // 2^120
 
 union Frag {
   uint4 u;
@@ -37,6 +44,8 @@ struct ScoreSmem {
   static constexpr int kRowElems = D + 8;
 };
 
+enum { kPass1Sum = 0, kPass1Max = 1, kPass2 = 2 };
+
 // MFMA v_mfma_f32_16x16x32_bf16 layout used below (per 64-lane wave):
 //   A (16 keys x 32 dims): lane (grp = lane/16, c = lane%16) supplies key c,
 //     8 consecutive dims of its group's slice;
@@ -45,18 +54,17 @@ struct ScoreSmem {
 //     r = 0..3.
 // Each lane group owns a contiguous quarter of the head dimension for all of
 // its k-steps, so a lane loads one 2*D/4-byte run of its key row.
-constexpr int kNqtMax = 32;  // up to 512 window rows (16 per query tile)
-
-template <int D, bool P2>
+template <int D, int NQT, int KT, int MODE>
 __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
     int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
     int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, float2* __restrict__ part,
-    const float* __restrict__ lse2, float* __restrict__ scores,
-    float* __restrict__ kpart) {
+    const float* __restrict__ lse2, const int32_t* __restrict__ flag,
+    float* __restrict__ scores, float* __restrict__ kpart) {
   constexpr int KS = D / 32;   // MFMA k-steps
   constexpr int QD = D / 4;    // dims per lane group
   constexpr int RE = ScoreSmem<D>::kRowElems;
+  constexpr bool P2 = MODE == kPass2;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   uint16_t* q_lds = reinterpret_cast<uint16_t*>(smem_raw);
 
@@ -72,11 +80,15 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
   if (key_begin >= n) return;
   const int key_end = min(n, key_begin + keys_per_block);
   const int M = g.w * g.G;
-  const int Mp = (M + 15) & ~15;  // rows padded to whole 16-query tiles
+  const int Mp = NQT * 16;  // rows padded to whole 16-query tiles
   const int64_t u = unit_index(g, l, b, h);
+  if (MODE == kPass1Max && flag[u] == 0) return;
 
   float* lse_lds = reinterpret_cast<float*>(smem_raw + (size_t)Mp * RE * 2);
-  float* red_lds = lse_lds + Mp;  // [4][Mp][2] or [4][D]
+  int* lim_lds = reinterpret_cast<int*>(lse_lds + Mp);
+  // Cross-wave reduction area, aliasing the staged queries once the key loop
+  // is done: [8][Mp] sums, [8][Mp][2] (max, sum) pairs or [8][D] key sums.
+  float* red_lds = reinterpret_cast<float*>(smem_raw);
 
   // Stage the window queries of this KV head: row rho = q*G + gq; padding
   // rows are zero and are never written out (pass 2 gives them lse = +inf).
@@ -93,9 +105,13 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
       }
       *reinterpret_cast<uint4*>(q_lds + rho * RE + part8 * 8) = val;
     }
-    if (P2) {
-      for (int i = threadIdx.x; i < Mp; i += kScoreThreads)
-        lse_lds[i] = i < M ? lse2[u * M + i] : INFINITY;
+    // Last visible key of each row: the causal limit of its window position,
+    // -1 for padding rows.
+    for (int i = threadIdx.x; i < Mp; i += kScoreThreads) {
+      int lim = -1;
+      if (i < M) lim = g.causal ? min(n - g.w + i / g.G, n - 1) : n - 1;
+      lim_lds[i] = lim;
+      if (P2) lse_lds[i] = i < M ? lse2[u * M + i] : INFINITY;
     }
   }
   __syncthreads();
@@ -105,66 +121,79 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
   const int grp = lane >> 4;
   const int c16 = lane & 15;
   const float c2 = g.scale * kLog2e;
-  const int nqt = Mp / 16;
   const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
   const uint16_t* kbase = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
 
-  float mrun[kNqtMax], srun[kNqtMax];  // pass 1: this lane's query column, per tile
+  float srun[NQT];  // pass 1: this lane's query column, per query tile
+  float mrun[MODE == kPass1Max ? NQT : 1];
 #pragma unroll
-  for (int i = 0; i < kNqtMax; ++i) {
-    mrun[i] = -INFINITY;
-    srun[i] = 0.f;
-  }
-  float kacc[QD];  // pass 2: weighted key sum over this lane's dims
+  for (int i = 0; i < NQT; ++i) srun[i] = 0.f;
 #pragma unroll
-  for (int i = 0; i < QD; ++i) kacc[i] = 0.f;
+  for (int i = 0; i < (MODE == kPass1Max ? NQT : 1); ++i) mrun[i] = -INFINITY;
+  float kacc[P2 ? QD : 1];  // pass 2: weighted key sum over this lane's dims
+#pragma unroll
+  for (int i = 0; i < (P2 ? QD : 1); ++i) kacc[i] = 0.f;
 
-  for (int it = key_begin + wave * kKeysPerWaveIter; it < key_end; it += kKeysPerIter) {
-    // Four 16-key tiles (keys it..it+63) as A fragments, straight from HBM.
-    Frag kf[4][KS];
+  constexpr int KPW = 16 * KT;        // keys per wave iteration
+  constexpr int KPI = KPW * kScoreThreads / 64;  // keys per workgroup iteration
+  constexpr int NV = 4 * KT;          // per-lane D values per query tile
+  for (int it = key_begin + wave * KPW; it < key_end; it += KPI) {
+    // KT 16-key tiles (keys it..it+KPW-1) as A fragments, straight from HBM.
+    Frag kf[KT][KS];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < KT; ++t) {
       int key = it + t * 16 + c16;
       int keyc = key < n ? key : n - 1;
       const uint4* src = reinterpret_cast<const uint4*>(kbase + (int64_t)keyc * k_st + grp * QD);
 #pragma unroll
       for (int s = 0; s < KS; ++s) kf[t][s].u = src[s];
     }
-    const bool need_mask = (it + 63 >= first_masked) || (it + 63 >= n);
-    float ssum[4][4];
+    const bool need_mask = (it + KPW - 1 >= first_masked) || (it + KPW - 1 >= n);
+    float ssum[KT][4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < KT; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) ssum[t][r] = 0.f;
 
+    // The query-tile loop is instantiated twice, with and without the
+    // causal / tail mask, so that no branch splits it (a branch lets the
+    // compiler sink every tile's exponentials below all the MFMAs, which
+    // keeps every tile's accumulators live at once).
+    auto tiles = [&](auto masked_tag) {
+      constexpr bool MASKED = decltype(masked_tag)::value;
 #pragma unroll
-    for (int qt = 0; qt < kNqtMax; ++qt) {
-      if (qt >= nqt) break;
-      f32x4_t acc[4];
+    for (int qt = 0; qt < NQT; ++qt) {
+      f32x4_t acc[KT];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < KT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const uint16_t* qrow = q_lds + (qt * 16 + c16) * RE + grp * QD;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         Frag qf;
         qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < KT; ++t)
           acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t][s].v, qf.v, acc[t], 0, 0, 0);
       }
-      if (need_mask) {
-        const int qpos = n - g.w + (qt * 16 + c16) / g.G;
-        const int lim = g.causal ? min(qpos, n - 1) : n - 1;
+      if (MASKED) {
+        const int lim = lim_lds[qt * 16 + c16];
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < KT; ++t)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (it + t * 16 + grp * 4 + r > lim) acc[t][r] = -INFINITY;
       }
-      if (!P2) {
+      if (MODE == kPass1Sum) {
+        float sacc = 0.f;
+#pragma unroll
+        for (int t = 0; t < KT; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sacc += __builtin_amdgcn_exp2f(acc[t][r] * c2);
+        srun[qt] += sacc;
+      } else if (MODE == kPass1Max) {
         float mx = acc[0][0];
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < KT; ++t)
 #pragma unroll
           for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[t][r]);
         const float mnew = fmaxf(mrun[qt], mx * c2);
@@ -172,7 +201,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
           const float sc = __builtin_amdgcn_exp2f(mrun[qt] - mnew);
           float sacc = 0.f;
 #pragma unroll
-          for (int t = 0; t < 4; ++t)
+          for (int t = 0; t < KT; ++t)
 #pragma unroll
             for (int r = 0; r < 4; ++r) sacc += __builtin_amdgcn_exp2f(fmaf(acc[t][r], c2, -mnew));
           srun[qt] = fmaf(srun[qt], sc, sacc);
@@ -181,23 +210,33 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
       } else {
         const float l2 = lse_lds[qt * 16 + c16];
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < KT; ++t)
 #pragma unroll
           for (int r = 0; r < 4; ++r) ssum[t][r] += __builtin_amdgcn_exp2f(fmaf(acc[t][r], c2, -l2));
       }
+      // Keep each query tile's LDS loads inside its own iteration: hoisting
+      // them across tiles multiplies the live fragments.
+      __builtin_amdgcn_sched_barrier(0);
     }
+    };
+    if (need_mask)
+      tiles(std::integral_constant<bool, true>());
+    else
+      tiles(std::integral_constant<bool, false>());
 
     if (P2) {
       // Sum each key's per-lane partials over the 16 query columns of its lane
-      // group: transpose-reduce so lane (grp, c16) ends with value index c16,
-      // i.e. tile c16/4, register c16%4 = key 16*(c16/4) + 4*grp + c16%4.
-      float v[16];
+      // group.  Value i = 4*t + r of lane (grp, c16) belongs to key
+      // 16*t + 4*grp + r; a transpose-reduce over lane bits 8, 4, ... leaves
+      // value i = c16 / (16/NV) in lanes c16 = (16/NV)*i + j, and the last
+      // xor steps add the j copies.
+      float v[NV];
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < KT; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[t * 4 + r] = ssum[t][r];
 #pragma unroll
-      for (int m = 8, half = 8; m >= 1; m >>= 1, half >>= 1) {
+      for (int m = 8, half = NV / 2; half >= 1; m >>= 1, half >>= 1) {
         const bool up = (lane & m) != 0;
 #pragma unroll
         for (int i = 0; i < half; ++i) {
@@ -206,15 +245,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
           v[i] = keep + __shfl_xor(send, m, 64);
         }
       }
+      constexpr int SPREAD = 16 / NV;  // lanes sharing one value index
+#pragma unroll
+      for (int m = SPREAD / 2; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, 64);
       const float s_mine = v[0];
-      const int key_mine = it + (c16 >> 2) * 16 + grp * 4 + (c16 & 3);
-      if (key_mine < n) scores[lht_base(g, l, h, tok0) + key_mine] = s_mine;
+      const int i_mine = c16 / SPREAD;
+      const int key_mine = it + (i_mine >> 2) * 16 + grp * 4 + (i_mine & 3);
+      if ((c16 % SPREAD) == 0 && key_mine < n) scores[lht_base(g, l, h, tok0) + key_mine] = s_mine;
       if (kpart) {
         // Lane (grp, c16) holds key c16 of each tile over dims grp*QD..; the
-        // score of key (t, i) sits in lane 16*(i/4) + 4*t + i%4.
+        // score of key (t, c16) is value 4*t + c16%4 of lane group c16/4.
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int src = 16 * (c16 >> 2) + 4 * t + (c16 & 3);
+        for (int t = 0; t < KT; ++t) {
+          const int src = 16 * (c16 >> 2) + SPREAD * (4 * t + (c16 & 3));
           float s_t = __shfl(s_mine, src, 64);
           const int key = it + t * 16 + c16;
           s_t = (key < n && s_t > 0.f) ? s_t : 0.f;
@@ -232,12 +275,26 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     }
   }
 
-  if (!P2) {
-    // Merge the four lane groups (same query column, other key rows), then the
-    // four waves, then write this block's (max, sum) per row.
+  constexpr int NW = kScoreThreads / 64;
+  __syncthreads();  // every wave is done with the staged queries
+  if (MODE == kPass1Sum) {
+    // Sum the four lane groups (same query column), then the waves.
 #pragma unroll
-    for (int qt = 0; qt < kNqtMax; ++qt) {
-      if (qt >= nqt) break;
+    for (int qt = 0; qt < NQT; ++qt) {
+      float s0 = srun[qt];
+      s0 += __shfl_xor(s0, 16, 64);
+      s0 += __shfl_xor(s0, 32, 64);
+      if (grp == 0) red_lds[wave * Mp + qt * 16 + c16] = s0;
+    }
+    __syncthreads();
+    for (int rho = threadIdx.x; rho < M; rho += kScoreThreads) {
+      float sacc = 0.f;
+      for (int wv = 0; wv < NW; ++wv) sacc += red_lds[wv * Mp + rho];
+      part[(u * nkb_max + kb) * M + rho] = make_float2(sacc, 0.f);
+    }
+  } else if (MODE == kPass1Max) {
+#pragma unroll
+    for (int qt = 0; qt < NQT; ++qt) {
       float m0 = mrun[qt], s0 = srun[qt];
 #pragma unroll
       for (int msk = 16; msk <= 32; msk <<= 1) {
@@ -258,10 +315,10 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     __syncthreads();
     for (int rho = threadIdx.x; rho < M; rho += kScoreThreads) {
       float mt = -INFINITY;
-      for (int wv = 0; wv < 4; ++wv) mt = fmaxf(mt, red_lds[(wv * Mp + rho) * 2]);
+      for (int wv = 0; wv < NW; ++wv) mt = fmaxf(mt, red_lds[(wv * Mp + rho) * 2]);
       float sacc = 0.f;
       if (mt != -INFINITY) {
-        for (int wv = 0; wv < 4; ++wv) {
+        for (int wv = 0; wv < NW; ++wv) {
           float mw = red_lds[(wv * Mp + rho) * 2];
           if (mw != -INFINITY) sacc += red_lds[(wv * Mp + rho) * 2 + 1] * __builtin_amdgcn_exp2f(mw - mt);
         }
@@ -270,7 +327,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     }
   } else if (kpart) {
     // Reduce the weighted key sums over the 16 lanes of each group, then over
-    // the four waves.
+    // the waves.
     float v[QD];
 #pragma unroll
     for (int i = 0; i < QD; ++i) v[i] = kacc[i];
@@ -285,23 +342,30 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
       }
     }
     constexpr int PER = QD / 16;  // dims left per lane
-    __syncthreads();
 #pragma unroll
     for (int e = 0; e < PER; ++e) red_lds[wave * D + grp * QD + c16 * PER + e] = v[e];
     __syncthreads();
     for (int dd = threadIdx.x; dd < D; dd += kScoreThreads) {
-      float s = red_lds[dd] + red_lds[D + dd] + red_lds[2 * D + dd] + red_lds[3 * D + dd];
+      float s = 0.f;
+      for (int wv = 0; wv < NW; ++wv) s += red_lds[wv * D + dd];
       kpart[(u * nkb_max + kb) * D + dd] = s;
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// Combine per-block (max, sum) into the per-row log2-sum-exp.
+// Per-row log2-sum-exp from the pass-1 partials.
+// Sum format (shift-free partial sums): writes lse2 and flags the unit when a
+// row's total leaves [2^-60, 2^120].  Max format ((max, sum) partials):
+// combines with rescaling; with `only_flagged` it touches flagged units only.
+template <bool SUM_FORMAT>
 __global__ __launch_bounds__(256) void lse_combine_kernel(Geo g, SeqTab st, int32_t keys_per_block,
                                                            int32_t nkb_max,
                                                            const float2* __restrict__ part,
-                                                           float* __restrict__ lse2) {
+                                                           float* __restrict__ lse2,
+                                                           int32_t* __restrict__ flag,
+                                                           int32_t only_flagged) {
+  __shared__ int bad;
   const int h = blockIdx.x % g.H;
   const int bl = blockIdx.x / g.H;
   const int l = blockIdx.y;
@@ -311,15 +375,29 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(Geo g, SeqTab st, int3
   const int nkb = (n + keys_per_block - 1) / keys_per_block;
   const int M = g.w * g.G;
   const int64_t u = unit_index(g, l, b, h);
+  if (!SUM_FORMAT && only_flagged && flag[u] == 0) return;
+  if (SUM_FORMAT && threadIdx.x == 0) bad = 0;
+  __syncthreads();
   for (int rho = threadIdx.x; rho < M; rho += blockDim.x) {
-    float mt = -INFINITY;
-    for (int kb = 0; kb < nkb; ++kb) mt = fmaxf(mt, part[(u * nkb_max + kb) * M + rho].x);
-    float s = 0.f;
-    for (int kb = 0; kb < nkb; ++kb) {
-      float2 p = part[(u * nkb_max + kb) * M + rho];
-      if (p.x != -INFINITY) s += p.y * __builtin_amdgcn_exp2f(p.x - mt);
+    if (SUM_FORMAT) {
+      float s = 0.f;
+      for (int kb = 0; kb < nkb; ++kb) s += part[(u * nkb_max + kb) * M + rho].x;
+      if (!(s >= kSumLo && s <= kSumHi)) bad = 1;
+      lse2[u * M + rho] = __builtin_amdgcn_logf(s);
+    } else {
+      float mt = -INFINITY;
+      for (int kb = 0; kb < nkb; ++kb) mt = fmaxf(mt, part[(u * nkb_max + kb) * M + rho].x);
+      float s = 0.f;
+      for (int kb = 0; kb < nkb; ++kb) {
+        float2 p = part[(u * nkb_max + kb) * M + rho];
+        if (p.x != -INFINITY) s += p.y * __builtin_amdgcn_exp2f(p.x - mt);
+      }
+      lse2[u * M + rho] = mt + __builtin_amdgcn_logf(s);
     }
-    lse2[u * M + rho] = mt + __builtin_amdgcn_logf(s);
+  }
+  if (SUM_FORMAT) {
+    __syncthreads();
+    if (threadIdx.x == 0) flag[u] = bad;
   }
 }
 
@@ -429,19 +507,19 @@ __global__ __launch_bounds__(256) void score_f32_kernel(
 // ---------------------------------------------------------------------------
 // Host side.
 
-
 size_t score_smem_bytes(const Geo& g, int32_t dtype) {
   const int M = g.w * g.G;
   if (dtype == CERTKV_BF16) {
-    const size_t Mp = (size_t)((M + 15) & ~15);
-    size_t q = Mp * (g.D + 8) * 2;
-    size_t red = (size_t)4 * (Mp * 2 > (size_t)g.D ? Mp * 2 : (size_t)g.D) * 4;
-    return q + Mp * 4 + red;
+    const size_t Mp = (size_t)score_nqt(M) * 16;
+    const size_t q = Mp * (g.D + 8) * 2;
+    const size_t nw = kScoreThreads / 64;
+    const size_t red = nw * (Mp * 2 > (size_t)g.D ? Mp * 2 : (size_t)g.D) * 4;
+    return (q > red ? q : red) + Mp * 8;
   }
   return (size_t)M * g.D * 4 + (size_t)M * 4 + 8 * 4 + (size_t)4 * g.D * 4;
 }
 
-template <int D>
+template <int D, int NQT>
 static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_len,
                                  hipStream_t s) {
   const Geo& g = a.g;
@@ -450,24 +528,34 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
   size_t smem = score_smem_bytes(g, CERTKV_BF16);
   static bool attr_set = false;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, false>,
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass1Sum>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, true>,
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass1Max>,
+                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass2>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
   const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
   const uint16_t* k = static_cast<const uint16_t*>(a.k.ptr);
-  CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, false>), grid, dim3(kScoreThreads), smem,
-                s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token,
-                a.k.s_head, a.keys_per_block, a.nkb_max, a.part, (const float*)nullptr,
-                (float*)nullptr, (float*)nullptr);
-  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel, dim3(g.H * st.count, g.L), dim3(256), 0, s,
-                g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2);
-  CERTKV_LAUNCH("score_pass2_mfma", (score_mfma_kernel<D, true>), grid, dim3(kScoreThreads), smem,
-                s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token,
-                a.k.s_head, a.keys_per_block, a.nkb_max, (float2*)nullptr, (const float*)a.lse2,
-                a.scores, a.ksum ? a.kpart : (float*)nullptr);
+  CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kScoreKT, kPass1Sum>), grid,
+                dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
+                (const float*)nullptr, (const int32_t*)nullptr, (float*)nullptr, (float*)nullptr);
+  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
+                s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
+  // fallback for flagged units (returns at once for the others)
+  CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kScoreKT, kPass1Max>), grid,
+                dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
+                (const float*)nullptr, (const int32_t*)a.flag, (float*)nullptr, (float*)nullptr);
+  CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
+                0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 1);
+  CERTKV_LAUNCH("score_pass2_mfma", (score_mfma_kernel<D, NQT, kScoreKT, kPass2>), grid, dim3(kScoreThreads),
+                smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
+                a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (float2*)nullptr,
+                (const float*)a.lse2, (const int32_t*)nullptr, a.scores,
+                a.ksum ? a.kpart : (float*)nullptr);
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
                   s, g, st, a.keys_per_block, a.nkb_max, (const float*)a.kpart, a.ksum);
@@ -485,8 +573,8 @@ static certkv_status launch_f32(const ScoreArgs& a, const SeqTab& st, int max_le
   CERTKV_LAUNCH("score_pass1_f32", (score_f32_kernel<D, false>), grid, dim3(256), smem, s, g, st, q,
                 a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token, a.k.s_head,
                 a.nkb_max, a.part, (const float*)nullptr, (float*)nullptr, (float*)nullptr);
-  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel, dim3(g.H * st.count, g.L), dim3(256), 0, s,
-                g, st, 256, a.nkb_max, (const float2*)a.part, a.lse2);
+  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
+                0, s, g, st, 256, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
   CERTKV_LAUNCH("score_pass2_f32", (score_f32_kernel<D, true>), grid, dim3(256), smem, s, g, st, q,
                 a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token, a.k.s_head,
                 a.nkb_max, (float2*)nullptr, (const float*)a.lse2, a.scores,
@@ -497,11 +585,23 @@ static certkv_status launch_f32(const ScoreArgs& a, const SeqTab& st, int max_le
   return CERTKV_OK;
 }
 
+template <int D>
+static certkv_status dispatch_nqt(const ScoreArgs& a, const SeqTab& st, int max_len, hipStream_t s) {
+  switch (score_nqt(a.g.w * a.g.G)) {
+    case 1: return launch_mfma<D, 1>(a, st, max_len, s);
+    case 2: return launch_mfma<D, 2>(a, st, max_len, s);
+    case 4: return launch_mfma<D, 4>(a, st, max_len, s);
+    case 8: return launch_mfma<D, 8>(a, st, max_len, s);
+    case 16: return launch_mfma<D, 16>(a, st, max_len, s);
+    default: return launch_mfma<D, 32>(a, st, max_len, s);
+  }
+}
+
 certkv_status run_score(const ScoreArgs& a, const SeqTab& st, int max_len, hipStream_t s) {
   if (a.dtype == CERTKV_F32)
     return a.g.D == 128 ? launch_f32<128>(a, st, max_len, s) : launch_f32<64>(a, st, max_len, s);
-  if (a.g.D == 128) return launch_mfma<128>(a, st, max_len, s);
-  return launch_mfma<64>(a, st, max_len, s);
+  if (a.g.D == 128) return dispatch_nqt<128>(a, st, max_len, s);
+  return dispatch_nqt<64>(a, st, max_len, s);
 }
 
 }  // namespace certkv
