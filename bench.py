@@ -23,26 +23,41 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
-BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+# Full-rate VALU lane operations per second: 256 CUs x 4 SIMDs x 16 lanes x
+# 2.4 GHz.  (The published fp32 vector peak, 157.3 TFLOP/s, is this rate x 2
+# for FMA x 2 for packed fp32; fp64 FMA issues at the same rate, 78.6 TFLOP/s.)
+VALU_PEAK_TSLOTS = 256 * 4 * 16 * 2.4e9 / 1e12
+COPY_BYTES = 1 << 30           # calibration copy: 1 GiB read, 1 GiB written
+
+KERNEL_SOURCES = {
+    "score_": "score.hip", "sort_segments": "sort.hip", "curves": "curves.hip",
+    "curve_blockstats": "allocate.hip", "allocate": "allocate.hip", "select": "select.hip",
+    "kept_offsets": "select.hip", "clamp_budgets": "select.hip", "packed_offsets": "select.hip",
+    "coverage_budget": "select.hip", "tail_": "tail.hip", "compact_": "tail.hip",
+    "kept_bitmap": "tail.hip",
+}
 
 
 def algorithmic_model(cfg, n_keep):
-    """Algorithmic bytes and flops per launch of each kernel (whole workload).
+    """Algorithmic HBM bytes, MFMA flops and VALU slots per launch of each kernel.
 
     Per (KV head, token) unit with d = head_dim, e = element bytes, keep
-    fraction f = (n_keep - 1) / n:
-      score pass 1          K read                                   d*e
-      score pass 2          K read + score write                     d*e + 4
-      sort                  score read + order write                 4 + 4
-      curves                V gathered + order + key + curve write   d*e + 12
-      curve block stats     curve read                               4
-      allocate              curve read                               4
-      select                score read + kept index write + bitmap   4 + 4f + 1/8
+    fraction f = (n_keep - 1) / n, M = w*G window rows:
+      kernel                bytes                                   MFMA flops  VALU slots
+      score pass 1          K read: d*e                              2*M*d       4*M
+      score pass 2          K read + score write: d*e + 4            2*M*d       4*M
+      sort                  score read + order write: 8
+      curves                V gathered + order + key + curve: d*e+12             9*d
+      curve block stats     curve read: 4
+      allocate              curve read: 4
+      select                score read + kept index + bitmap: 4+4f+1/8
       tail+compact gather   kept index, score, K, V read; K, V and
-                            position written                          f*(4*d*e + 12)
-    MFMA flops of each scoring pass: 2 * M * d per (head, token), M = w*G.
-    Small per-unit kernels (row combines, offsets, slot finalize) are
-    modelled by their per-unit traffic only.
+                            position written: f*(4*d*e + 12)
+    A VALU slot is one full-rate lane operation: per softmax term the passes
+    spend one multiply (or fma), one exp2 (half rate: 2 slots) and one add;
+    the fp64 curves spend per (rank, dim) two conversions and two fma in the
+    totals pass and two conversions and three fma in the walk.
     """
     L, H, D = cfg.layers, cfg.kv_heads, cfg.head_dim
     e = 2 if cfg.dtype_name == "bf16" else 4
@@ -50,32 +65,148 @@ def algorithmic_model(cfg, n_keep):
     f = sum((nk - 1) for nk in n_keep) / sum(cfg.seqlens)
     M = cfg.window * cfg.group
     per = {
-        "score_pass1_mfma": (D * e, 2 * M * D),
-        "score_pass2_mfma": (D * e + 4, 2 * M * D),
-        "sort_segments": (8, 0),
-        "curves": (D * e + 12, 0),
-        "curve_blockstats": (4, 0),
-        "allocate": (4, 0),
-        "select": (4 + 4 * f + 0.125, 0),
-        "tail_compact_gather": (f * (4 * D * e + 12), 0),
+        "score_pass1_mfma": (D * e, 2 * M * D, 4 * M),
+        "score_pass2_mfma": (D * e + 4, 2 * M * D, 4 * M),
+        "sort_segments": (8, 0, 0),
+        "curves": (D * e + 12, 0, 9 * D),
+        "curve_blockstats": (4, 0, 0),
+        "allocate": (4, 0, 0),
+        "select": (4 + 4 * f + 0.125, 0, 0),
+        "tail_compact_gather": (f * (4 * D * e + 12), 0, 0),
     }
-    return {k: (b * ht, fl * ht) for k, (b, fl) in per.items()}, ht
+    return {k: (b * ht, fl * ht, sl * ht) for k, (b, fl, sl) in per.items()}, ht
 
 
-def cpu_baseline(cache, cfg, n_keep, log):
-    """The fp64 oracle on one full layer of the workload (all KV heads)."""
+def source_digest(kernel):
+    """sha256 over the source file of a kernel and the shared headers."""
+    import hashlib
+    fname = next((f for pre, f in KERNEL_SOURCES.items() if kernel.startswith(pre)), None)
+    if fname is None:
+        return None
+    h = hashlib.sha256()
+    for part in ("common.h", "stages.h", fname):
+        with open(os.path.join(ROOT, "paper_2608_21541_amd", "csrc", part), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch from a committed counter summary, if its kernel
+    source is unchanged since the counters were taken (else None)."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    digest = source_digest(kernel)
+    for name in sorted(os.listdir(pdir)):
+        if not name.endswith(".md"):
+            continue
+        with open(os.path.join(pdir, name)) as fh:
+            for line in fh:
+                if line.startswith("traffic-record: "):
+                    rec = json.loads(line[len("traffic-record: "):])
+                    if rec.get("kernel") == kernel and rec.get("workload") == workload \
+                            and rec.get("source_sha256") == digest:
+                        return rec["bytes_per_launch"]
+    return None
+
+
+def roofline_of(name, model, avg_ms, workload):
+    """Bound of one kernel: the resource with the largest lower-bound time."""
+    b, fl, sl = model.get(name, (0, 0, 0))
+    sec = avg_ms / 1e3
+    cands = [("hbm", b / (HBM_PEAK_GBS * 1e9), b / sec / 1e9, HBM_PEAK_GBS, "GB/s"),
+             ("mfma", fl / (BF16_PEAK_TFLOPS * 1e12), fl / sec / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"),
+             ("alu", sl / (VALU_PEAK_TSLOTS * 1e12), sl / sec / 1e12, VALU_PEAK_TSLOTS,
+              "T VALU lane-slots/s")]
+    bound, _, ach, peak, unit = max(cands, key=lambda c: c[1])
+    return {"bound": bound, "achieved": ach, "peak": peak, "unit": unit, "frac": ach / peak,
+            "traffic": recorded_traffic(name, workload), "kernel": name,
+            "lower_bounds_ms": {c[0]: c[1] * 1e3 for c in cands}}
+
+
+def cpu_baseline(cache, cfg, n_keep, log, layers=6):
+    """The fp64 oracle on the first `layers` layers of the workload (all KV
+    heads, full length): about ten seconds of host work."""
     import oracle
-    q = cache["q_win"][0, :cfg.window].double().cpu().numpy()
-    k = cache["k"][0, :cfg.seqlens[0]].double().cpu().numpy()
-    v = cache["v"][0, :cfg.seqlens[0]].double().cpu().numpy()
-    log(f"cpu baseline: oracle on 1 layer x {cfg.kv_heads} heads x {cfg.seqlens[0]} tokens")
-    t0 = time.perf_counter()
-    oracle.compress_block(q, k, v, n_keep[0], 1.0 / math.sqrt(cfg.head_dim))
-    dt = time.perf_counter() - t0
-    return {"value": cfg.seqlens[0] / dt, "unit": "KV tokens/s per layer",
+    layers = min(layers, cfg.layers)
+    n = cfg.seqlens[0]
+    log(f"cpu baseline: oracle on {layers} layers x {cfg.kv_heads} heads x {n} tokens")
+    dt = 0.0
+    for li in range(layers):
+        q = cache["q_win"][li, :cfg.window].double().cpu().numpy()
+        k = cache["k"][li, :n].double().cpu().numpy()
+        v = cache["v"][li, :n].double().cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.compress_block(q, k, v, n_keep[0], 1.0 / math.sqrt(cfg.head_dim))
+        dt += time.perf_counter() - t0
+    return {"value": n / (dt / layers), "unit": "KV tokens/s per layer",
             "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"layer 0 of the workload: {cfg.kv_heads} KV heads x {cfg.seqlens[0]} tokens, "
-                      f"full pass (score, order, curves, allocation, selection, tail), {dt:.1f} s"}
+            "sample": f"layers 0-{layers - 1} of the workload: {cfg.kv_heads} KV heads x {n} tokens "
+                      f"each, full pass (score, order, curves, allocation, selection, tail), "
+                      f"{dt:.1f} s of oracle time"}
+
+
+def _read_csv(path):
+    import csv
+    with open(path, newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def summarize_stats(csv_path, out, command):
+    """Markdown summary of a rocprofv3 --kernel-trace --stats kernel table."""
+    rows = _read_csv(csv_path)
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = ["# Kernel time summary", "", "Command:", "", "```", command, "```", "",
+             "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append("| %s | %s | %.1f | %.3f | %.1f |" % (
+            r["Name"][:90].replace("|", "/"), r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["TotalDurationNs"]) / 1e6, 100.0 * float(r["TotalDurationNs"]) / total))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
+def summarize_traffic(fetch_csv, write_csv, kernel_regex, kernel, workload, out, commands):
+    """HBM traffic of one kernel from two rocprofv3 --pmc runs (FETCH_SIZE, then
+    WRITE_SIZE, KiB per dispatch), scaled by the readings of a 1 GiB device
+    copy in the same runs."""
+    import re
+    import statistics
+
+    def per_kernel(path, counter):
+        vals, copies = [], []
+        for r in _read_csv(path):
+            if r.get("Counter_Name") != counter:
+                continue
+            name, val = r["Kernel_Name"], float(r["Counter_Value"])
+            if re.search(kernel_regex, name):
+                vals.append(val)
+            elif "copy" in name.lower():
+                copies.append(val)
+        return vals, copies
+
+    fv, fc = per_kernel(fetch_csv, "FETCH_SIZE")
+    wv, wc = per_kernel(write_csv, "WRITE_SIZE")
+    f_copy, w_copy = max(fc), max(wc)
+    f_scale = COPY_BYTES / 1024.0 / f_copy
+    w_scale = COPY_BYTES / 1024.0 / w_copy
+    fetch_b = statistics.mean(fv) * 1024.0 * f_scale
+    write_b = statistics.mean(wv) * 1024.0 * w_scale
+    rec = {"kernel": kernel, "workload": workload, "source_sha256": source_digest(kernel),
+           "bytes_per_launch": fetch_b + write_b, "fetch_bytes": fetch_b, "write_bytes": write_b,
+           "fetch_scale": f_scale, "write_scale": w_scale, "dispatches": [len(fv), len(wv)]}
+    lines = ["# HBM traffic of %s (%s)" % (kernel, workload), "",
+             "Counters FETCH_SIZE and WRITE_SIZE (KiB per dispatch) from two separate",
+             "rocprofv3 --pmc runs, each scaled by the reading of a plain 1 GiB device",
+             "copy in the same run (copy read %.0f KiB, written %.0f KiB: scale %.4f / %.4f)."
+             % (f_copy, w_copy, f_scale, w_scale), "",
+             "Commands:", "", "```"] + commands + ["```", "",
+             "| | per launch |", "|---|---:|",
+             "| fetched | %.3f GB |" % (fetch_b / 1e9), "| written | %.3f GB |" % (write_b / 1e9),
+             "| total | %.3f GB |" % ((fetch_b + write_b) / 1e9), "",
+             "traffic-record: " + json.dumps(rec)]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
 
 
 def main():
@@ -86,7 +217,21 @@ def main():
     ap.add_argument("--config", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run a 1 GiB device copy first (counter calibration)")
+    ap.add_argument("--summarize-stats", nargs=3, metavar=("CSV", "OUT", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--summarize-traffic", nargs=7,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "REGEX", "KERNEL", "OUT", "CMD1", "CMD2"),
+                    help="write the HBM traffic record of one kernel from two pmc runs")
     args = ap.parse_args()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_traffic:
+        fc, wc, rx, kn, out, c1, c2 = args.summarize_traffic
+        summarize_traffic(fc, wc, rx, kn, args.config, out, [c1, c2])
+        return
 
     def log(msg):
         if not args.quiet:
@@ -115,29 +260,37 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream(dev)
+    if args.calibrate_copy:
+        # A plain device copy of known size: its FETCH_SIZE / WRITE_SIZE
+        # readings scale the counters of the pass's kernels to bytes.
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         ck.compress(spec, q, k, v, n_keep, bufs=bufs)
     torch.cuda.synchronize()
+    # Timed region.  Every launch of the pass is bracketed by HIP events on
+    # the stream it runs on, giving per-kernel durations of these same steps.
+    ck.profile_reset()
+    ck.profile_enable(True)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
         ck.compress(spec, q, k, v, n_keep, bufs=bufs)
     end.record(stream)
     torch.cuda.synchronize()
+    prof = ck.profile_read()
+    ck.profile_enable(False)
+    ck.profile_reset()
     ms = start.elapsed_time(end) / args.steps
     tokens = sum(cfg.seqlens)
     value = tokens * cfg.layers / (ms / 1e3) / cfg.layers  # tokens per second per layer
     log(f"pass: {ms:.3f} ms")
 
-    # Per-kernel durations from HIP events around each launch (same stream).
-    ck.profile_reset()
-    ck.profile_enable(True)
-    for _ in range(args.steps):
-        ck.compress(spec, q, k, v, n_keep, bufs=bufs)
-    torch.cuda.synchronize()
-    prof = ck.profile_read()
-    ck.profile_enable(False)
-    ck.profile_reset()
     st = bufs.alloc_stats.cpu()
     alloc_diag = {"repairs_mean": float(st[:, 0].float().mean()), "repairs_max": int(st[:, 0].max()),
                   "bisect_us_mean": float(st[:, 1].float().mean()) / 100.0,
@@ -149,25 +302,12 @@ def main():
         avg = tot / max(cnt, 1)
         kernels[name] = {"launches_per_step": cnt / args.steps, "avg_ms": avg}
     dom = max(kernels, key=lambda n_: kernels[n_]["avg_ms"] * kernels[n_]["launches_per_step"])
-    dbytes, dflops = model.get(dom, (0, 0))
-    davg = kernels[dom]["avg_ms"] / 1e3
-    gbs = dbytes / davg / 1e9
-    tfl = dflops / davg / 1e12
-    if dflops and dflops / max(dbytes, 1) > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": tfl, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": tfl / BF16_PEAK_TFLOPS}
-    else:
-        roof = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": gbs / HBM_PEAK_GBS}
-    roof["kernel"] = dom
-    roof["traffic"] = None
-    pass_bytes = sum(b for b, _ in model.values())
+    roof = roofline_of(dom, model, kernels[dom]["avg_ms"], args.config)
+    pass_bytes = sum(b for b, _, _ in model.values())
     for name, kk in kernels.items():
-        b_, f_ = model.get(name, (0, 0))
-        if b_:
-            kk["alg_GBps"] = b_ / (kk["avg_ms"] / 1e3) / 1e9
-        if f_:
-            kk["alg_TFLOPs"] = f_ / (kk["avg_ms"] / 1e3) / 1e12
+        if name in model:
+            r = roofline_of(name, model, kk["avg_ms"], args.config)
+            kk.update({"bound": r["bound"], "frac": r["frac"]})
     log(json.dumps(kernels, indent=1))
 
     cpu = None

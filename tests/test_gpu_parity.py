@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_2608_21541_amd as ck
 import synth
-from _parity import check_block_stages, run_gpu, spec_of, unit_id
+from _parity import check_block_stages, run_gpu, score_rel_err, spec_of, unit_id
 
 pytestmark = pytest.mark.gpu
 
@@ -213,3 +213,42 @@ def test_full_size_sampled(name):
     log(f"{name}: invariants hold; oracle on sampled layers")
     for li in [0, cfg.layers - 1]:
         check_block_stages(spec, cfg, cache, out, li, 0, check_scores=(li == 0), log=log)
+
+
+# --------------------------------------------------------------------------
+# Rows whose unshifted exponentials leave fp32 range take the max-shifted
+# fallback of the scoring pass.
+
+@pytest.mark.parametrize("case", ["overflow", "underflow"])
+def test_extreme_logits_take_shifted_fallback(case):
+    cfg = synth.config("C2", seqlens=[3000])
+    cache = synth.make_cache(cfg, "cpu")
+    q, k = cache["q_win"].clone(), cache["k"].clone()
+    n, H, G, D, w = 3000, cfg.kv_heads, cfg.group, cfg.head_dim, cfg.window
+    if case == "overflow":
+        scale = 0.4   # heads carrying the planted needles exceed 2^128 in fp32
+    else:
+        # a common offset along dim 0 of every key, met by a strongly negative
+        # query component: every logit of most heads sits far below zero
+        k[..., 0] = (k[..., 0].float() + 16.0).to(k.dtype)
+        q = (q.float() * 0.05).to(q.dtype)
+        q[..., 0] = -8.0
+        scale = 1.0
+    spec = ck.ProblemSpec(1, H, G, D, w, [n], cfg.dtype, softmax_scale=scale)
+    s = ck.score(spec, q.cuda(), k.cuda()).cpu().numpy()
+    log2e = 1.0 / math.log(2.0)
+    extreme = 0
+    for h in range(H):
+        Q = q[0, :, h * G:(h + 1) * G].reshape(w * G, D).double().numpy()
+        qpos = np.repeat(np.arange(n - w, n), G)
+        K = k[0, :, h].double().numpy()
+        logits2 = (Q @ K.T) * scale * log2e
+        if case == "overflow":
+            extreme += int(logits2.max() > 130.0)
+        else:
+            extreme += int(logits2.max() < -130.0)
+        ref = oracle.scores(Q, qpos, K, scale)
+        r, sm = score_rel_err(s[0, h], ref)
+        assert r <= 1e-4 and sm <= 1e-4, (h, r, sm)
+        assert abs(s[0, h].astype(np.float64).sum() - w * G) <= 1e-4 * w * G
+    assert extreme >= 1
