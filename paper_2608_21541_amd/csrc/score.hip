@@ -55,7 +55,7 @@ enum { kPass1Sum = 0, kPass1Max = 1, kPass2 = 2 };
 // Each lane group owns a contiguous quarter of the head dimension for all of
 // its k-steps, so a lane loads one 2*D/4-byte run of its key row.
 template <int D, int NQT, int KT, int MODE>
-__global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((MODE == kPass2 || NQT > 16) ? 2 : 4, 8))) void score_mfma_kernel(
     Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
     int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
     int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, float2* __restrict__ part,
