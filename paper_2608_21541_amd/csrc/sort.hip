@@ -2,27 +2,35 @@
 //
 // One workgroup (16 waves) sorts one unit's segment with a least-significant-
 // digit radix sort: 4 passes of 8-bit digits over the order-inverting key
-// transform of the fp32 score (desc_key).  Stability is what makes equal
-// scores keep ascending position, so every pass ranks elements in exactly
-// their input order:
-//   - a wave takes 256 consecutive elements of the tile in 4 rounds of 64;
-//   - within a round, lanes with equal digits are found with 8 ballots and
-//     ranked by mbcnt (lanes below them with the same digit);
-//   - a per-wave, per-digit counter in LDS carries ranks across rounds;
-//   - after the tile, an exclusive scan over waves per digit gives each wave's
-//     offset, added to the digit's running bucket offset.
-// All four digit histograms come from one counting pass that also sums
-// (s)_+ in fp64 (the normalizer of the weights a_j).
+// transform of the fp32 score (desc_key).  One counting pass first forms all
+// four digit histograms with LDS atomics (and the fp64 sum of (s)_+, the
+// normalizer of a_j).
+// Each pass then walks the segment in tiles of 16 * 64 * R elements; wave w
+// holds the R rounds of 64 consecutive elements at offset 64 R w:
+//   rank     lanes with equal digits are found with 8 ballots; an element's
+//            rank among equal digits of its wave is a per-wave LDS counter
+//            plus mbcnt within the round (input order);
+//   offsets  per digit, an exclusive scan over the waves, and per tile an
+//            exclusive scan over the digits of the tile's digit counts (the
+//            two run concurrently on different waves);
+//   stage    every element is written to LDS at its digit-major position in
+//            the tile (stable);
+//   write    thread i stores staged element i to the digit's running bucket
+//            offset plus its position inside the tile's run of that digit,
+//            so consecutive threads write consecutive addresses.
+// Ranking in input order and runs in tile order make every pass stable, so
+// equal scores keep ascending position.  The next tile's elements are loaded
+// while the current one is ranked.
 #include "stages.h"
 
 namespace certkv {
 
 constexpr int kSortThreads = 1024;
 constexpr int kSortWaves = kSortThreads / 64;
-constexpr int kSortRounds = 4;
-constexpr int kSortTile = kSortThreads * kSortRounds;
+constexpr int kSortRounds = 8;
+constexpr int kSortTile = kSortThreads * kSortRounds;  // 8192 elements
 
-// Lanes of the wave whose 8-bit digit equals this lane's (among `active`).
+// Lanes of the wave whose 8-bit digit equals this lane's (among `valid`).
 __device__ __forceinline__ uint64_t match_digit(uint32_t digit, bool valid) {
   uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -39,15 +47,40 @@ __device__ __forceinline__ uint32_t count_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// Exclusive scan of 256 counters by one wave (4 per lane), in place.
+__device__ __forceinline__ void wave_scan256(uint32_t* v, int lane) {
+  uint32_t c[4], run = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    c[j] = v[lane * 4 + j];
+    run += c[j];
+  }
+  uint32_t incl = run;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  uint32_t excl = incl - run;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[lane * 4 + j] = excl;
+    excl += c[j];
+  }
+}
+
 __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
     Geo g, SeqTab st, const float* __restrict__ scores, uint32_t* __restrict__ keysA,
     int32_t* __restrict__ valsA, uint32_t* __restrict__ keysB, int32_t* __restrict__ valsB,
     uint32_t* __restrict__ keys_out, int32_t* __restrict__ perm_out,
     double* __restrict__ ssum_out) {
   __shared__ uint32_t hist[4][256];
-  __shared__ uint32_t bucket[256];
-  __shared__ uint32_t tile_tot[256];
+  __shared__ uint32_t bucket[256];      // running start of each digit's bucket
+  __shared__ uint32_t tile_tot[256];    // digit counts of the tile
+  __shared__ uint32_t tile_start[256];  // digit-major start inside the tile
   __shared__ volatile uint32_t wave_cnt[kSortWaves][256];
+  __shared__ uint32_t stage_key[kSortTile];
+  __shared__ int32_t stage_val[kSortTile];
   __shared__ double dred[kSortWaves];
 
   const int h = blockIdx.x % g.H;
@@ -62,28 +95,34 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   const int wave = threadIdx.x >> 6;
 
   for (int i = threadIdx.x; i < 4 * 256; i += kSortThreads) (&hist[0][0])[i] = 0u;
+  if (threadIdx.x < 256) tile_tot[threadIdx.x] = 0u;
   __syncthreads();
 
   // Counting pass: four digit histograms and the fp64 sum of (s)_+.
-  double psum = 0.0;
-  for (int t0 = 0; t0 < n; t0 += kSortTile) {
+  {
+    double psum = 0.0;
+    for (int t0 = 0; t0 < n; t0 += kSortTile) {
+      float sv[kSortRounds];
 #pragma unroll
-    for (int r = 0; r < kSortRounds; ++r) {
-      const int e = t0 + wave * 256 + r * 64 + lane;
-      const bool valid = e < n;
-      float s = valid ? scores[base + e] : 0.f;
-      if (valid && s > 0.f) psum += (double)s;
-      const uint32_t key = desc_key(s);
+      for (int r = 0; r < kSortRounds; ++r) {
+        const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+        sv[r] = e < n ? scores[base + e] : 0.f;
+      }
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const uint32_t dg = (key >> (8 * p)) & 255u;
-        const uint64_t peers = match_digit(dg, valid);
-        if (valid && count_below(peers) == 0) atomicAdd(&hist[p][dg], (uint32_t)__popcll(peers));
+      for (int r = 0; r < kSortRounds; ++r) {
+        const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+        const bool valid = e < n;
+        if (valid && sv[r] > 0.f) psum += (double)sv[r];
+        const uint32_t key = desc_key(sv[r]);
+        if (valid) {
+#pragma unroll
+          for (int p = 0; p < 4; ++p) atomicAdd(&hist[p][(key >> (8 * p)) & 255u], 1u);
+        }
       }
     }
+    psum = wave_sum(psum);
+    if (lane == 0) dred[wave] = psum;
   }
-  psum = wave_sum(psum);
-  if (lane == 0) dred[wave] = psum;
   __syncthreads();
   if (threadIdx.x == 0) {
     double tot = 0.0;
@@ -96,83 +135,105 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   for (int p = 0; p < 4; ++p) {
     uint32_t* kout = (p == 0 || p == 2) ? keysB : (p == 1 ? keysA : keys_out);
     int32_t* vout = (p == 0 || p == 2) ? valsB : (p == 1 ? valsA : perm_out);
-    // Exclusive scan of the digit histogram -> bucket starts.
-    __syncthreads();
-    if (wave == 0) {
-      uint32_t c[4], run = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        c[j] = hist[p][lane * 4 + j];
-        run += c[j];
-      }
-      uint32_t incl = run;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        uint32_t y = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += y;
-      }
-      uint32_t excl = incl - run;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bucket[lane * 4 + j] = excl;
-        excl += c[j];
-      }
-    }
-    __syncthreads();
     const int sh = 8 * p;
+    if (wave == 0) {
+      for (int j = 0; j < 4; ++j) bucket[lane * 4 + j] = hist[p][lane * 4 + j];
+      wave_scan256(bucket, lane);
+    }
+    auto load = [&](int t0, uint32_t (&key)[kSortRounds], int32_t (&val)[kSortRounds]) {
+#pragma unroll
+      for (int r = 0; r < kSortRounds; ++r) {
+        const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+        const bool ok = e < n;
+        if (p == 0) {
+          key[r] = desc_key(ok ? scores[base + e] : 0.f);
+          val[r] = e;
+        } else {
+          key[r] = ok ? kin[base + e] : 0u;
+          val[r] = ok ? vin[base + e] : 0;
+        }
+      }
+    };
+    uint32_t key[kSortRounds], nkey[kSortRounds];
+    int32_t val[kSortRounds], nval[kSortRounds];
+    load(0, key, val);
     for (int t0 = 0; t0 < n; t0 += kSortTile) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) wave_cnt[wave][lane * 4 + j] = 0u;
-      uint32_t key[kSortRounds], dg[kSortRounds], rank[kSortRounds];
-      int32_t val[kSortRounds];
-      bool ok[kSortRounds];
+      if (t0 + kSortTile < n) load(t0 + kSortTile, nkey, nval);  // prefetch
+      // rank within the wave
+      uint32_t rank[kSortRounds];
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
-        const int e = t0 + wave * 256 + r * 64 + lane;
-        ok[r] = e < n;
-        if (p == 0) {
-          key[r] = desc_key(ok[r] ? scores[base + e] : 0.f);
-          val[r] = e;
-        } else {
-          key[r] = ok[r] ? kin[base + e] : 0u;
-          val[r] = ok[r] ? vin[base + e] : 0;
-        }
-        dg[r] = (key[r] >> sh) & 255u;
-        const uint64_t peers = match_digit(dg[r], ok[r]);
+        const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+        const bool ok = e < n;
+        const uint32_t dg = (key[r] >> sh) & 255u;
+        const uint64_t peers = match_digit(dg, ok);
         const uint32_t below = count_below(peers);
         uint32_t pre = 0;
-        if (ok[r]) pre = wave_cnt[wave][dg[r]];
+        if (ok) pre = wave_cnt[wave][dg];
         rank[r] = pre + below;
-        if (ok[r] && below == 0) wave_cnt[wave][dg[r]] = pre + (uint32_t)__popcll(peers);
+        if (ok && below == 0) {
+          const uint32_t c = (uint32_t)__popcll(peers);
+          wave_cnt[wave][dg] = pre + c;
+          atomicAdd(&tile_tot[dg], c);
+        }
+      }
+      __syncthreads();
+      // per digit: exclusive scan over the waves (waves 1-4) and over the
+      // digits of the tile counts (wave 0), concurrently
+      if (wave == 0) {
+        for (int j = 0; j < 4; ++j) tile_start[lane * 4 + j] = tile_tot[lane * 4 + j];
+        wave_scan256(tile_start, lane);
+      } else if (threadIdx.x < 256 + 64) {
+        const int d = threadIdx.x - 64;
+        uint32_t run = 0;
+        for (int w = 0; w < kSortWaves; ++w) {
+          const uint32_t c = wave_cnt[w][d];
+          wave_cnt[w][d] = run;
+          run += c;
+        }
+      }
+      __syncthreads();
+      // stage in digit-major order
+#pragma unroll
+      for (int r = 0; r < kSortRounds; ++r) {
+        const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+        if (e < n) {
+          const uint32_t dg = (key[r] >> sh) & 255u;
+          const uint32_t lp = tile_start[dg] + wave_cnt[wave][dg] + rank[r];
+          stage_key[lp] = key[r];
+          stage_val[lp] = val[r];
+        }
+      }
+      __syncthreads();
+      // coalesced write of the staged tile
+      const int cnt = min(kSortTile, n - t0);
+      for (int i = threadIdx.x; i < cnt; i += kSortThreads) {
+        const uint32_t kk = stage_key[i];
+        const uint32_t d = (kk >> sh) & 255u;
+        const uint32_t dst = bucket[d] + (uint32_t)i - tile_start[d];
+        if (dst < (uint32_t)n) {  // always true when the counts are right
+          kout[base + dst] = kk;
+          vout[base + dst] = stage_val[i];
+        }
       }
       __syncthreads();
       if (threadIdx.x < 256) {
-        uint32_t run = 0;
-        for (int w = 0; w < kSortWaves; ++w) {
-          uint32_t c = wave_cnt[w][threadIdx.x];
-          wave_cnt[w][threadIdx.x] = run;
-          run += c;
-        }
-        tile_tot[threadIdx.x] = run;
+        bucket[threadIdx.x] += tile_tot[threadIdx.x];
+        tile_tot[threadIdx.x] = 0u;
       }
-      __syncthreads();
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
-        const uint32_t dst = bucket[dg[r]] + wave_cnt[wave][dg[r]] + rank[r];
-        if (ok[r] && dst < (uint32_t)n) {  // always true when the counts are right
-          kout[base + dst] = key[r];
-          vout[base + dst] = val[r];
-        }
+        key[r] = nkey[r];
+        val[r] = nval[r];
       }
-      __syncthreads();
-      if (threadIdx.x < 256) bucket[threadIdx.x] += tile_tot[threadIdx.x];
-      __syncthreads();
     }
+    __syncthreads();  // the pass's output is the next pass's input
     kin = kout;
     vin = vout;
   }
 }
-
 
 certkv_status run_sort(const SortArgs& a, const SeqTab& st, hipStream_t s) {
   CERTKV_LAUNCH("sort_segments", seg_sort_kernel, dim3(a.g.H * st.count, a.g.L), dim3(kSortThreads),
