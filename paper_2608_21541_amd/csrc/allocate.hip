@@ -28,11 +28,19 @@
 
 namespace certkv {
 
-constexpr int kAllocThreads = 256;
-constexpr int kHeadGroup = 8;      // heads evaluated concurrently (32 threads each)
+constexpr int kAllocThreads = 1024;
+constexpr int kAllocWaves = kAllocThreads / 64;
+constexpr int kHeadGroup = kAllocThreads / 32;  // heads handled concurrently (32 threads each)
+constexpr int kCandCap = 1024;    // candidate blocks evaluated per round
 constexpr int kBlk = 256;          // ranks per pruning block
 constexpr int kLdsItems = 8192;    // H * blocks handled from LDS
 constexpr int kRepairWin = 64;     // cached curve values per head (fallback repair)
+
+// Lanes below this one among those set in `mask`.
+__device__ __forceinline__ uint32_t count_below64(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
 
 __device__ __forceinline__ bool lex_less(double f1, int b1, double f2, int b2) {
   return f1 < f2 || (f1 == f2 && b1 < b2);
@@ -137,10 +145,12 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   int32_t* cand = reinterpret_cast<int32_t*>(pool + kLdsItems * 4);
   double* pbm = reinterpret_cast<double*>(pool);
   __shared__ double fbest[64];
-  __shared__ int32_t bbest[64], kstar[64], ccount[64], coff[65], cfill[64];
+  __shared__ int32_t bbest[64], kstar[64];
   __shared__ int32_t bcur[64], bhi[64];
-  __shared__ double redf[4];
-  __shared__ int32_t redb[4];
+  __shared__ double redf[kAllocWaves];
+  __shared__ double cres_f[kCandCap];
+  __shared__ int32_t cres_b[kCandCap];
+  __shared__ int32_t ncand, scan_pos;
   __shared__ int64_t cnt_lt[64], cnt_le[64];
   __shared__ float win[64][kRepairWin + 1];
 
@@ -177,16 +187,17 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     }
   }
   __syncthreads();
-  cm = fmax(fmax(redf[0], redf[1]), fmax(redf[2], redf[3]));
+  for (int w = 0; w < kAllocWaves; ++w) cm = fmax(cm, redf[w]);
   double lo = 0.0, hi = 2.0 * cm + 1.0;
 
   auto mh_at = [&](int h, int k) -> float {
     return fast ? mcache[h * nblk + k] : cmin[unit_index(g, l, b, h) * nblk_max + k];
   };
 
-  // argmin over [bmin, n-1] of fma(lam, b, c_h(b)) for every head -> out[h]
-  auto evaluate = [&](double lam, int32_t* out) {
-    // (a) + (b): per head, best-bound block evaluated exactly (32 threads)
+  // Per head, the block with the smallest bound fma(lambda, b0, min c) is
+  // evaluated exactly by 32 threads: (fbest, bbest) is then an exact upper
+  // bound of the head's minimum and kstar its block.
+  auto best_bound = [&](double lam) {
     for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
       const int h = h0 + hg;
       if (h < H) {
@@ -227,96 +238,18 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
           fbest[h] = r.f;
           bbest[h] = r.b;
           kstar[h] = ks;
-          ccount[h] = 0;
         }
       }
     }
     __syncthreads();
-    if (fast) {
-      // (c) candidate blocks grouped by head, then evaluated by all threads
-      for (int i = tid; i < H * nblk; i += kAllocThreads) {
-        const int h = i / nblk, k = i % nblk;
-        if (k < kfirst || k == kstar[h]) continue;
-        const int b0 = max(k * kBlk, bmin);
-        const double lb = fma(lam, (double)b0, (double)mcache[i]);
-        if (lex_less(lb, b0, fbest[h], bbest[h])) atomicAdd(&ccount[h], 1);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        int run = 0;
-        for (int h = 0; h < H; ++h) {
-          coff[h] = run;
-          cfill[h] = run;
-          run += ccount[h];
-        }
-        coff[H] = run;
-      }
-      __syncthreads();
-      for (int i = tid; i < H * nblk; i += kAllocThreads) {
-        const int h = i / nblk, k = i % nblk;
-        if (k < kfirst || k == kstar[h]) continue;
-        const int b0 = max(k * kBlk, bmin);
-        const double lb = fma(lam, (double)b0, (double)mcache[i]);
-        if (lex_less(lb, b0, fbest[h], bbest[h])) cand[atomicAdd(&cfill[h], 1)] = k;
-      }
-      __syncthreads();
-      for (int h = 0; h < H; ++h) {
-        const int c0 = coff[h], c1 = coff[h + 1];
-        if (c0 == c1) continue;
-        const float* ch = curves + lht_base(g, l, h, tok0);
-        double f = INFINITY;
-        int bb = 0x7fffffff;
-        int c = c0;
-        for (; c + 4 <= c1; c += 4) {
-          float cv[4];
-          int xs[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            xs[e] = cand[c + e] * kBlk + tid;
-            cv[e] = (xs[e] >= bmin && xs[e] <= n - 1) ? ch[xs[e]] : 0.f;
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (xs[e] >= bmin && xs[e] <= n - 1) {
-              const double v = fma(lam, (double)xs[e], (double)cv[e]);
-              if (lex_less(v, xs[e], f, bb)) {
-                f = v;
-                bb = xs[e];
-              }
-            }
-          }
-        }
-        for (; c < c1; ++c) {
-          const int x = cand[c] * kBlk + tid;
-          if (x >= bmin && x <= n - 1) {
-            const double v = fma(lam, (double)x, (double)ch[x]);
-            if (lex_less(v, x, f, bb)) {
-              f = v;
-              bb = x;
-            }
-          }
-        }
-        const BestFB r = wave_lexmin(f, bb);
-        if (lane == 0) {
-          redf[wave] = r.f;
-          redb[wave] = r.b;
-        }
-        __syncthreads();
-        if (tid == 0) {
-          double ff = fbest[h];
-          int b2 = bbest[h];
-          for (int w = 0; w < 4; ++w)
-            if (lex_less(redf[w], redb[w], ff, b2)) {
-              ff = redf[w];
-              b2 = redb[w];
-            }
-          fbest[h] = ff;
-          bbest[h] = b2;
-        }
-        __syncthreads();
-      }
-    } else {
-      // large problems: every other block re-checked by its head's 32 threads
+  };
+
+  // argmin over [bmin, n-1] of fma(lam, b, c_h(b)) for every head -> out[h],
+  // for problems whose block minima do not fit in LDS: per-head pruned scans
+  auto evaluate_scan = [&](double lam, int32_t* out) {
+    best_bound(lam);
+    {
+      // every other block re-checked by its head's 32 threads
       for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
         const int h = h0 + hg;
         if (h < H) {
@@ -348,6 +281,131 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     }
     if (tid < H) out[tid] = bbest[tid];
     __syncthreads();
+  };
+
+  // The same argmin with the block minima in LDS.
+  //  1. per head, the block with the smallest bound is evaluated exactly
+  //     (32 threads per head): an exact upper bound (f*, b*) of the minimum;
+  //  2. every other block whose bound undercuts (f*, b*) is a candidate;
+  //     candidates of all heads are gathered (up to kCandCap per round) and
+  //     evaluated one block per wave, all loads of a round in flight at once;
+  //  3. per head, the smallest (f, b) over its candidates and (f*, b*).
+  // Blocks left out cannot hold the answer (ties favour smaller b), so the
+  // result is the full scan's.
+  auto evaluate_fast = [&](double lam, int32_t* out) {
+    best_bound(lam);
+    if (tid == 0) scan_pos = 0;
+    __syncthreads();
+    const int nitems = H * nblk;
+    while (true) {
+      // gather candidates from scan_pos on, until the list is full
+      if (tid == 0) ncand = 0;
+      __syncthreads();
+      const int start = scan_pos;
+      int stop = nitems;
+      for (int i0 = start; i0 < nitems; i0 += kAllocThreads) {
+        const int i = i0 + tid;
+        bool take = false;
+        int h = 0, k = 0;
+        if (i < nitems) {
+          h = i / nblk;
+          k = i - h * nblk;
+          if (k >= kfirst && k != kstar[h]) {
+            const int b0 = max(k * kBlk, bmin);
+            const double lb = fma(lam, (double)b0, (double)mcache[i]);
+            take = lex_less(lb, b0, fbest[h], bbest[h]);
+          }
+        }
+        const uint64_t m = __ballot(take);
+        int slot0 = 0;
+        if (lane == 0 && m) slot0 = atomicAdd(&ncand, __popcll(m));
+        slot0 = __shfl(slot0, 0, 64);
+        const int slot = slot0 + (int)count_below64(m);
+        if (take && slot < kCandCap) cand[slot] = (h << 16) | k;
+        __syncthreads();
+        if (ncand > kCandCap) {  // overflow: this sweep is scanned again next round
+          stop = i0;
+          break;
+        }
+        if (ncand == kCandCap) {  // full: resume after this sweep
+          stop = i0 + kAllocThreads;
+          break;
+        }
+      }
+      __syncthreads();
+      const int C = min(ncand, kCandCap);
+      // evaluate: one candidate block per wave, up to 4 per wave per batch
+      for (int c0 = wave; c0 < C; c0 += 4 * kAllocWaves) {
+        float cv[4][kBlk / 64];
+        int it[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = c0 + q * kAllocWaves;
+          it[q] = c < C ? cand[c] : -1;
+          const int hq = it[q] < 0 ? 0 : (it[q] >> 16), kq = it[q] < 0 ? 0 : (it[q] & 0xffff);
+          const float* ch = curves + lht_base(g, l, hq, tok0);
+#pragma unroll
+          for (int e = 0; e < kBlk / 64; ++e) {
+            const int x = kq * kBlk + lane + 64 * e;
+            cv[q][e] = (it[q] >= 0 && x >= bmin && x <= n - 1) ? ch[x] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (it[q] < 0) continue;
+          const int kq = it[q] & 0xffff;
+          double f = INFINITY;
+          int bb = 0x7fffffff;
+#pragma unroll
+          for (int e = 0; e < kBlk / 64; ++e) {
+            const int x = kq * kBlk + lane + 64 * e;
+            if (x >= bmin && x <= n - 1) {
+              const double v = fma(lam, (double)x, (double)cv[q][e]);
+              if (lex_less(v, x, f, bb)) {
+                f = v;
+                bb = x;
+              }
+            }
+          }
+          const BestFB r = wave_lexmin(f, bb);
+          if (lane == 0) {
+            cres_f[c0 + q * kAllocWaves] = r.f;
+            cres_b[c0 + q * kAllocWaves] = r.b;
+          }
+        }
+      }
+      __syncthreads();
+      // per head: fold the candidates' minima into (f*, b*), 32 threads a head
+      for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+        const int h = h0 + hg;
+        if (h < H) {
+          double f = INFINITY;
+          int bb = 0x7fffffff;
+          for (int c = sub; c < C; c += 32) {
+            if ((cand[c] >> 16) == h && lex_less(cres_f[c], cres_b[c], f, bb)) {
+              f = cres_f[c];
+              bb = cres_b[c];
+            }
+          }
+          const BestFB r = half_wave_min(f, bb);
+          if (sub == 0 && lex_less(r.f, r.b, fbest[h], bbest[h])) {
+            fbest[h] = r.f;
+            bbest[h] = r.b;
+          }
+        }
+      }
+      if (tid == 0) scan_pos = stop;
+      __syncthreads();
+      if (stop >= nitems) break;
+    }
+    if (tid < H) out[tid] = bbest[tid];
+    __syncthreads();
+  };
+  auto evaluate = [&](double lam, int32_t* out) {
+    if (fast)
+      evaluate_fast(lam, out);
+    else
+      evaluate_scan(lam, out);
   };
 
   evaluate(hi, bhi);
