@@ -3,9 +3,10 @@
 // The top-b keys of a unit (score descending, ties by position) are exactly
 // the keys whose (radix key, position) pair is lexicographically <= the pair
 // at rank b-1 of the sort.  One workgroup streams the unit's scores in
-// position order, tests each key against that threshold, and compacts the
-// kept positions with wave ballots and a 4-wave prefix, so kept indices come
-// out ascending without a scatter.  The same pass sums (s)_+ over the evicted
+// position order (4096 positions per step, 4 consecutive per thread), tests
+// each key against that threshold, and compacts the kept positions with wave
+// ballots and a prefix over the 16 waves, so kept indices come out ascending
+// without a scatter.  The same pass sums (s)_+ over the evicted
 // keys and over all keys in fp64 (the tail mass and its normalizer).
 #include "stages.h"
 
@@ -61,14 +62,29 @@ __global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, const int32_t*
   }
 }
 
-__global__ __launch_bounds__(256) void select_kernel(
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelPer = 4;                        // consecutive positions per thread
+constexpr int kSelTile = kSelThreads * kSelPer;   // 4096 positions per iteration
+
+// Spread the 16 low bits of x to every fourth bit of a 64-bit word.
+__device__ __forceinline__ uint64_t spread4(uint64_t x) {
+  x &= 0xffffull;
+  x = (x | (x << 24)) & 0x000000ff000000ffull;
+  x = (x | (x << 12)) & 0x000f000f000f000full;
+  x = (x | (x << 6)) & 0x0303030303030303ull;
+  x = (x | (x << 3)) & 0x1111111111111111ull;
+  return x;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
     Geo g, SeqTab st, const float* __restrict__ scores, const uint32_t* __restrict__ sorted_keys,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ budgets,
     const int64_t* __restrict__ kept_offsets, int32_t* __restrict__ kept_idx, int64_t capacity,
     double* __restrict__ evicted_sum, double* __restrict__ total_sum, uint64_t* __restrict__ bm,
     int32_t bm_stride) {
-  __shared__ int32_t wcount[4];
-  __shared__ double dsum[2][4];
+  __shared__ int32_t wtot[2][kSelWaves];
+  __shared__ double dsum[2][kSelWaves];
   const int h = blockIdx.x % g.H;
   const int bl = blockIdx.x / g.H;
   const int l = blockIdx.y;
@@ -88,32 +104,65 @@ __global__ __launch_bounds__(256) void select_kernel(
   const int64_t off = kept_offsets[u];
   int64_t run = 0;
   double se = 0.0, sa = 0.0;
-  for (int j0 = 0; j0 < n; j0 += 256) {
-    const int j = j0 + threadIdx.x;
-    const bool valid = j < n;
-    const float s = valid ? scores[base + j] : 0.f;
-    const uint32_t key = desc_key(s);
-    const bool keep = valid && (key < kthr || (key == kthr && j <= ithr));
-    if (valid) {
-      const double sp = s > 0.f ? (double)s : 0.0;
-      sa += sp;
-      if (!keep) se += sp;
+  auto load = [&](int j0, float (&sv)[kSelPer]) {
+#pragma unroll
+    for (int r = 0; r < kSelPer; ++r) {
+      const int j = j0 + kSelPer * threadIdx.x + r;
+      sv[r] = j < n ? scores[base + j] : 0.f;
     }
-    const uint64_t bal = __ballot(keep);
-    const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
-                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-    if (lane == 0) {
-      wcount[wave] = __popcll(bal);
-      const int word = (j0 >> 6) + wave;
-      if (bm && word < bm_stride) bm[u * bm_stride + word] = bal;
+  };
+  float cur[kSelPer], nxt[kSelPer];
+  load(0, cur);
+  for (int j0 = 0, it = 0; j0 < n; j0 += kSelTile, ++it) {
+    if (j0 + kSelTile < n) load(j0 + kSelTile, nxt);
+    const int jt = j0 + kSelPer * threadIdx.x;
+    bool keep[kSelPer];
+    uint64_t bal[kSelPer];
+    uint32_t below = 0, wsum = 0;
+#pragma unroll
+    for (int r = 0; r < kSelPer; ++r) {
+      const int j = jt + r;
+      const bool valid = j < n;
+      const uint32_t key = desc_key(cur[r]);
+      keep[r] = valid && (key < kthr || (key == kthr && j <= ithr));
+      if (valid) {
+        const double sp = cur[r] > 0.f ? (double)cur[r] : 0.0;
+        sa += sp;
+        if (!keep[r]) se += sp;
+      }
+      bal[r] = __ballot(keep[r]);
+      below += __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[r] >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal[r], 0u));
+      wsum += (uint32_t)__popcll(bal[r]);
     }
+    // kept bitmap: lanes 16q..16q+15 of the wave cover word q of its 256 positions
+    if (bm && lane < 4) {
+      uint64_t word = 0;
+#pragma unroll
+      for (int r = 0; r < kSelPer; ++r) word |= spread4(bal[r] >> (16 * lane)) << r;
+      const int widx = (j0 >> 6) + wave * 4 + lane;
+      if (widx < bm_stride) bm[u * bm_stride + widx] = word;
+    }
+    if (lane == 0) wtot[it & 1][wave] = (int32_t)wsum;
     __syncthreads();
     int64_t pre = run;
-    for (int w = 0; w < wave; ++w) pre += wcount[w];
-    const int64_t dst = off + pre + below;
-    if (keep && dst < capacity) kept_idx[dst] = j;
-    run += wcount[0] + wcount[1] + wcount[2] + wcount[3];
-    __syncthreads();
+    int64_t tile = 0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      const int32_t c = wtot[it & 1][w];
+      if (w < wave) pre += c;
+      tile += c;
+    }
+    int64_t dst = off + pre + below;
+#pragma unroll
+    for (int r = 0; r < kSelPer; ++r) {
+      if (keep[r]) {
+        if (dst < capacity) kept_idx[dst] = jt + r;
+        ++dst;
+      }
+    }
+    run += tile;
+#pragma unroll
+    for (int r = 0; r < kSelPer; ++r) cur[r] = nxt[r];
   }
   se = wave_sum(se);
   sa = wave_sum(sa);
@@ -123,8 +172,13 @@ __global__ __launch_bounds__(256) void select_kernel(
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    if (evicted_sum) evicted_sum[u] = dsum[0][0] + dsum[0][1] + dsum[0][2] + dsum[0][3];
-    if (total_sum) total_sum[u] = dsum[1][0] + dsum[1][1] + dsum[1][2] + dsum[1][3];
+    double e = 0.0, t = 0.0;
+    for (int w = 0; w < kSelWaves; ++w) {
+      e += dsum[0][w];
+      t += dsum[1][w];
+    }
+    if (evicted_sum) evicted_sum[u] = e;
+    if (total_sum) total_sum[u] = t;
   }
 }
 
@@ -208,7 +262,7 @@ certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64
 }
 
 certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s) {
-  CERTKV_LAUNCH("select", select_kernel, dim3(a.g.H * st.count, a.g.L), dim3(256), 0, s, a.g, st,
+  CERTKV_LAUNCH("select", select_kernel, dim3(a.g.H * st.count, a.g.L), dim3(kSelThreads), 0, s, a.g, st,
                 a.scores, a.sorted_keys, a.perm, (const int32_t*)a.budgets,
                 (const int64_t*)a.kept_offsets, a.kept_idx, a.capacity, a.evicted_sum, a.total_sum,
                 a.bitmap, a.bm_stride);
