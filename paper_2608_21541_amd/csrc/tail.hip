@@ -153,22 +153,41 @@ __global__ __launch_bounds__(kTailThreads) void tail_gather_kernel(
   double ak[EPL], av[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) ak[e] = av[e] = 0.0;
-  for (int i = i0 + ri; i < i1; i += RPS) {
-    const int j = min(max(kept_idx[off + i], 0), n - 1);  // caller indices clamped
-    const uint4 kq = *reinterpret_cast<const uint4*>(kb + (int64_t)j * k_st + ci * EPL);
-    const uint4 vq = *reinterpret_cast<const uint4*>(vb + (int64_t)j * v_st + ci * EPL);
-    if (DO_COMPACT) {
-      *reinterpret_cast<uint4*>(k_packed + (poff + i) * D + ci * EPL) = kq;
-      *reinterpret_cast<uint4*>(v_packed + (poff + i) * D + ci * EPL) = vq;
-      if (ci == 0) pos_packed[poff + i] = j;
-    }
-    if (DO_TAIL) {
-      const float s = scores[sbase + j];
-      const double w = s > 0.f ? (double)s : 0.0;
+  // Four rows per lane group per step: their indices, then their rows and
+  // scores, are loaded together so that each step waits for two round trips.
+  constexpr int UR = 4;
+  for (int i = i0 + ri; i < i1; i += RPS * UR) {
+    int j[UR];
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) {
-        ak[e] = fma(w, (double)elem_f32<T>(kq, e), ak[e]);
-        av[e] = fma(w, (double)elem_f32<T>(vq, e), av[e]);
+    for (int q = 0; q < UR; ++q) {
+      const int ii = i + q * RPS;
+      j[q] = ii < i1 ? min(max(kept_idx[off + ii], 0), n - 1) : -1;  // caller indices clamped
+    }
+    uint4 kq[UR], vq[UR];
+    float sv[UR];
+#pragma unroll
+    for (int q = 0; q < UR; ++q) {
+      const int jj = j[q] < 0 ? 0 : j[q];
+      kq[q] = *reinterpret_cast<const uint4*>(kb + (int64_t)jj * k_st + ci * EPL);
+      vq[q] = *reinterpret_cast<const uint4*>(vb + (int64_t)jj * v_st + ci * EPL);
+      sv[q] = DO_TAIL ? scores[sbase + jj] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < UR; ++q) {
+      if (j[q] < 0) continue;
+      const int ii = i + q * RPS;
+      if (DO_COMPACT) {
+        *reinterpret_cast<uint4*>(k_packed + (poff + ii) * D + ci * EPL) = kq[q];
+        *reinterpret_cast<uint4*>(v_packed + (poff + ii) * D + ci * EPL) = vq[q];
+        if (ci == 0) pos_packed[poff + ii] = j[q];
+      }
+      if (DO_TAIL) {
+        const double w = sv[q] > 0.f ? (double)sv[q] : 0.0;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+          ak[e] = fma(w, (double)elem_f32<T>(kq[q], e), ak[e]);
+          av[e] = fma(w, (double)elem_f32<T>(vq[q], e), av[e]);
+        }
       }
     }
   }
