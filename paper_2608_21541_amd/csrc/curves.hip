@@ -44,6 +44,29 @@ __device__ __forceinline__ void unpack_dims(uint32_t raw0, uint32_t raw1, float 
   }
 }
 
+// One transpose-reduce step over lane bit 5 (half = true) or 4: lanes with
+// the bit clear end with lo + partner's lo, lanes with it set with hi +
+// partner's hi.  v_permlane32_swap exchanges the upper half-wave of its first
+// operand with the lower half-wave of its second (v_permlane16_swap likewise
+// for odd and even rows of 16), which is exactly that exchange.
+__device__ __forceinline__ double combine_swap(double lo, double hi, bool half) {
+  const uint64_t a = (uint64_t)__double_as_longlong(lo);
+  const uint64_t b = (uint64_t)__double_as_longlong(hi);
+  uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32), b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+  if (half) {
+    const auto r0 = __builtin_amdgcn_permlane32_swap(a0, b0, false, false);
+    const auto r1 = __builtin_amdgcn_permlane32_swap(a1, b1, false, false);
+    a0 = r0[0]; b0 = r0[1]; a1 = r1[0]; b1 = r1[1];
+  } else {
+    const auto r0 = __builtin_amdgcn_permlane16_swap(a0, b0, false, false);
+    const auto r1 = __builtin_amdgcn_permlane16_swap(a1, b1, false, false);
+    a0 = r0[0]; b0 = r0[1]; a1 = r1[0]; b1 = r1[1];
+  }
+  const double x = __longlong_as_double((long long)(((uint64_t)a1 << 32) | a0));
+  const double y = __longlong_as_double((long long)(((uint64_t)b1 << 32) | b0));
+  return x + y;
+}
+
 template <int D, bool BF16>
 __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     Geo g, SeqTab st, const uint32_t* __restrict__ sorted_keys, const int32_t* __restrict__ perm,
@@ -230,6 +253,8 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
         if (((r >> lev) & 1) == 0) {
           pend[lev] = cur;
           placed = true;
+        } else if (lev < 2) {
+          cur = combine_swap(pend[lev], cur, lev == 0);
         } else {
           const int msk = 32 >> lev;
           const bool up = (lane & msk) != 0;
