@@ -44,6 +44,14 @@ __device__ __forceinline__ void unpack_dims(uint32_t raw0, uint32_t raw1, float 
   }
 }
 
+// Lane r's value of x, as a wave-uniform (scalar) value.
+__device__ __forceinline__ double lane_f64(double x, int r) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, r);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), r);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // One transpose-reduce step over lane bit 5 (half = true) or 4: lanes with
 // the bit clear end with lo + partner's lo, lanes with it set with hi +
 // partner's hi.  v_permlane32_swap exchanges the upper half-wave of its first
@@ -77,7 +85,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   __shared__ double tW[kCurveWaves][D];   // phase-1 totals per wave
   __shared__ double tQ[kCurveWaves];
   __shared__ double tM[kCurveWaves];
-  __shared__ double a_lds[kCurveWaves][kRPW];
   // chunk carry (suffix sums above the chunk), double-buffered by chunk
   // parity: the last wave writes the next carry while others may still read
   // the current one
@@ -136,7 +143,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   auto fetch_rows = [&](int pos, uint32_t (&raw)[kRPW][RAW]) {
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
-      const int pr = __shfl(pos, r, 64);
+      const int pr = __builtin_amdgcn_readlane(pos, r);  // uniform: one SGPR
       const uint32_t off = (uint32_t)pr * vrow_bytes + vlane;
       if (RAW == 2) {
         const uint2 w2 = buf_load_u64(vrs, off);
@@ -171,8 +178,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     // pipeline: order entries two chunks ahead, value rows one chunk ahead
     fetch_meta(k - 2, k_n2, p_n2, ok_n2);
     fetch_rows(p_n1, vnext);
-    if (lane < kRPW) a_lds[wave][lane] = a_cur;
-    __builtin_amdgcn_wave_barrier();
 
     // phase 1: totals of the wave's rows
     {
@@ -181,7 +186,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       for (int t = 0; t < DP; ++t) sW[t] = 0.0;
 #pragma unroll
       for (int r = 0; r < kRPW; ++r) {
-        const double ar = a_lds[wave][r];
+        const double ar = lane_f64(a_cur, r);
         float v[DP];
         unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
         double vv = 0.0;
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     double c2 = 0.0;
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
-      const double ar = a_lds[wave][r];
+      const double ar = lane_f64(a_cur, r);
       float v[DP];
       unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
       double vv = 0.0, w2 = 0.0;
