@@ -3,8 +3,8 @@
 // m, W and Q the suffix sums of a, a v and a |v|^2.
 //
 // One workgroup (16 waves) per unit walks the ranks from the top (rank n-1)
-// down in chunks of 256.  Wave w owns the 16 ranks [256k + 16(15-w),
-// 256k + 16(16-w)) of chunk k and lane i owns dims DP*i..DP*i+DP-1
+// down in chunks of 512.  Wave w owns the 32 ranks [512k + 32(15-w),
+// 512k + 32(16-w)) of chunk k and lane i owns dims DP*i..DP*i+DP-1
 // (DP = d/64).  Per chunk:
 //   phase 1  each wave forms the totals of its 16 rows: m, W (per dim) and
 //            Q (sum of a |v|^2);
@@ -14,7 +14,7 @@
 //            lane-local part q of Q; per rank each lane forms
 //            x = m q - |W|^2 over its dims (lane 0 adds m * Q_carry) and a
 //            transpose-reduce over the 64 lanes, folded in as the ranks are
-//            produced, yields c^2 of all 16 ranks.  The last wave's final
+//            produced, yields c^2 of all 32 ranks.  The last wave's final
 //            state is the carry of the next chunk.
 // The gathers are software-pipelined: while chunk k is computed, the value
 // rows of chunk k-1 are in flight and the order/score entries of chunk k-2
@@ -26,8 +26,9 @@ namespace certkv {
 
 constexpr int kCurveThreads = 1024;
 constexpr int kCurveWaves = kCurveThreads / 64;
-constexpr int kRPW = 16;                          // ranks per wave and chunk
-constexpr int kCurveChunk = kCurveWaves * kRPW;   // 256 ranks
+constexpr int kRPW = 32;                          // ranks per wave and chunk
+constexpr int kLev = kRPW == 32 ? 5 : (kRPW == 16 ? 4 : 3);  // log2(kRPW)
+constexpr int kCurveChunk = kCurveWaves * kRPW;   // 512 ranks
 
 template <int DP, bool BF16>
 __device__ __forceinline__ void unpack_dims(uint32_t raw0, uint32_t raw1, float (&v)[DP]) {
@@ -138,7 +139,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     return tot > 0.0 ? (s > 0.f ? (double)s / tot : 0.0) : inv_n;
   };
   auto row_of = [&](int pos, bool valid) { return valid ? min(max(pos, 0), n - 1) : 0; };
-  // Value rows of the 16 ranks of chunk k (row 0 stands in for absent ranks,
+  // Value rows of the 32 ranks of chunk k (row 0 stands in for absent ranks,
   // whose weight is zero).
   auto fetch_rows = [&](int pos, uint32_t (&raw)[kRPW][RAW]) {
 #pragma unroll
@@ -227,12 +228,12 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       if (RAW == 2) __asm__ volatile("" : "+v"(vcur[r][RAW - 1]));
     }
     // phase 2: walk the ranks top-down.  Streaming transpose-reduce of the
-    // per-lane values over lane bits 5..2: ranks 2i and 2i+1 combine over
+    // per-lane values over lane bits 5, 4, ...: ranks 2i and 2i+1 combine over
     // lane bit 5 as soon as both exist, pairs of those over bit 4, and so on,
-    // so at most one pending value per level is live.  Lane bits (5, 4, 3, 2)
-    // end up naming rank bits (0, 1, 2, 3).
+    // so at most one pending value per level is live.  Lane bit 5 - j ends up
+    // naming rank bit j.
     double q = 0.0;
-    double pend[4];
+    double pend[kLev];
     double c2 = 0.0;
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       if (lane == 0) cur = fma(m, Qc, cur);
       bool placed = false;
 #pragma unroll
-      for (int lev = 0; lev < 4; ++lev) {
+      for (int lev = 0; lev < kLev; ++lev) {
         if (placed) continue;
         if (((r >> lev) & 1) == 0) {
           pend[lev] = cur;
@@ -270,12 +271,14 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       }
       if (!placed) c2 = cur;
     }
-    c2 += __shfl_xor(c2, 1, 64);
-    c2 += __shfl_xor(c2, 2, 64);
-    const int r_mine = ((lane >> 5) & 1) | (((lane >> 4) & 1) << 1) | (((lane >> 3) & 1) << 2) |
-                       (((lane >> 2) & 1) << 3);
+    // the lanes sharing a rank: add their copies
+#pragma unroll
+    for (int m2 = 1; m2 < 64 / kRPW; m2 <<= 1) c2 += __shfl_xor(c2, m2, 64);
+    int r_mine = 0;
+#pragma unroll
+    for (int lev = 0; lev < kLev; ++lev) r_mine |= ((lane >> (5 - lev)) & 1) << lev;
     const int rk = rank_of(k, r_mine);
-    if ((lane & 3) == 0 && rk < n) curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
+    if ((lane & (64 / kRPW - 1)) == 0 && rk < n) curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
     // the last wave's final state carries into the next chunk
     if (wave == kCurveWaves - 1) {
 #pragma unroll
