@@ -21,6 +21,8 @@
 // Ranking in input order and runs in tile order make every pass stable, so
 // equal scores keep ascending position.  The next tile's elements are loaded
 // while the current one is ranked.
+#include <type_traits>
+
 #include "stages.h"
 
 namespace certkv {
@@ -78,7 +80,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   __shared__ uint32_t bucket[256];      // running start of each digit's bucket
   __shared__ uint32_t tile_tot[256];    // digit counts of the tile
   __shared__ uint32_t tile_start[256];  // digit-major start inside the tile
-  __shared__ volatile uint32_t wave_cnt[kSortWaves][256];
+  __shared__ uint32_t wave_cnt[kSortWaves][256];
   __shared__ uint32_t stage_key[kSortTile];
   __shared__ int32_t stage_val[kSortTile];
   __shared__ double dred[kSortWaves];
@@ -106,7 +108,8 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
-        sv[r] = e < n ? scores[base + e] : 0.f;
+        const float x = scores[base + min(e, n - 1)];  // clamped: no branch around the load
+        sv[r] = e < n ? x : 0.f;
       }
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
@@ -130,9 +133,13 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
     ssum_out[u] = tot;
   }
 
-  const uint32_t* kin = nullptr;
-  const int32_t* vin = nullptr;
-  for (int p = 0; p < 4; ++p) {
+  // One pass per digit, instantiated per pass so that its input (the scores
+  // or the previous pass's output) is fixed at compile time and no branch
+  // splits the tile loads.
+  auto pass = [&](auto pass_tag) {
+    constexpr int p = decltype(pass_tag)::value;
+    const uint32_t* kin = p == 1 || p == 3 ? keysB : keysA;
+    const int32_t* vin = p == 1 || p == 3 ? valsB : valsA;
     uint32_t* kout = (p == 0 || p == 2) ? keysB : (p == 1 ? keysA : keys_out);
     int32_t* vout = (p == 0 || p == 2) ? valsB : (p == 1 ? valsA : perm_out);
     const int sh = 8 * p;
@@ -146,11 +153,14 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
         const bool ok = e < n;
         if (p == 0) {
-          key[r] = desc_key(ok ? scores[base + e] : 0.f);
+          const float x = scores[base + min(e, n - 1)];
+          key[r] = desc_key(ok ? x : 0.f);
           val[r] = e;
         } else {
-          key[r] = ok ? kin[base + e] : 0u;
-          val[r] = ok ? vin[base + e] : 0;
+          const uint32_t kx = kin[base + min(e, n - 1)];
+          const int32_t vx = vin[base + min(e, n - 1)];
+          key[r] = ok ? kx : 0u;
+          val[r] = ok ? vx : 0;
         }
       }
     };
@@ -230,9 +240,11 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
       }
     }
     __syncthreads();  // the pass's output is the next pass's input
-    kin = kout;
-    vin = vout;
-  }
+  };
+  pass(std::integral_constant<int, 0>());
+  pass(std::integral_constant<int, 1>());
+  pass(std::integral_constant<int, 2>());
+  pass(std::integral_constant<int, 3>());
 }
 
 certkv_status run_sort(const SortArgs& a, const SeqTab& st, hipStream_t s) {
