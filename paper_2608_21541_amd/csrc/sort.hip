@@ -197,11 +197,14 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         wave_scan256(tile_start, lane);
       } else if (threadIdx.x < 256 + 64) {
         const int d = threadIdx.x - 64;
+        uint32_t c[kSortWaves];
+#pragma unroll
+        for (int w = 0; w < kSortWaves; ++w) c[w] = wave_cnt[w][d];  // all reads in flight
         uint32_t run = 0;
+#pragma unroll
         for (int w = 0; w < kSortWaves; ++w) {
-          const uint32_t c = wave_cnt[w][d];
           wave_cnt[w][d] = run;
-          run += c;
+          run += c[w];
         }
       }
       __syncthreads();
@@ -219,13 +222,28 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
       __syncthreads();
       // coalesced write of the staged tile
       const int cnt = min(kSortTile, n - t0);
-      for (int i = threadIdx.x; i < cnt; i += kSortThreads) {
-        const uint32_t kk = stage_key[i];
-        const uint32_t d = (kk >> sh) & 255u;
-        const uint32_t dst = bucket[d] + (uint32_t)i - tile_start[d];
-        if (dst < (uint32_t)n) {  // always true when the counts are right
-          kout[base + dst] = kk;
-          vout[base + dst] = stage_val[i];
+      {
+        uint32_t kk[kSortRounds], dst[kSortRounds];
+        int32_t vv[kSortRounds];
+#pragma unroll
+        for (int r = 0; r < kSortRounds; ++r) {
+          const int i = threadIdx.x + r * kSortThreads;
+          kk[r] = i < cnt ? stage_key[i] : 0u;
+          vv[r] = i < cnt ? stage_val[i] : 0;
+        }
+#pragma unroll
+        for (int r = 0; r < kSortRounds; ++r) {
+          const int i = threadIdx.x + r * kSortThreads;
+          const uint32_t d = (kk[r] >> sh) & 255u;
+          dst[r] = bucket[d] + (uint32_t)i - tile_start[d];
+        }
+#pragma unroll
+        for (int r = 0; r < kSortRounds; ++r) {
+          const int i = threadIdx.x + r * kSortThreads;
+          if (i < cnt && dst[r] < (uint32_t)n) {  // always true when the counts are right
+            kout[base + dst[r]] = kk[r];
+            vout[base + dst[r]] = vv[r];
+          }
         }
       }
       __syncthreads();
