@@ -12,11 +12,11 @@
 // [2^-60, 2^120] (where fp32 exponentials could under- or overflow) flags its
 // unit, and a fallback pass recomputes that unit's partials with a running
 // maximum; it returns immediately for units that are not flagged.
-// The contraction runs on MFMA v_mfma_f32_16x16x32_bf16 with key tiles as the
-// A operand (rows = 16 keys, held in VGPRs straight from HBM) and the window
-// queries as the B operand (columns = 16 queries, staged once per workgroup in
+// The contraction runs on MFMA v_mfma_f32_32x32x16_bf16 with key tiles as the
+// A operand (rows = 32 keys, held in VGPRs straight from HBM) and the window
+// queries as the B operand (columns = 32 queries, staged once per workgroup in
 // LDS).  Each lane owns one query column, so row sums are lane-local and
-// per-key sums are one transposed reduction per 64 keys.
+// per-key sums are one transposed reduction per wave iteration.
 #include <type_traits>
 
 #include "stages.h"
@@ -24,11 +24,10 @@
 namespace certkv {
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
-typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+typedef float f32x16_t __attribute__((__vector_size__(16 * sizeof(float))));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kScoreThreads = 512;  // 8 waves
-constexpr int kScoreKT = 2;         // 16-key tiles per wave iteration
 constexpr float kSumLo = 8.673617379884035e-19f;  // 2^-60
 constexpr float kSumHi = 1.329227995784916e+36f;  // 2^120
 
@@ -46,23 +45,40 @@ struct ScoreSmem {
 
 enum { kPass1Sum = 0, kPass1Max = 1, kPass2 = 2 };
 
-// MFMA v_mfma_f32_16x16x32_bf16 layout used below (per 64-lane wave):
-//   A (16 keys x 32 dims): lane (grp = lane/16, c = lane%16) supplies key c,
-//     8 consecutive dims of its group's slice;
-//   B (32 dims x 16 queries): the same lane supplies query c, same dims;
-//   D (16 x 16): lane (grp, c) holds query column c, key rows 4*grp + r,
-//     r = 0..3.
-// Each lane group owns a contiguous quarter of the head dimension for all of
-// its k-steps, so a lane loads one 2*D/4-byte run of its key row.
-template <int D, int NQT, int KT, int MODE>
-__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((MODE == kPass2 || NQT > 16) ? 2 : 4, 8))) void score_mfma_kernel(
+// One round of a transpose-reduce over lane bit M: lanes with that bit set
+// keep the upper HALF of their 2*HALF values, the others the lower HALF, and
+// each adds its partner's copy of the half it keeps.  The rounds recurse at
+// compile time (HALF and M halve) so that every register index is a constant.
+template <int HALF, int M>
+__device__ __forceinline__ void xpose_round(float* v, int lane) {
+  const bool up = (lane & M) != 0;
+#pragma unroll
+  for (int i = 0; i < HALF; ++i) {
+    const float keep = up ? v[HALF + i] : v[i];
+    const float send = up ? v[i] : v[HALF + i];
+    v[i] = keep + __shfl_xor(send, M, 64);
+  }
+  if constexpr (HALF > 1 && M > 1) xpose_round<HALF / 2, M / 2>(v, lane);
+}
+
+// MFMA v_mfma_f32_32x32x16_bf16 layout used below (per 64-lane wave):
+//   A (32 keys x 16 dims): lane (hh = lane/32, c = lane%32) supplies key c,
+//     8 dims of its half's slice;
+//   B (16 dims x 32 queries): the same lane supplies query c, same dims;
+//   D (32 x 32): lane (hh, c) holds query column c, key rows
+//     8*(v/4) + 4*hh + v%4 for v = 0..15.
+// The contraction order is free, so lane half hh owns the contiguous dims
+// hh*D/2 .. hh*D/2 + D/2 - 1 for all of its k-steps: a lane loads one D-byte
+// run of its key row, and k-step s takes its dims 8*s .. 8*s + 7.
+template <int D, int NQT, int MODE>
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((MODE == kPass2 || NQT > 8) ? 2 : 4, 8))) void score_mfma_kernel(
     Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
     int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
     int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, float2* __restrict__ part,
     const float* __restrict__ lse2, const int32_t* __restrict__ flag,
     float* __restrict__ scores, float* __restrict__ kpart) {
-  constexpr int KS = D / 32;   // MFMA k-steps
-  constexpr int QD = D / 4;    // dims per lane group
+  constexpr int KS = D / 16;   // MFMA k-steps
+  constexpr int HD = D / 2;    // dims per lane half
   constexpr int RE = ScoreSmem<D>::kRowElems;
   constexpr bool P2 = MODE == kPass2;
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -80,7 +96,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
   if (key_begin >= n) return;
   const int key_end = min(n, key_begin + keys_per_block);
   const int M = g.w * g.G;
-  const int Mp = NQT * 16;  // rows padded to whole 16-query tiles
+  const int Mp = NQT * 32;  // rows padded to whole 32-query tiles
   const int64_t u = unit_index(g, l, b, h);
   if (MODE == kPass1Max && flag[u] == 0) return;
 
@@ -118,8 +134,8 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int grp = lane >> 4;
-  const int c16 = lane & 15;
+  const int hh = lane >> 5;
+  const int c32 = lane & 31;
   const float c2 = g.scale * kLog2e;
   const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
   const uint16_t* kbase = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
@@ -130,94 +146,123 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
   for (int i = 0; i < NQT; ++i) srun[i] = 0.f;
 #pragma unroll
   for (int i = 0; i < (MODE == kPass1Max ? NQT : 1); ++i) mrun[i] = -INFINITY;
-  float kacc[P2 ? QD : 1];  // pass 2: weighted key sum over this lane's dims
+  float kacc[P2 ? HD : 1];  // pass 2: weighted key sum over this lane's dims
 #pragma unroll
-  for (int i = 0; i < (P2 ? QD : 1); ++i) kacc[i] = 0.f;
+  for (int i = 0; i < (P2 ? HD : 1); ++i) kacc[i] = 0.f;
 
-  constexpr int KPW = 16 * KT;        // keys per wave iteration
+  constexpr int KPW = 32;             // keys per wave iteration
   constexpr int KPI = KPW * kScoreThreads / 64;  // keys per workgroup iteration
-  constexpr int NV = 4 * KT;          // per-lane D values per query tile
+  constexpr int NV = 16;              // per-lane values per query tile
   for (int it = key_begin + wave * KPW; it < key_end; it += KPI) {
-    // KT 16-key tiles (keys it..it+KPW-1) as A fragments, straight from HBM.
-    Frag kf[KT][KS];
+    // The 32-key tile (keys it..it+31) as A fragments, straight from HBM.
+    Frag kf[KS];
+    {
+      const int key = it + c32;
+      const int keyc = key < n ? key : n - 1;
+      const uint4* src = reinterpret_cast<const uint4*>(kbase + (int64_t)keyc * k_st + hh * HD);
 #pragma unroll
-    for (int t = 0; t < KT; ++t) {
-      int key = it + t * 16 + c16;
-      int keyc = key < n ? key : n - 1;
-      const uint4* src = reinterpret_cast<const uint4*>(kbase + (int64_t)keyc * k_st + grp * QD);
-#pragma unroll
-      for (int s = 0; s < KS; ++s) kf[t][s].u = src[s];
+      for (int s = 0; s < KS; ++s) kf[s].u = src[s];
     }
     const bool need_mask = (it + KPW - 1 >= first_masked) || (it + KPW - 1 >= n);
-    float ssum[KT][4];
+    float ssum[P2 ? NV : 1];
 #pragma unroll
-    for (int t = 0; t < KT; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) ssum[t][r] = 0.f;
+    for (int i = 0; i < (P2 ? NV : 1); ++i) ssum[i] = 0.f;
 
-    // The query-tile loop is instantiated twice, with and without the
-    // causal / tail mask, so that no branch splits it (a branch lets the
-    // compiler sink every tile's exponentials below all the MFMAs, which
-    // keeps every tile's accumulators live at once).
+    // The query-tile loop is software-pipelined: the MFMA chain of tile qt+1
+    // is interleaved with the masking and exponentials of tile qt (a slice
+    // of 16/KS values behind each MFMA), so that the matrix core and the VALU
+    // of one wave work at once; gfx950 overlaps them within a wave, not
+    // across waves.  It is instantiated with and without the causal / tail
+    // mask so that no branch splits it.
     auto tiles = [&](auto masked_tag) {
       constexpr bool MASKED = decltype(masked_tag)::value;
+      constexpr int SL = 16 / KS;  // values of the current tile per k-step
+      // value v of the current tile's accumulator, masked and scaled
+      auto logit = [&](const f32x16_t& acc, int v, int lim) {
+        float x = acc[v];
+        if (MASKED && it + 8 * (v >> 2) + 4 * hh + (v & 3) > lim) x = -INFINITY;
+        return x;
+      };
+      f32x16_t acc;
 #pragma unroll
-    for (int qt = 0; qt < NQT; ++qt) {
-      f32x4_t acc[KT];
+      for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+      {
+        const uint16_t* qrow = q_lds + c32 * RE + hh * HD;
 #pragma unroll
-      for (int t = 0; t < KT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      const uint16_t* qrow = q_lds + (qt * 16 + c16) * RE + grp * QD;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        Frag qf;
-        qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
-#pragma unroll
-        for (int t = 0; t < KT; ++t)
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t][s].v, qf.v, acc[t], 0, 0, 0);
+        for (int s = 0; s < KS; ++s) {
+          Frag qf;
+          qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf.v, acc, 0, 0, 0);
+        }
       }
-      if (MASKED) {
-        const int lim = lim_lds[qt * 16 + c16];
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int t = 0; t < KT; ++t)
+      for (int qt = 0; qt < NQT; ++qt) {
+        const bool more = qt + 1 < NQT;
+        const int lim = MASKED ? lim_lds[qt * 32 + c32] : 0;
+        f32x16_t nacc;
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (it + t * 16 + grp * 4 + r > lim) acc[t][r] = -INFINITY;
-      }
-      if (MODE == kPass1Sum) {
-        float sacc = 0.f;
+        for (int v = 0; v < 16; ++v) nacc[v] = 0.f;
+        const uint16_t* qrow = q_lds + ((qt + 1) * 32 + c32) * RE + hh * HD;
+        if (MODE == kPass1Max) {
+          // fallback pass: a running maximum needs the whole tile first
+          if (more) {
 #pragma unroll
-        for (int t = 0; t < KT; ++t)
+            for (int s = 0; s < KS; ++s) {
+              Frag qf;
+              qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+              nacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf.v, nacc, 0, 0, 0);
+            }
+          }
+          float mx = logit(acc, 0, lim);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) sacc += __builtin_amdgcn_exp2f(acc[t][r] * c2);
-        srun[qt] += sacc;
-      } else if (MODE == kPass1Max) {
-        float mx = acc[0][0];
+          for (int v = 1; v < 16; ++v) mx = fmaxf(mx, logit(acc, v, lim));
+          const float mnew = fmaxf(mrun[qt], mx * c2);
+          if (mnew != -INFINITY) {
+            const float sc = __builtin_amdgcn_exp2f(mrun[qt] - mnew);
+            float sacc = 0.f;
 #pragma unroll
-        for (int t = 0; t < KT; ++t)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[t][r]);
-        const float mnew = fmaxf(mrun[qt], mx * c2);
-        if (mnew != -INFINITY) {
-          const float sc = __builtin_amdgcn_exp2f(mrun[qt] - mnew);
+            for (int v = 0; v < 16; ++v)
+              sacc += __builtin_amdgcn_exp2f(fmaf(logit(acc, v, lim), c2, -mnew));
+            srun[qt] = fmaf(srun[qt], sc, sacc);
+            mrun[qt] = mnew;
+          }
+        } else {
+          const float l2 = P2 ? lse_lds[qt * 32 + c32] : 0.f;
           float sacc = 0.f;
 #pragma unroll
-          for (int t = 0; t < KT; ++t)
+          for (int s = 0; s < KS; ++s) {
+            if (more) {
+              Frag qf;
+              qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+              nacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s].v, qf.v, nacc, 0, 0, 0);
+            }
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sacc += __builtin_amdgcn_exp2f(fmaf(acc[t][r], c2, -mnew));
-          srun[qt] = fmaf(srun[qt], sc, sacc);
-          mrun[qt] = mnew;
+            for (int j = 0; j < SL; ++j) {
+              const int v = s * SL + j;
+              const float x = logit(acc, v, lim);
+              if (P2)
+                ssum[v] += __builtin_amdgcn_exp2f(fmaf(x, c2, -l2));
+              else
+                sacc += __builtin_amdgcn_exp2f(x * c2);
+            }
+          }
+          if (!P2) srun[qt] += sacc;
+          if (more) {
+            // LDS reads two k-steps ahead of their MFMA, each k-step's VALU
+            // slice right behind its MFMA.
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 + (MASKED ? 1 : 0) + (P2 ? 1 : 0), 0);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x402, (MASKED ? 5 : 3) * SL, 0);
+              if (s + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+          }
         }
-      } else {
-        const float l2 = lse_lds[qt * 16 + c16];
-#pragma unroll
-        for (int t = 0; t < KT; ++t)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) ssum[t][r] += __builtin_amdgcn_exp2f(fmaf(acc[t][r], c2, -l2));
+        acc = nacc;
+        __builtin_amdgcn_sched_barrier(0);
       }
-      // Keep each query tile's LDS loads inside its own iteration: hoisting
-      // them across tiles multiplies the live fragments.
-      __builtin_amdgcn_sched_barrier(0);
-    }
     };
     if (need_mask)
       tiles(std::integral_constant<bool, true>());
@@ -225,50 +270,35 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       tiles(std::integral_constant<bool, false>());
 
     if (P2) {
-      // Sum each key's per-lane partials over the 16 query columns of its lane
-      // group.  Value i = 4*t + r of lane (grp, c16) belongs to key
-      // 16*t + 4*grp + r; a transpose-reduce over lane bits 8, 4, ... leaves
-      // value i = c16 / (16/NV) in lanes c16 = (16/NV)*i + j, and the last
-      // xor steps add the j copies.
+      // Sum each key's per-lane partials over the 32 query columns of its
+      // lane half.  Value v of lane (hh, c32) belongs to key
+      // 8*(v/4) + 4*hh + v%4; a transpose-reduce over lane bits 16, 8, 4, 2
+      // leaves value v = c32 / 2 in lanes c32 = 2*v + j, and the last xor
+      // step adds the two copies.
       float v[NV];
 #pragma unroll
-      for (int t = 0; t < KT; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[t * 4 + r] = ssum[t][r];
-#pragma unroll
-      for (int m = 8, half = NV / 2; half >= 1; m >>= 1, half >>= 1) {
-        const bool up = (lane & m) != 0;
-#pragma unroll
-        for (int i = 0; i < half; ++i) {
-          float keep = up ? v[half + i] : v[i];
-          float send = up ? v[i] : v[half + i];
-          v[i] = keep + __shfl_xor(send, m, 64);
-        }
-      }
-      constexpr int SPREAD = 16 / NV;  // lanes sharing one value index
+      for (int i = 0; i < NV; ++i) v[i] = ssum[i];
+      xpose_round<NV / 2, 16>(v, lane);
+      constexpr int SPREAD = 32 / NV;  // lanes sharing one value index
 #pragma unroll
       for (int m = SPREAD / 2; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, 64);
       const float s_mine = v[0];
-      const int i_mine = c16 / SPREAD;
-      const int key_mine = it + (i_mine >> 2) * 16 + grp * 4 + (i_mine & 3);
-      if ((c16 % SPREAD) == 0 && key_mine < n) scores[lht_base(g, l, h, tok0) + key_mine] = s_mine;
+      const int vi = c32 / SPREAD;
+      const int key_mine = it + 8 * (vi >> 2) + 4 * hh + (vi & 3);
+      if ((c32 % SPREAD) == 0 && key_mine < n) scores[lht_base(g, l, h, tok0) + key_mine] = s_mine;
       if (kpart) {
-        // Lane (grp, c16) holds key c16 of each tile over dims grp*QD..; the
-        // score of key (t, c16) is value 4*t + c16%4 of lane group c16/4.
+        // Lane (hh, c32) holds key c32 over dims hh*HD..; its score is
+        // value 4*(c32/8) + c32%4 of lane half (c32/4)%2.
+        const int src = 32 * ((c32 >> 2) & 1) + SPREAD * (4 * (c32 >> 3) + (c32 & 3));
+        float s_t = __shfl(s_mine, src, 64);
+        s_t = (it + c32 < n && s_t > 0.f) ? s_t : 0.f;
 #pragma unroll
-        for (int t = 0; t < KT; ++t) {
-          const int src = 16 * (c16 >> 2) + SPREAD * (4 * t + (c16 & 3));
-          float s_t = __shfl(s_mine, src, 64);
-          const int key = it + t * 16 + c16;
-          s_t = (key < n && s_t > 0.f) ? s_t : 0.f;
+        for (int s = 0; s < KS; ++s) {
+          const uint32_t* w4 = reinterpret_cast<const uint32_t*>(&kf[s].u);
 #pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            const uint32_t* w4 = reinterpret_cast<const uint32_t*>(&kf[t][s].u);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              kacc[s * 8 + 2 * e] = fmaf(s_t, bf16_lo(w4[e]), kacc[s * 8 + 2 * e]);
-              kacc[s * 8 + 2 * e + 1] = fmaf(s_t, bf16_hi(w4[e]), kacc[s * 8 + 2 * e + 1]);
-            }
+          for (int e = 0; e < 4; ++e) {
+            kacc[s * 8 + 2 * e] = fmaf(s_t, bf16_lo(w4[e]), kacc[s * 8 + 2 * e]);
+            kacc[s * 8 + 2 * e + 1] = fmaf(s_t, bf16_hi(w4[e]), kacc[s * 8 + 2 * e + 1]);
           }
         }
       }
@@ -278,13 +308,12 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
   constexpr int NW = kScoreThreads / 64;
   __syncthreads();  // every wave is done with the staged queries
   if (MODE == kPass1Sum) {
-    // Sum the four lane groups (same query column), then the waves.
+    // Sum the two lane halves (same query column), then the waves.
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
       float s0 = srun[qt];
-      s0 += __shfl_xor(s0, 16, 64);
       s0 += __shfl_xor(s0, 32, 64);
-      if (grp == 0) red_lds[wave * Mp + qt * 16 + c16] = s0;
+      if (hh == 0) red_lds[wave * Mp + qt * 32 + c32] = s0;
     }
     __syncthreads();
     for (int rho = threadIdx.x; rho < M; rho += kScoreThreads) {
@@ -296,20 +325,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
 #pragma unroll
     for (int qt = 0; qt < NQT; ++qt) {
       float m0 = mrun[qt], s0 = srun[qt];
-#pragma unroll
-      for (int msk = 16; msk <= 32; msk <<= 1) {
-        float mo = __shfl_xor(m0, msk, 64);
-        float so = __shfl_xor(s0, msk, 64);
-        float mn = fmaxf(m0, mo);
-        float sn = 0.f;
-        if (mn != -INFINITY)
-          sn = s0 * __builtin_amdgcn_exp2f(m0 - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
-        m0 = mn;
-        s0 = sn;
-      }
-      if (grp == 0) {
-        red_lds[(wave * Mp + qt * 16 + c16) * 2] = m0;
-        red_lds[(wave * Mp + qt * 16 + c16) * 2 + 1] = s0;
+      const float mo = __shfl_xor(m0, 32, 64);
+      const float so = __shfl_xor(s0, 32, 64);
+      const float mn = fmaxf(m0, mo);
+      float sn = 0.f;
+      if (mn != -INFINITY)
+        sn = s0 * __builtin_amdgcn_exp2f(m0 - mn) + so * __builtin_amdgcn_exp2f(mo - mn);
+      if (hh == 0) {
+        red_lds[(wave * Mp + qt * 32 + c32) * 2] = mn;
+        red_lds[(wave * Mp + qt * 32 + c32) * 2 + 1] = sn;
       }
     }
     __syncthreads();
@@ -326,24 +350,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       part[(u * nkb_max + kb) * M + rho] = make_float2(mt, sacc);
     }
   } else if (kpart) {
-    // Reduce the weighted key sums over the 16 lanes of each group, then over
+    // Reduce the weighted key sums over the 32 lanes of each half, then over
     // the waves.
-    float v[QD];
+    float v[HD];
 #pragma unroll
-    for (int i = 0; i < QD; ++i) v[i] = kacc[i];
+    for (int i = 0; i < HD; ++i) v[i] = kacc[i];
+    xpose_round<HD / 2, 16>(v, lane);
+    constexpr int PER = HD / 32;  // dims left per lane
 #pragma unroll
-    for (int m = 8, half = QD / 2; m >= 1; m >>= 1, half >>= 1) {
-      const bool up = (lane & m) != 0;
-#pragma unroll
-      for (int i = 0; i < half; ++i) {
-        float keep = up ? v[half + i] : v[i];
-        float send = up ? v[i] : v[half + i];
-        v[i] = keep + __shfl_xor(send, m, 64);
-      }
-    }
-    constexpr int PER = QD / 16;  // dims left per lane
-#pragma unroll
-    for (int e = 0; e < PER; ++e) red_lds[wave * D + grp * QD + c16 * PER + e] = v[e];
+    for (int e = 0; e < PER; ++e) red_lds[wave * D + hh * HD + c32 * PER + e] = v[e];
     __syncthreads();
     for (int dd = threadIdx.x; dd < D; dd += kScoreThreads) {
       float s = 0.f;
@@ -510,7 +525,7 @@ __global__ __launch_bounds__(256) void score_f32_kernel(
 size_t score_smem_bytes(const Geo& g, int32_t dtype) {
   const int M = g.w * g.G;
   if (dtype == CERTKV_BF16) {
-    const size_t Mp = (size_t)score_nqt(M) * 16;
+    const size_t Mp = (size_t)score_nqt(M) * 32;
     const size_t q = Mp * (g.D + 8) * 2;
     const size_t nw = kScoreThreads / 64;
     const size_t red = nw * (Mp * 2 > (size_t)g.D ? Mp * 2 : (size_t)g.D) * 4;
@@ -528,30 +543,30 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
   size_t smem = score_smem_bytes(g, CERTKV_BF16);
   static bool attr_set = false;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass1Sum>,
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass1Sum>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass1Max>,
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass1Max>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kScoreKT, kPass2>,
+    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass2>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
   const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
   const uint16_t* k = static_cast<const uint16_t*>(a.k.ptr);
-  CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kScoreKT, kPass1Sum>), grid,
+  CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kPass1Sum>), grid,
                 dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
                 a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
                 (const float*)nullptr, (const int32_t*)nullptr, (float*)nullptr, (float*)nullptr);
   CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
                 s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
   // fallback for flagged units (returns at once for the others)
-  CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kScoreKT, kPass1Max>), grid,
+  CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kPass1Max>), grid,
                 dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
                 a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
                 (const float*)nullptr, (const int32_t*)a.flag, (float*)nullptr, (float*)nullptr);
   CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
                 0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 1);
-  CERTKV_LAUNCH("score_pass2_mfma", (score_mfma_kernel<D, NQT, kScoreKT, kPass2>), grid, dim3(kScoreThreads),
+  CERTKV_LAUNCH("score_pass2_mfma", (score_mfma_kernel<D, NQT, kPass2>), grid, dim3(kScoreThreads),
                 smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
                 a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (float2*)nullptr,
                 (const float*)a.lse2, (const int32_t*)nullptr, a.scores,
@@ -592,8 +607,7 @@ static certkv_status dispatch_nqt(const ScoreArgs& a, const SeqTab& st, int max_
     case 2: return launch_mfma<D, 2>(a, st, max_len, s);
     case 4: return launch_mfma<D, 4>(a, st, max_len, s);
     case 8: return launch_mfma<D, 8>(a, st, max_len, s);
-    case 16: return launch_mfma<D, 16>(a, st, max_len, s);
-    default: return launch_mfma<D, 32>(a, st, max_len, s);
+    default: return launch_mfma<D, 16>(a, st, max_len, s);
   }
 }
 

@@ -18,10 +18,10 @@ struct ScoreArgs {
   int32_t keys_per_block;
   int32_t nkb_max;
 };
-// Query tiles of 16 rows covering the M window rows, rounded up to a power of two.
+// Query tiles of 32 rows covering the M window rows, rounded up to a power of two.
 inline int score_nqt(int M) {
   int t = 1;
-  while (t * 16 < M) t *= 2;
+  while (t * 32 < M) t *= 2;
   return t;
 }
 certkv_status run_score(const ScoreArgs& a, const SeqTab& st, int max_len, hipStream_t s);
