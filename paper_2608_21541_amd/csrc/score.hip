@@ -12,11 +12,11 @@
 // [2^-60, 2^120] (where fp32 exponentials could under- or overflow) flags its
 // unit, and a fallback pass recomputes that unit's partials with a running
 // maximum; it returns immediately for units that are not flagged.
-// The contraction runs on MFMA v_mfma_f32_32x32x16_bf16 with key tiles as the
-// A operand (rows = 32 keys, held in VGPRs straight from HBM) and the window
-// queries as the B operand (columns = 32 queries, staged once per workgroup in
-// LDS).  Each lane owns one query column, so row sums are lane-local and
-// per-key sums are one transposed reduction per wave iteration.
+// The contraction runs on MFMA v_mfma_f32_32x32x16_bf16 with the key tile in
+// VGPRs straight from HBM and the window queries staged once per workgroup in
+// LDS.  Pass 1 makes the key tile the A operand, so each lane owns one query
+// column and row sums are lane-local; pass 2 makes it the B operand, so each
+// lane owns one key and per-key sums are lane-local.
 #include <type_traits>
 
 #include "stages.h"
@@ -43,7 +43,7 @@ struct ScoreSmem {
   static constexpr int kRowElems = D + 8;
 };
 
-enum { kPass1Sum = 0, kPass1Max = 1, kPass2 = 2 };
+enum { kPass1Sum = 0, kPass1Max = 1 };
 
 // One round of a transpose-reduce over lane bit M: lanes with that bit set
 // keep the upper HALF of their 2*HALF values, the others the lower HALF, and
@@ -71,16 +71,14 @@ __device__ __forceinline__ void xpose_round(float* v, int lane) {
 // hh*D/2 .. hh*D/2 + D/2 - 1 for all of its k-steps: a lane loads one D-byte
 // run of its key row, and k-step s takes its dims 8*s .. 8*s + 7.
 template <int D, int NQT, int MODE>
-__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((MODE == kPass2 || NQT > 8) ? 2 : 4, 8))) void score_mfma_kernel(
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(NQT > 8 ? 2 : 4, 8))) void score_mfma_kernel(
     Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
     int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
     int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, float2* __restrict__ part,
-    const float* __restrict__ lse2, const int32_t* __restrict__ flag,
-    float* __restrict__ scores, float* __restrict__ kpart) {
+    const int32_t* __restrict__ flag) {
   constexpr int KS = D / 16;   // MFMA k-steps
   constexpr int HD = D / 2;    // dims per lane half
   constexpr int RE = ScoreSmem<D>::kRowElems;
-  constexpr bool P2 = MODE == kPass2;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   uint16_t* q_lds = reinterpret_cast<uint16_t*>(smem_raw);
 
@@ -100,14 +98,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
   const int64_t u = unit_index(g, l, b, h);
   if (MODE == kPass1Max && flag[u] == 0) return;
 
-  float* lse_lds = reinterpret_cast<float*>(smem_raw + (size_t)Mp * RE * 2);
-  int* lim_lds = reinterpret_cast<int*>(lse_lds + Mp);
+  int* lim_lds = reinterpret_cast<int*>(smem_raw + (size_t)Mp * RE * 2 + (size_t)Mp * 4);
   // Cross-wave reduction area, aliasing the staged queries once the key loop
-  // is done: [8][Mp] sums, [8][Mp][2] (max, sum) pairs or [8][D] key sums.
+  // is done: [8][Mp] sums or [8][Mp][2] (max, sum) pairs.
   float* red_lds = reinterpret_cast<float*>(smem_raw);
 
   // Stage the window queries of this KV head: row rho = q*G + gq; padding
-  // rows are zero and are never written out (pass 2 gives them lse = +inf).
+  // rows are zero and are never written out.
   {
     const int chunks = D / 8;
     for (int c = threadIdx.x; c < Mp * chunks; c += kScoreThreads) {
@@ -127,7 +124,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       int lim = -1;
       if (i < M) lim = g.causal ? min(n - g.w + i / g.G, n - 1) : n - 1;
       lim_lds[i] = lim;
-      if (P2) lse_lds[i] = i < M ? lse2[u * M + i] : INFINITY;
     }
   }
   __syncthreads();
@@ -140,19 +136,15 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
   const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
   const uint16_t* kbase = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
 
-  float srun[NQT];  // pass 1: this lane's query column, per query tile
+  float srun[NQT];  // this lane's query column, per query tile
   float mrun[MODE == kPass1Max ? NQT : 1];
 #pragma unroll
   for (int i = 0; i < NQT; ++i) srun[i] = 0.f;
 #pragma unroll
   for (int i = 0; i < (MODE == kPass1Max ? NQT : 1); ++i) mrun[i] = -INFINITY;
-  float kacc[P2 ? HD : 1];  // pass 2: weighted key sum over this lane's dims
-#pragma unroll
-  for (int i = 0; i < (P2 ? HD : 1); ++i) kacc[i] = 0.f;
 
   constexpr int KPW = 32;             // keys per wave iteration
   constexpr int KPI = KPW * kScoreThreads / 64;  // keys per workgroup iteration
-  constexpr int NV = 16;              // per-lane values per query tile
   for (int it = key_begin + wave * KPW; it < key_end; it += KPI) {
     // The 32-key tile (keys it..it+31) as A fragments, straight from HBM.
     Frag kf[KS];
@@ -164,9 +156,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       for (int s = 0; s < KS; ++s) kf[s].u = src[s];
     }
     const bool need_mask = (it + KPW - 1 >= first_masked) || (it + KPW - 1 >= n);
-    float ssum[P2 ? NV : 1];
-#pragma unroll
-    for (int i = 0; i < (P2 ? NV : 1); ++i) ssum[i] = 0.f;
 
     // The query-tile loop is software-pipelined: the MFMA chain of tile qt+1
     // is interleaved with the masking and exponentials of tile qt (a slice
@@ -228,7 +217,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
             mrun[qt] = mnew;
           }
         } else {
-          const float l2 = P2 ? lse_lds[qt * 32 + c32] : 0.f;
           float sacc = 0.f;
 #pragma unroll
           for (int s = 0; s < KS; ++s) {
@@ -240,18 +228,14 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
 #pragma unroll
             for (int j = 0; j < SL; ++j) {
               const int v = s * SL + j;
-              const float x = logit(acc, v, lim);
-              if (P2)
-                ssum[v] += __builtin_amdgcn_exp2f(fmaf(x, c2, -l2));
-              else
-                sacc += __builtin_amdgcn_exp2f(x * c2);
+              sacc += __builtin_amdgcn_exp2f(logit(acc, v, lim) * c2);
             }
           }
-          if (!P2) srun[qt] += sacc;
+          srun[qt] += sacc;
           if (more) {
             // LDS reads two k-steps ahead of their MFMA, each k-step's VALU
             // slice right behind its MFMA.
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 + (MASKED ? 1 : 0) + (P2 ? 1 : 0), 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 + (MASKED ? 1 : 0), 0);
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
               __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -268,41 +252,6 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       tiles(std::integral_constant<bool, true>());
     else
       tiles(std::integral_constant<bool, false>());
-
-    if (P2) {
-      // Sum each key's per-lane partials over the 32 query columns of its
-      // lane half.  Value v of lane (hh, c32) belongs to key
-      // 8*(v/4) + 4*hh + v%4; a transpose-reduce over lane bits 16, 8, 4, 2
-      // leaves value v = c32 / 2 in lanes c32 = 2*v + j, and the last xor
-      // step adds the two copies.
-      float v[NV];
-#pragma unroll
-      for (int i = 0; i < NV; ++i) v[i] = ssum[i];
-      xpose_round<NV / 2, 16>(v, lane);
-      constexpr int SPREAD = 32 / NV;  // lanes sharing one value index
-#pragma unroll
-      for (int m = SPREAD / 2; m >= 1; m >>= 1) v[0] += __shfl_xor(v[0], m, 64);
-      const float s_mine = v[0];
-      const int vi = c32 / SPREAD;
-      const int key_mine = it + 8 * (vi >> 2) + 4 * hh + (vi & 3);
-      if ((c32 % SPREAD) == 0 && key_mine < n) scores[lht_base(g, l, h, tok0) + key_mine] = s_mine;
-      if (kpart) {
-        // Lane (hh, c32) holds key c32 over dims hh*HD..; its score is
-        // value 4*(c32/8) + c32%4 of lane half (c32/4)%2.
-        const int src = 32 * ((c32 >> 2) & 1) + SPREAD * (4 * (c32 >> 3) + (c32 & 3));
-        float s_t = __shfl(s_mine, src, 64);
-        s_t = (it + c32 < n && s_t > 0.f) ? s_t : 0.f;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const uint32_t* w4 = reinterpret_cast<const uint32_t*>(&kf[s].u);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            kacc[s * 8 + 2 * e] = fmaf(s_t, bf16_lo(w4[e]), kacc[s * 8 + 2 * e]);
-            kacc[s * 8 + 2 * e + 1] = fmaf(s_t, bf16_hi(w4[e]), kacc[s * 8 + 2 * e + 1]);
-          }
-        }
-      }
-    }
   }
 
   constexpr int NW = kScoreThreads / 64;
@@ -349,14 +298,214 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
       }
       part[(u * nkb_max + kb) * M + rho] = make_float2(mt, sacc);
     }
-  } else if (kpart) {
-    // Reduce the weighted key sums over the 32 lanes of each half, then over
-    // the waves.
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2 with the operands swapped: the window queries are the A operand
+// (rows = 32 queries of a tile, from LDS) and the key tile the B operand
+// (columns = 32 keys, in VGPRs straight from HBM).  Lane (hh, c) then holds
+// key c of the tile and the query rows 8*(v/4) + 4*hh + v%4 (v = 0..15) of
+// every query tile, so a key's score is a lane-local sum over its rows plus
+// one exchange between the two lane halves, and its weighted key row is
+// already in the lane's registers.  The next key tile is loaded while the
+// current one is consumed.
+template <int D, int NQT>
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void score_pass2_kernel(
+    Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
+    int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
+    int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, const float* __restrict__ lse2,
+    float* __restrict__ scores, float* __restrict__ kpart) {
+  constexpr int KS = D / 16;   // MFMA k-steps
+  constexpr int HD = D / 2;    // dims per lane half
+  constexpr int RE = ScoreSmem<D>::kRowElems;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  uint16_t* q_lds = reinterpret_cast<uint16_t*>(smem_raw);
+
+  const int kb = blockIdx.x;
+  const int h = blockIdx.y % g.H;
+  const int bl = blockIdx.y / g.H;
+  const int l = blockIdx.z;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int n = st.len[bl];
+  const int64_t tok0 = st.start[bl];
+  const int key_begin = kb * keys_per_block;
+  if (key_begin >= n) return;
+  const int key_end = min(n, key_begin + keys_per_block);
+  const int M = g.w * g.G;
+  const int Mp = NQT * 32;
+  const int64_t u = unit_index(g, l, b, h);
+
+  float* lse_lds = reinterpret_cast<float*>(smem_raw + (size_t)Mp * RE * 2);
+  int* lim_lds = reinterpret_cast<int*>(lse_lds + Mp);
+  float* red_lds = reinterpret_cast<float*>(smem_raw);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int hh = lane >> 5;
+  const int c32 = lane & 31;
+  const uint16_t* kbase = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
+  constexpr int KPW = 32;                        // keys per wave iteration
+  constexpr int KPI = KPW * kScoreThreads / 64;  // keys per workgroup iteration
+  // Key tile starting at `it` (rows clamped into the sequence) into kf.
+  auto load_tile = [&](int it, Frag(&kf)[KS]) {
+    const int key = it + c32;
+    const int keyc = key < n ? key : n - 1;
+    const uint4* src = reinterpret_cast<const uint4*>(kbase + (int64_t)keyc * k_st + hh * HD);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) kf[s].u = src[s];
+  };
+  Frag kf[KS], kn[KS];
+  const int it0 = key_begin + wave * KPW;
+  if (it0 < key_end) load_tile(it0, kf);
+
+  // Stage the window queries (row rho = q*G + gq, zero padding rows), the
+  // row log2-sums (+inf for padding rows, whose weights are then zero) and
+  // the causal limits.
+  {
+    const int chunks = D / 8;
+    for (int c = threadIdx.x; c < Mp * chunks; c += kScoreThreads) {
+      int rho = c / chunks, part8 = c % chunks;
+      uint4 val = make_uint4(0u, 0u, 0u, 0u);
+      if (rho < M) {
+        int qq = rho / g.G, gq = rho % g.G;
+        const uint16_t* src = qw + (int64_t)l * q_sl + (int64_t)(b * g.w + qq) * q_st +
+                              (int64_t)(h * g.G + gq) * q_sh + part8 * 8;
+        val = *reinterpret_cast<const uint4*>(src);
+      }
+      *reinterpret_cast<uint4*>(q_lds + rho * RE + part8 * 8) = val;
+    }
+    for (int i = threadIdx.x; i < Mp; i += kScoreThreads) {
+      int lim = -1;
+      if (i < M) lim = g.causal ? min(n - g.w + i / g.G, n - 1) : n - 1;
+      lim_lds[i] = lim;
+      lse_lds[i] = i < M ? lse2[u * M + i] : INFINITY;
+    }
+  }
+  __syncthreads();
+
+  const float c2 = g.scale * kLog2e;
+  const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
+  float kacc[HD];
+#pragma unroll
+  for (int i = 0; i < HD; ++i) kacc[i] = 0.f;
+
+  for (int it = it0; it < key_end; it += KPI) {
+    if (it + KPI < key_end) load_tile(it + KPI, kn);
+    const bool need_mask = it + KPW - 1 >= first_masked;
+    float sp[16 / KS];  // this lane's key: sums over its rows (independent chains)
+#pragma unroll
+    for (int j = 0; j < 16 / KS; ++j) sp[j] = 0.f;
+
+    // Query tiles software-pipelined as in pass 1: the MFMA chain of tile
+    // qt+1 interleaved with the exponentials of tile qt.
+    auto tiles = [&](auto masked_tag) {
+      constexpr bool MASKED = decltype(masked_tag)::value;
+      constexpr int SL = 16 / KS;  // values of the current tile per k-step
+      const int key = it + c32;
+      f32x16_t acc;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+      {
+        const uint16_t* qrow = q_lds + c32 * RE + hh * HD;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          Frag qf;
+          qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.v, kf[s].v, acc, 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        const bool more = qt + 1 < NQT;
+        // rows of value v: qt*32 + 4*hh + 8*(v/4) + v%4, four runs of four
+        const int rb = qt * 32 + 4 * hh;
+        float4 l2[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) l2[i] = *reinterpret_cast<const float4*>(lse_lds + rb + 8 * i);
+        int4 lim[4];
+        if (MASKED) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) lim[i] = *reinterpret_cast<const int4*>(lim_lds + rb + 8 * i);
+        }
+        f32x16_t nacc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) nacc[v] = 0.f;
+        const uint16_t* qrow = q_lds + ((qt + 1) * 32 + c32) * RE + hh * HD;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          if (more) {
+            Frag qf;
+            qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+            nacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.v, kf[s].v, nacc, 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < SL; ++j) {
+            const int v = s * SL + j;
+            const float4 lv = l2[v >> 2];
+            const float lsev = (v & 3) == 0 ? lv.x : (v & 3) == 1 ? lv.y : (v & 3) == 2 ? lv.z : lv.w;
+            float x = acc[v];
+            if (MASKED) {
+              const int4 mv = lim[v >> 2];
+              const int limv = (v & 3) == 0 ? mv.x : (v & 3) == 1 ? mv.y : (v & 3) == 2 ? mv.z : mv.w;
+              if (key > limv) x = -INFINITY;
+            }
+            sp[j] += __builtin_amdgcn_exp2f(fmaf(x, c2, -lsev));
+          }
+        }
+        if (more) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 + 4 + (MASKED ? 4 : 0), 0);
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x402, (MASKED ? 5 : 3) * SL, 0);
+            if (s + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+        }
+        acc = nacc;
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    if (need_mask)
+      tiles(std::integral_constant<bool, true>());
+    else
+      tiles(std::integral_constant<bool, false>());
+
+    float sp_all = sp[0];
+#pragma unroll
+    for (int j = 1; j < 16 / KS; ++j) sp_all += sp[j];
+    const float s_key = sp_all + __shfl_xor(sp_all, 32, 64);
+    const int key = it + c32;
+    if (hh == 0 && key < n) scores[lht_base(g, l, h, tok0) + key] = s_key;
+    if (kpart) {
+      const float s_t = (key < n && s_key > 0.f) ? s_key : 0.f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const uint32_t* w4 = reinterpret_cast<const uint32_t*>(&kf[s].u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          kacc[s * 8 + 2 * e] = fmaf(s_t, bf16_lo(w4[e]), kacc[s * 8 + 2 * e]);
+          kacc[s * 8 + 2 * e + 1] = fmaf(s_t, bf16_hi(w4[e]), kacc[s * 8 + 2 * e + 1]);
+        }
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s) kf[s].u = kn[s].u;
+  }
+
+  if (kpart) {
+    constexpr int NW = kScoreThreads / 64;
+    __syncthreads();  // every wave is done with the staged queries
+    // Sum the weighted key rows over the 32 keys of each lane half (a
+    // transpose-reduce leaves dims hh*HD + c32*PER + e in lane (hh, c32)),
+    // then over the waves.
     float v[HD];
 #pragma unroll
     for (int i = 0; i < HD; ++i) v[i] = kacc[i];
     xpose_round<HD / 2, 16>(v, lane);
-    constexpr int PER = HD / 32;  // dims left per lane
+    constexpr int PER = HD / 32;
 #pragma unroll
     for (int e = 0; e < PER; ++e) red_lds[wave * D + hh * HD + c32 * PER + e] = v[e];
     __syncthreads();
@@ -547,7 +696,7 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass1Max>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass2>,
+    hipFuncSetAttribute((const void*)score_pass2_kernel<D, NQT>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
@@ -556,20 +705,19 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
   CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kPass1Sum>), grid,
                 dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
                 a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
-                (const float*)nullptr, (const int32_t*)nullptr, (float*)nullptr, (float*)nullptr);
+                (const int32_t*)nullptr);
   CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
                 s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
   // fallback for flagged units (returns at once for the others)
   CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kPass1Max>), grid,
                 dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
                 a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
-                (const float*)nullptr, (const int32_t*)a.flag, (float*)nullptr, (float*)nullptr);
+                (const int32_t*)a.flag);
   CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
                 0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 1);
-  CERTKV_LAUNCH("score_pass2_mfma", (score_mfma_kernel<D, NQT, kPass2>), grid, dim3(kScoreThreads),
-                smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
-                a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (float2*)nullptr,
-                (const float*)a.lse2, (const int32_t*)nullptr, a.scores,
+  CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT>), grid, dim3(kScoreThreads), smem,
+                s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token,
+                a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2, a.scores,
                 a.ksum ? a.kpart : (float*)nullptr);
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
