@@ -56,6 +56,19 @@ __device__ __forceinline__ uint2 buf_load_u64(BufRsrc r, uint32_t off) {
   auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
   return make_uint2(v[0], v[1]);
 }
+// The same loads with a wave-uniform byte offset `soff` (held in the
+// instruction's scalar offset; only `off` is range-checked, so the caller
+// keeps soff + off inside the buffer).
+__device__ __forceinline__ uint32_t buf_load_u32s(BufRsrc r, uint32_t off, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, (int)soff, 0);
+}
+__device__ __forceinline__ uint32_t buf_load_u16s(BufRsrc r, uint32_t off, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, (int)soff, 0);
+}
+__device__ __forceinline__ uint2 buf_load_u64s(BufRsrc r, uint32_t off, uint32_t soff) {
+  auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, (int)soff, 0);
+  return make_uint2(v[0], v[1]);
+}
 
 // bf16 <-> fp32.  bf16 is the upper half of an IEEE binary32.
 __device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }

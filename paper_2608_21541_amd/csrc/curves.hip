@@ -12,7 +12,8 @@
 //            0..w-1 (higher ranks), added in that fixed order (deterministic);
 //   phase 2  the wave walks its ranks top-down extending m, W and the
 //            lane-local part q of Q; per rank each lane forms
-//            x = m q - |W|^2 over its dims (lane 0 adds m * Q_carry) and a
+//            x = m q - |W|^2 over its dims (lane 0's q starts from Q_carry,
+//            the part of Q above the wave) and a
 //            transpose-reduce over the 64 lanes, folded in as the ranks are
 //            produced, yields c^2 of all 32 ranks.  The last wave's final
 //            state is the carry of the next chunk.
@@ -43,14 +44,6 @@ __device__ __forceinline__ void unpack_dims(uint32_t raw0, uint32_t raw1, float 
     v[0] = __uint_as_float(raw0);
     if (DP == 2) v[DP - 1] = __uint_as_float(raw1);
   }
-}
-
-// Lane r's value of x, as a wave-uniform (scalar) value.
-__device__ __forceinline__ double lane_f64(double x, int r) {
-  const uint64_t u = (uint64_t)__double_as_longlong(x);
-  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, r);
-  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), r);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
 // One transpose-reduce step over lane bit 5 (half = true) or 4: lanes with
@@ -144,16 +137,18 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   auto fetch_rows = [&](int pos, uint32_t (&raw)[kRPW][RAW]) {
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
-      const int pr = __builtin_amdgcn_readlane(pos, r);  // uniform: one SGPR
-      const uint32_t off = (uint32_t)pr * vrow_bytes + vlane;
+      // the row offset is uniform (scalar offset of the load); rows are
+      // clamped into the sequence, so soff + vlane stays inside the slice
+      const int pr = __builtin_amdgcn_readlane(pos, r);
+      const uint32_t soff = (uint32_t)pr * vrow_bytes;
       if (RAW == 2) {
-        const uint2 w2 = buf_load_u64(vrs, off);
+        const uint2 w2 = buf_load_u64s(vrs, vlane, soff);
         raw[r][0] = w2.x;
         raw[r][RAW - 1] = w2.y;
       } else if (BF16 && DP == 1) {
-        raw[r][0] = buf_load_u16(vrs, off);
+        raw[r][0] = buf_load_u16s(vrs, vlane, soff);
       } else {
-        raw[r][0] = buf_load_u32(vrs, off);
+        raw[r][0] = buf_load_u32s(vrs, vlane, soff);
       }
     }
   };
@@ -180,6 +175,14 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     fetch_meta(k - 2, k_n2, p_n2, ok_n2);
     fetch_rows(p_n1, vnext);
 
+    // weight of lane r's rank, as a wave-uniform (scalar) value
+    auto a_at = [&](int r) -> double {
+      const uint64_t u = (uint64_t)__double_as_longlong(a_cur);
+      const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, r);
+      const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), r);
+      return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+    };
+
     // phase 1: totals of the wave's rows
     {
       double sW[DP], sQ = 0.0, sM = 0.0;
@@ -187,7 +190,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       for (int t = 0; t < DP; ++t) sW[t] = 0.0;
 #pragma unroll
       for (int r = 0; r < kRPW; ++r) {
-        const double ar = lane_f64(a_cur, r);
+        const double ar = a_at(r);
         float v[DP];
         unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
         double vv = 0.0;
@@ -232,12 +235,14 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     // lane bit 5 as soon as both exist, pairs of those over bit 4, and so on,
     // so at most one pending value per level is live.  Lane bit 5 - j ends up
     // naming rank bit j.
-    double q = 0.0;
+    // lane 0 carries the chunk's Q above the wave, so that every lane forms
+    // m * q - |W|^2 over its dims and their sum is m Q - |W|^2
+    double q = lane == 0 ? Qc : 0.0;
     double pend[kLev];
     double c2 = 0.0;
 #pragma unroll
     for (int r = 0; r < kRPW; ++r) {
-      const double ar = lane_f64(a_cur, r);
+      const double ar = a_at(r);
       float v[DP];
       unpack_dims<DP, BF16>(vcur[r][0], vcur[r][RAW - 1], v);
       double vv = 0.0, w2 = 0.0;
@@ -251,7 +256,6 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       m += ar;
       q = fma(ar, vv, q);
       double cur = fma(m, q, -w2);
-      if (lane == 0) cur = fma(m, Qc, cur);
       bool placed = false;
 #pragma unroll
       for (int lev = 0; lev < kLev; ++lev) {
