@@ -308,10 +308,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(N
 // key c of the tile and the query rows 8*(v/4) + 4*hh + v%4 (v = 0..15) of
 // every query tile, so a key's score is a lane-local sum over its rows plus
 // one exchange between the two lane halves, and its weighted key row is
-// already in the lane's registers.  The next key tile is loaded while the
-// current one is consumed.
-template <int D, int NQT>
-__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void score_pass2_kernel(
+// already in the lane's registers.  With the key sums (64 accumulators per
+// lane) the kernel runs two waves per SIMD and loads the next key tile while
+// the current one is consumed; without them (and for windows of at most 256
+// rows) it keeps four waves per SIMD and lets the other waves hide the load
+// latency.
+template <int D, int NQT, bool KSUM>
+__global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((KSUM || NQT > 8) ? 2 : 4, 8))) void score_pass2_kernel(
     Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
     int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
     int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, const float* __restrict__ lse2,
@@ -356,7 +359,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
     for (int s = 0; s < KS; ++s) kf[s].u = src[s];
   };
-  Frag kf[KS], kn[KS];
+  Frag kf[KS], kn[KSUM ? KS : 1];
   const int it0 = key_begin + wave * KPW;
   if (it0 < key_end) load_tile(it0, kf);
 
@@ -387,12 +390,16 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
 
   const float c2 = g.scale * kLog2e;
   const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
-  float kacc[HD];
+  float kacc[KSUM ? HD : 1];
 #pragma unroll
-  for (int i = 0; i < HD; ++i) kacc[i] = 0.f;
+  for (int i = 0; i < (KSUM ? HD : 1); ++i) kacc[i] = 0.f;
 
   for (int it = it0; it < key_end; it += KPI) {
-    if (it + KPI < key_end) load_tile(it + KPI, kn);
+    if constexpr (KSUM) {
+      if (it + KPI < key_end) load_tile(it + KPI, kn);
+    } else {
+      if (it != it0) load_tile(it, kf);
+    }
     const bool need_mask = it + KPW - 1 >= first_masked;
     float sp[16 / KS];  // this lane's key: sums over its rows (independent chains)
 #pragma unroll
@@ -479,7 +486,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
     const float s_key = sp_all + __shfl_xor(sp_all, 32, 64);
     const int key = it + c32;
     if (hh == 0 && key < n) scores[lht_base(g, l, h, tok0) + key] = s_key;
-    if (kpart) {
+    if constexpr (KSUM) {
       const float s_t = (key < n && s_key > 0.f) ? s_key : 0.f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
@@ -491,11 +498,13 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(2
         }
       }
     }
+    if constexpr (KSUM) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) kf[s].u = kn[s].u;
+      for (int s = 0; s < KS; ++s) kf[s].u = kn[s].u;
+    }
   }
 
-  if (kpart) {
+  if constexpr (KSUM) {
     constexpr int NW = kScoreThreads / 64;
     __syncthreads();  // every wave is done with the staged queries
     // Sum the weighted key rows over the 32 keys of each lane half (a
@@ -696,7 +705,9 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     hipFuncSetAttribute((const void*)score_mfma_kernel<D, NQT, kPass1Max>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    hipFuncSetAttribute((const void*)score_pass2_kernel<D, NQT>,
+    hipFuncSetAttribute((const void*)score_pass2_kernel<D, NQT, true>,
+                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    hipFuncSetAttribute((const void*)score_pass2_kernel<D, NQT, false>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
@@ -715,10 +726,16 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                 (const int32_t*)a.flag);
   CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
                 0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 1);
-  CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT>), grid, dim3(kScoreThreads), smem,
-                s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token,
-                a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2, a.scores,
-                a.ksum ? a.kpart : (float*)nullptr);
+  if (a.ksum)
+    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid, dim3(kScoreThreads),
+                  smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
+                  a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2,
+                  a.scores, a.kpart);
+  else
+    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, false>), grid, dim3(kScoreThreads),
+                  smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
+                  a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2,
+                  a.scores, (float*)nullptr);
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
                   s, g, st, a.keys_per_block, a.nkb_max, (const float*)a.kpart, a.ksum);

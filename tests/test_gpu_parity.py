@@ -106,6 +106,10 @@ def test_stage_entry_points_match_fused():
     spec, out, (q, k, v), _ = run_gpu(cfg, cache)
     s, ksum = ck.score(spec, q, k, with_ksum=True)
     assert torch.equal(s.cpu(), out["scores"])
+    # the scoring variant without key sums (four waves per SIMD, no prefetch)
+    # accumulates every key's score in the same order: identical bits
+    s_nk = ck.score(spec, q, k, with_ksum=False)
+    assert torch.equal(s_nk.cpu(), out["scores"])
     al = ck.allocate(spec, s, v, cache["n_keep"], with_perm=True, with_curves=True, with_vsum=True)
     assert torch.equal(al["budgets"].cpu(), out["budgets"])
     assert torch.equal(al["perm"].cpu(), out["perm"])
