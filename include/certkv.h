@@ -60,6 +60,9 @@ enum {
   CERTKV_EUNSUPPORTED = -2, /* head_dim not 64/128, dtype not built, or a  */
                             /* per-head slice spanning 4 GiB or more      */
   CERTKV_EINFEASIBLE = -3,  /* n_keep < 2 or n_keep > n_b (budget algebra) */
+  CERTKV_ENONFINITE = -4,   /* written to *dev_status by a kernel that met */
+                            /* a non-finite input (never returned by a    */
+                            /* call: the launches are asynchronous)        */
   CERTKV_EWORKSPACE = -5,   /* workspace smaller than required             */
   CERTKV_EHIP = -6          /* a HIP runtime call or launch failed         */
 };
@@ -111,6 +114,16 @@ typedef struct certkv_problem {
   int32_t kv_dtype;              /* CERTKV_F32 or CERTKV_BF16; equal to q_dtype */
   float softmax_scale;           /* logit scale; 0 selects 1/sqrt(d)          */
   uint32_t flags;                /* CERTKV_CAUSAL | CERTKV_DRY_RUN            */
+  int32_t* dev_status;           /* optional device int32: kernels that meet a
+                                    non-finite value (a window row whose
+                                    log-sum-exp is not finite, a caller log-sum
+                                    that is not finite, or a non-finite
+                                    dispersion value) store CERTKV_ENONFINITE
+                                    there; nothing else writes it, so the
+                                    caller sets it to CERTKV_OK beforehand and
+                                    reads it after synchronising.  NULL: no
+                                    reporting.  Outputs computed from
+                                    non-finite inputs are unspecified. */
 } certkv_problem;
 
 /* Outputs of the fused pass.  Layouts:
@@ -132,6 +145,11 @@ typedef struct certkv_problem {
  *   alloc_stats   optional [L*B][3] int64 diagnostics of the allocation per
  *                 (layer, sequence): one-token repairs performed, and the
  *                 bisection and repair durations in 100 MHz clock ticks
+ *   kept_mask     optional [L][H][T] uint8, 1 at the kept positions of each
+ *                 unit and 0 elsewhere
+ *   lse           optional [L][B*w][Hq] fp32, the natural-log log-sum-exp of
+ *                 every window row over its visible keys (the caller's lse_in
+ *                 when one was given)
  * Every (layer, sequence) block of the packed cache holds exactly
  * H * n_keep_b rows (the matched live-slot budget). */
 typedef struct certkv_outputs {
@@ -149,6 +167,8 @@ typedef struct certkv_outputs {
   float* curves;
   int32_t* perm;
   int64_t* alloc_stats;
+  uint8_t* kept_mask;
+  float* lse;
 } certkv_outputs;
 
 /* Human-readable name of a status code (static storage). */
@@ -163,15 +183,23 @@ size_t certkv_workspace_size(const certkv_problem* p, int32_t stage);
  * setup for the 1/sqrt(d) logit scale).
  *   q_win  [L][B*w][Hq][d]: row b*w+q holds window query q of sequence b
  *   k      [L][T][H][d]
+ *   lse_in optional [L][B*w][Hq] fp32: the natural-log log-sum-exp of each
+ *          window row's logits scale * q . k_j over its visible keys, as an
+ *          attention prefill already computes it.  When given, the pass that
+ *          forms the row sums is skipped and K is read once; a non-finite
+ *          entry is reported through dev_status.  NULL: computed here.
  *   scores [L][H][T] fp32 out: s_j = sum_{g in group(h)} sum_q softmax_j(
  *          scale * q_{g,q} . k_j) over the keys visible to row q
  *   ksum   optional [L*B*H][d] fp64 out: sum_j (s_j)_+ k_j (used by the tail
  *          summary to avoid re-reading evicted keys); NULL to skip.
+ *   lse_out optional [L][B*w][Hq] fp32 out: the row log-sum-exp used (natural
+ *          log), in lse_in's layout.
  * Softmax rows are normalized in fp32 from bf16 (or fp32) inputs with fp32
  * MFMA accumulation. */
 certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win,
-                           certkv_tensor k, float* scores, double* ksum,
-                           void* ws, size_t ws_bytes, void* stream);
+                           certkv_tensor k, const float* lse_in, float* scores,
+                           double* ksum, float* lse_out, void* ws,
+                           size_t ws_bytes, void* stream);
 
 /* Dispersion curves and budget allocation (paper Section 4.1, Eq.
  * certkv-curve; appendix Algorithm 1, the sort, suffix-scan, bisection and
@@ -216,6 +244,7 @@ certkv_status certkv_allocate_curves(const certkv_problem* p,
  *   kept_offsets [L*B*H+1] int64 out
  *   kept_idx     int32 out, capacity kept_capacity entries; needs
  *                sum(budgets) entries, L*H*T in coverage mode
+ *   kept_mask    optional [L][H][T] uint8 out: 1 at kept positions, else 0
  * Kept = the first b ranks of the order (s descending, ties by position);
  * positions are written ascending.  Coverage: k_eta = min{k >= 1 :
  * sum_{r<=k} a_(r) >= retain_mass}, the prefix summed in rank order in fp64,
@@ -223,8 +252,9 @@ certkv_status certkv_allocate_curves(const certkv_problem* p,
 certkv_status certkv_select(const certkv_problem* p, const float* scores,
                             int32_t* budgets_io, int32_t mode,
                             double retain_mass, int64_t* kept_offsets,
-                            int32_t* kept_idx, int64_t kept_capacity, void* ws,
-                            size_t ws_bytes, void* stream);
+                            int32_t* kept_idx, int64_t kept_capacity,
+                            uint8_t* kept_mask, void* ws, size_t ws_bytes,
+                            void* stream);
 
 /* Tail-summary slot (Section 4.1: the synthetic pair is the key and value
  * centroid of the evicted suffix under r = a/m; Theorem "fixed-row tail
@@ -257,12 +287,14 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k,
                              int64_t* packed_offsets, void* stream);
 
 /* The whole pass in order (score, allocate, select, tail summary, compact)
- * with one workspace of certkv_workspace_size(p, CERTKV_STAGE_COMPRESS). */
+ * with one workspace of certkv_workspace_size(p, CERTKV_STAGE_COMPRESS).
+ * lse_in is optional, as for certkv_score. */
 certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
                               certkv_tensor k, certkv_tensor v,
-                              const int32_t* n_keep_host, double alpha,
-                              int32_t steps, const certkv_outputs* out,
-                              void* ws, size_t ws_bytes, void* stream);
+                              const float* lse_in, const int32_t* n_keep_host,
+                              double alpha, int32_t steps,
+                              const certkv_outputs* out, void* ws,
+                              size_t ws_bytes, void* stream);
 
 /* Per-kernel timing.  While enabled, every kernel the library launches is
  * bracketed by two hipEvents on its launch stream; certkv_profile_read

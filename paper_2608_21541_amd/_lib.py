@@ -14,6 +14,7 @@ CERTKV_OK = 0
 CERTKV_EINVAL = -1
 CERTKV_EUNSUPPORTED = -2
 CERTKV_EINFEASIBLE = -3
+CERTKV_ENONFINITE = -4
 CERTKV_EWORKSPACE = -5
 CERTKV_EHIP = -6
 
@@ -51,6 +52,7 @@ class Problem(ctypes.Structure):
         ("kv_dtype", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float),
         ("flags", ctypes.c_uint32),
+        ("dev_status", ctypes.c_void_p),
     ]
 
 
@@ -66,7 +68,8 @@ class Tensor(ctypes.Structure):
 class Outputs(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "scores", "budgets", "kept_offsets", "kept_idx", "k_star", "v_star", "tail_mass",
-        "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm", "alloc_stats")]
+        "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm", "alloc_stats",
+        "kept_mask", "lse")]
 
 
 class CertKVError(RuntimeError):
@@ -95,14 +98,14 @@ def lib():
     L.certkv_status_string.restype = ctypes.c_char_p
     L.certkv_workspace_size.argtypes = [P, i32]
     L.certkv_workspace_size.restype = sz
-    L.certkv_score.argtypes = [P, Tensor, Tensor, vp, vp, vp, sz, vp]
+    L.certkv_score.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_allocate.argtypes = [P, vp, Tensor, vp, dbl, i32, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_allocate_curves.argtypes = [P, vp, vp, dbl, i32, vp, vp, sz, vp]
-    L.certkv_select.argtypes = [P, vp, vp, i32, dbl, vp, vp, i64, vp, sz, vp]
+    L.certkv_select.argtypes = [P, vp, vp, i32, dbl, vp, vp, i64, vp, vp, sz, vp]
     L.certkv_tail_summary.argtypes = [P, vp, Tensor, Tensor, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_compact.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp, vp, vp, vp, vp]
-    L.certkv_compress.argtypes = [P, Tensor, Tensor, Tensor, vp, dbl, i32, ctypes.POINTER(Outputs),
-                                  vp, sz, vp]
+    L.certkv_compress.argtypes = [P, Tensor, Tensor, Tensor, vp, vp, dbl, i32,
+                                  ctypes.POINTER(Outputs), vp, sz, vp]
     L.certkv_profile_enable.argtypes = [i32]
     L.certkv_profile_read.argtypes = [vp, vp, vp, i32]
     L.certkv_profile_read.restype = i32

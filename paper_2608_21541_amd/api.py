@@ -28,6 +28,7 @@ class ProblemSpec:
     softmax_scale: float = 0.0
     causal: bool = True
     dry_run: bool = False
+    status: Optional[torch.Tensor] = None  # device int32 [1]: CERTKV_ENONFINITE on non-finite input
     _cu: object = field(default=None, repr=False)
 
     @property
@@ -54,9 +55,10 @@ class ProblemSpec:
         dt = _dtype_code(self.dtype)
         flags = (_lib.CERTKV_CAUSAL if self.causal else 0) | (
             _lib.CERTKV_DRY_RUN if self.dry_run else 0)
+        st = self.status.data_ptr() if self.status is not None else None
         return _lib.Problem(self.layers, self.batch, self.kv_heads, self.group, self.head_dim,
                             self.window, ctypes.cast(self._cu, ctypes.POINTER(ctypes.c_int64)),
-                            dt, dt, float(self.softmax_scale), flags)
+                            dt, dt, float(self.softmax_scale), flags, st)
 
 
 def _dtype_code(dt):
@@ -100,19 +102,30 @@ def _workspace(spec, stage, device):
     return ws, n
 
 
-def score(spec: ProblemSpec, q_win, k, with_ksum=False):
-    """Window-mass scores [L][H][T] fp32 (and sum_j (s_j)_+ k_j [U][d] fp64)."""
+def _lse_shape(spec):
+    return (spec.layers, spec.batch * spec.window, spec.kv_heads * spec.group)
+
+
+def score(spec: ProblemSpec, q_win, k, with_ksum=False, lse_in=None, with_lse=False):
+    """Window-mass scores [L][H][T] fp32; with_ksum adds sum_j (s_j)_+ k_j [U][d] fp64 and
+    with_lse the row log-sum-exp [L][B*w][Hq] fp32 (in that order).  lse_in: the caller's
+    row log-sum-exp in the same layout (the row-sum pass is then skipped)."""
     L = _lib.lib()
     dev = k.device
     scores = torch.empty((spec.layers, spec.kv_heads, spec.total_tokens), dtype=torch.float32,
                          device=dev)
     ksum = torch.empty((spec.units, spec.head_dim), dtype=torch.float64, device=dev) \
         if with_ksum else None
+    lse = torch.empty(_lse_shape(spec), dtype=torch.float32, device=dev) if with_lse else None
+    if lse_in is not None:
+        assert lse_in.dtype == torch.float32 and lse_in.is_contiguous()
+        assert tuple(lse_in.shape) == _lse_shape(spec)
     ws, n = _workspace(spec, _lib.STAGE_SCORE, dev)
     p = spec.c_problem()
-    _check(L.certkv_score(ctypes.byref(p), _tensor(q_win), _tensor(k), _ptr(scores), _ptr(ksum),
-                          _ptr(ws), n, _stream(dev)), "certkv_score")
-    return (scores, ksum) if with_ksum else scores
+    _check(L.certkv_score(ctypes.byref(p), _tensor(q_win), _tensor(k), _ptr(lse_in), _ptr(scores),
+                          _ptr(ksum), _ptr(lse), _ptr(ws), n, _stream(dev)), "certkv_score")
+    out = [scores] + ([ksum] if with_ksum else []) + ([lse] if with_lse else [])
+    return out[0] if len(out) == 1 else tuple(out)
 
 
 def allocate(spec: ProblemSpec, scores, v, n_keep, alpha=0.2, steps=40, with_perm=False,
@@ -157,8 +170,9 @@ def allocate_curves(spec: ProblemSpec, curves, n_keep, alpha=0.2, steps=40):
     return budgets
 
 
-def select(spec: ProblemSpec, scores, budgets=None, mode="budget", retain_mass=0.9):
-    """(budgets, kept_offsets [U+1] int64, kept_idx int32)."""
+def select(spec: ProblemSpec, scores, budgets=None, mode="budget", retain_mass=0.9,
+           with_mask=False):
+    """(budgets, kept_offsets [U+1] int64, kept_idx int32[, kept_mask [L][H][T] uint8])."""
     L = _lib.lib()
     dev = scores.device
     if mode == "budget":
@@ -172,12 +186,14 @@ def select(spec: ProblemSpec, scores, budgets=None, mode="budget", retain_mass=0
         m = _lib.CERTKV_SELECT_COVERAGE
     kept_offsets = torch.empty(spec.units + 1, dtype=torch.int64, device=dev)
     kept_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    mask = torch.empty((spec.layers, spec.kv_heads, spec.total_tokens), dtype=torch.uint8,
+                       device=dev) if with_mask else None
     ws, n = _workspace(spec, _lib.STAGE_SELECT, dev)
     p = spec.c_problem()
     _check(L.certkv_select(ctypes.byref(p), _ptr(scores), _ptr(b), m, float(retain_mass),
-                           _ptr(kept_offsets), _ptr(kept_idx), cap, _ptr(ws), n, _stream(dev)),
-           "certkv_select")
-    return b, kept_offsets, kept_idx
+                           _ptr(kept_offsets), _ptr(kept_idx), cap, _ptr(mask), _ptr(ws), n,
+                           _stream(dev)), "certkv_select")
+    return (b, kept_offsets, kept_idx, mask) if with_mask else (b, kept_offsets, kept_idx)
 
 
 def tail_summary(spec: ProblemSpec, scores, k, v, kept_offsets, kept_idx, ksum=None, vsum=None):
@@ -216,7 +232,8 @@ def compact(spec: ProblemSpec, k, v, kept_offsets, kept_idx, k_star, v_star):
 class CompressBuffers:
     """Preallocated outputs and workspace of the fused pass (reusable)."""
 
-    def __init__(self, spec: ProblemSpec, n_keep, device, with_curves=False, with_perm=False):
+    def __init__(self, spec: ProblemSpec, n_keep, device, with_curves=False, with_perm=False,
+                 with_mask=False, with_lse=False):
         self.spec = spec
         self.n_keep = [int(x) for x in n_keep]
         H, D = spec.kv_heads, spec.head_dim
@@ -240,6 +257,9 @@ class CompressBuffers:
         self.perm = torch.empty(shape, dtype=torch.int32, device=device) if with_perm else None
         self.alloc_stats = torch.zeros((spec.layers * spec.batch, 3), dtype=torch.int64,
                                        device=device)
+        self.kept_mask = torch.empty(shape, dtype=torch.uint8, device=device) if with_mask else None
+        self.lse = torch.empty(_lse_shape(spec), dtype=torch.float32, device=device) \
+            if with_lse else None
         self.ws, self.ws_bytes = _workspace(spec, _lib.STAGE_COMPRESS, device)
         self._nk = (ctypes.c_int32 * spec.batch)(*self.n_keep)
         self._p = spec.c_problem()
@@ -247,25 +267,31 @@ class CompressBuffers:
             (t.data_ptr() if t is not None else None) for t in (
                 self.scores, self.budgets, self.kept_offsets, self.kept_idx, self.k_star,
                 self.v_star, self.tail_mass, self.k_packed, self.v_packed, self.pos_packed,
-                self.packed_offsets, self.curves, self.perm, self.alloc_stats)])
+                self.packed_offsets, self.curves, self.perm, self.alloc_stats, self.kept_mask,
+                self.lse)])
 
     def as_dict(self):
         return {k: getattr(self, k) for k in (
             "scores", "budgets", "kept_offsets", "kept_idx", "k_star", "v_star", "tail_mass",
             "k_packed", "v_packed", "pos_packed", "packed_offsets", "curves", "perm",
-            "alloc_stats")}
+            "alloc_stats", "kept_mask", "lse")}
 
 
 def compress(spec: ProblemSpec, q_win, k, v, n_keep, alpha=0.2, steps=40, bufs=None,
-             with_curves=False, with_perm=False):
+             with_curves=False, with_perm=False, with_mask=False, with_lse=False, lse_in=None):
     """The whole pass; returns the CompressBuffers holding every output."""
     L = _lib.lib()
     dev = k.device
     if bufs is None:
-        bufs = CompressBuffers(spec, n_keep, dev, with_curves=with_curves, with_perm=with_perm)
+        bufs = CompressBuffers(spec, n_keep, dev, with_curves=with_curves, with_perm=with_perm,
+                               with_mask=with_mask, with_lse=with_lse)
+    if lse_in is not None:
+        assert lse_in.dtype == torch.float32 and lse_in.is_contiguous()
+        assert tuple(lse_in.shape) == _lse_shape(spec)
     _check(L.certkv_compress(ctypes.byref(bufs._p), _tensor(q_win), _tensor(k), _tensor(v),
-                             bufs._nk, float(alpha), int(steps), ctypes.byref(bufs._out),
-                             _ptr(bufs.ws), bufs.ws_bytes, _stream(dev)), "certkv_compress")
+                             _ptr(lse_in), bufs._nk, float(alpha), int(steps),
+                             ctypes.byref(bufs._out), _ptr(bufs.ws), bufs.ws_bytes, _stream(dev)),
+           "certkv_compress")
     return bufs
 
 

@@ -95,6 +95,7 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.g.T = cu[p->batch];
   P.g.scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / sqrtf((float)p->head_dim);
   P.g.causal = (p->flags & CERTKV_CAUSAL) ? 1 : 0;
+  P.g.status = p->dev_status;
   P.dtype = p->kv_dtype;
   P.U = (int64_t)P.g.L * P.g.B * P.g.H;
   P.max_len = max_len;
@@ -300,10 +301,13 @@ static certkv_status check_ws(const Plan& P, uint32_t need, void* ws, size_t byt
   } while (0)
 
 // ---- stage drivers -----------------------------------------------------------
-static certkv_status do_score(const Plan& P, certkv_tensor q, certkv_tensor k, float* scores,
-                              double* ksum, const Bufs& w, hipStream_t s) {
+static certkv_status do_score(const Plan& P, certkv_tensor q, certkv_tensor k,
+                              const float* lse_in, float* scores, double* ksum, float* lse_out,
+                              const Bufs& w, hipStream_t s) {
   ScoreArgs a;
   a.g = P.g;
+  a.lse_in = lse_in;
+  a.lse_out = lse_out;
   a.q = q;
   a.k = k;
   a.dtype = P.dtype;
@@ -461,6 +465,8 @@ const char* certkv_status_string(certkv_status st) {
       return "unsupported configuration";
     case CERTKV_EINFEASIBLE:
       return "infeasible budget (need 2 <= n_keep <= n)";
+    case CERTKV_ENONFINITE:
+      return "non-finite input";
     case CERTKV_EWORKSPACE:
       return "workspace too small";
     case CERTKV_EHIP:
@@ -480,7 +486,8 @@ size_t certkv_workspace_size(const certkv_problem* p, int32_t stage) {
 }
 
 certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win, certkv_tensor k,
-                           float* scores, double* ksum, void* ws, size_t ws_bytes, void* stream) {
+                           const float* lse_in, float* scores, double* ksum, float* lse_out,
+                           void* ws, size_t ws_bytes, void* stream) {
   Plan P;
   TRY(make_plan(p, &P));
   TRY(check_tensor(q_win, P));
@@ -489,7 +496,7 @@ certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win, certkv_
   Bufs w;
   TRY(check_ws(P, stage_needs(CERTKV_STAGE_SCORE), ws, ws_bytes, &w));
   if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
-  return do_score(P, q_win, k, scores, ksum, w, (hipStream_t)stream);
+  return do_score(P, q_win, k, lse_in, scores, ksum, lse_out, w, (hipStream_t)stream);
 }
 
 certkv_status certkv_allocate(const certkv_problem* p, const float* scores, certkv_tensor v,
@@ -528,13 +535,14 @@ certkv_status certkv_allocate_curves(const certkv_problem* p, const float* curve
 
 certkv_status certkv_select(const certkv_problem* p, const float* scores, int32_t* budgets_io,
                             int32_t mode, double retain_mass, int64_t* kept_offsets,
-                            int32_t* kept_idx, int64_t kept_capacity, void* ws, size_t ws_bytes,
-                            void* stream) {
+                            int32_t* kept_idx, int64_t kept_capacity, uint8_t* kept_mask, void* ws,
+                            size_t ws_bytes, void* stream) {
   Plan P;
   TRY(make_plan(p, &P));
   if (!scores || !budgets_io || !kept_offsets || !kept_idx || kept_capacity < 0)
     return CERTKV_EINVAL;
   if (mode != CERTKV_SELECT_BUDGET && mode != CERTKV_SELECT_COVERAGE) return CERTKV_EINVAL;
+  if ((uintptr_t)kept_mask & 15u) return CERTKV_EINVAL;
   if (mode == CERTKV_SELECT_COVERAGE) {
     if (!(retain_mass > 0.0 && retain_mass <= 1.0)) return CERTKV_EINVAL;
     if (kept_capacity < (int64_t)P.g.L * P.g.H * P.g.T) return CERTKV_EINVAL;
@@ -544,8 +552,10 @@ certkv_status certkv_select(const certkv_problem* p, const float* scores, int32_
   if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
   hipStream_t s = (hipStream_t)stream;
   TRY(do_sort(P, scores, w.perm, w, s));
-  return do_select(P, scores, w.keysA, w.perm, budgets_io, mode, retain_mass, kept_offsets,
-                   nullptr, kept_idx, kept_capacity, nullptr, s);
+  TRY(do_select(P, scores, w.keysA, w.perm, budgets_io, mode, retain_mass, kept_offsets, nullptr,
+                kept_idx, kept_capacity, nullptr, s));
+  if (kept_mask) TRY(run_mask(P.g, make_tabs(P, nullptr, 0.f), kept_offsets, kept_idx, kept_mask, s));
+  return CERTKV_OK;
 }
 
 certkv_status certkv_tail_summary(const certkv_problem* p, const float* scores, certkv_tensor k,
@@ -593,9 +603,9 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k, certkv_te
 }
 
 certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, certkv_tensor k,
-                              certkv_tensor v, const int32_t* n_keep_host, double alpha,
-                              int32_t steps, const certkv_outputs* out, void* ws, size_t ws_bytes,
-                              void* stream) {
+                              certkv_tensor v, const float* lse_in, const int32_t* n_keep_host,
+                              double alpha, int32_t steps, const certkv_outputs* out, void* ws,
+                              size_t ws_bytes, void* stream) {
   Plan P;
   TRY(make_plan(p, &P));
   TRY(check_tensor(q_win, P));
@@ -606,6 +616,7 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, cert
       !out->pos_packed || !out->packed_offsets)
     return CERTKV_EINVAL;
   if (((uintptr_t)out->k_packed & 15u) || ((uintptr_t)out->v_packed & 15u)) return CERTKV_EINVAL;
+  if ((uintptr_t)out->kept_mask & 15u) return CERTKV_EINVAL;
   if (P.dtype == CERTKV_F32 && P.g.D != 64) return CERTKV_EUNSUPPORTED;
   TRY(check_budget(P, n_keep_host, alpha, steps));
   Bufs w;
@@ -617,15 +628,19 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, cert
   int64_t cap = 0;
   for (int b = 0; b < P.g.B; ++b) cap += (int64_t)P.g.H * n_keep_host[b] - P.g.H;
   cap *= P.g.L;
-  TRY(do_score(P, q_win, k, out->scores, w.ksum, w, s));
+  TRY(do_score(P, q_win, k, lse_in, out->scores, w.ksum, out->lse, w, s));
   TRY(do_sort(P, out->scores, pm, w, s));
   TRY(do_curves(P, v, pm, cv, w.vsum, w, s));
   TRY(do_allocate(P, cv, n_keep_host, alpha, steps, out->budgets, false, w, s, out->alloc_stats));
   TRY(do_select(P, out->scores, w.keysA, pm, out->budgets, CERTKV_SELECT_BUDGET, 0.0,
                 out->kept_offsets, out->packed_offsets, out->kept_idx, cap, &w, s));
-  return do_tail(P, out->scores, k, v, out->kept_offsets, out->kept_idx, w.ksum, w.vsum,
-                 out->k_star, out->v_star, out->tail_mass, out->k_packed, out->v_packed,
-                 out->pos_packed, true, true, true, w, s);
+  TRY(do_tail(P, out->scores, k, v, out->kept_offsets, out->kept_idx, w.ksum, w.vsum, out->k_star,
+              out->v_star, out->tail_mass, out->k_packed, out->v_packed, out->pos_packed, true, true,
+              true, w, s));
+  if (out->kept_mask)
+    TRY(run_mask(P.g, make_tabs(P, nullptr, 0.f), out->kept_offsets, out->kept_idx, out->kept_mask,
+                 s));
+  return CERTKV_OK;
 }
 
 certkv_status certkv_profile_enable(int32_t enable) {

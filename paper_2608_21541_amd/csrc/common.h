@@ -28,7 +28,14 @@ struct Geo {
   int64_t T;                 // total tokens
   float scale;               // softmax scale (natural-log units)
   int32_t causal;
+  int32_t* status;           // optional: set to CERTKV_ENONFINITE on a non-finite value
 };
+
+// Record a non-finite value in the caller's status word (racing stores all
+// write the same value).
+__device__ __forceinline__ void report_nonfinite(const Geo& g) {
+  if (g.status) *g.status = CERTKV_ENONFINITE;
+}
 
 __device__ __forceinline__ int64_t unit_index(const Geo& g, int l, int b, int h) {
   return ((int64_t)l * g.B + b) * g.H + h;

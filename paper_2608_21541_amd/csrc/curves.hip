@@ -282,7 +282,10 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
 #pragma unroll
     for (int lev = 0; lev < kLev; ++lev) r_mine |= ((lane >> (5 - lev)) & 1) << lev;
     const int rk = rank_of(k, r_mine);
-    if ((lane & (64 / kRPW - 1)) == 0 && rk < n) curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
+    if ((lane & (64 / kRPW - 1)) == 0 && rk < n) {
+      if (!isfinite(c2)) report_nonfinite(g);
+      curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
+    }
     // the last wave's final state carries into the next chunk
     if (wave == kCurveWaves - 1) {
 #pragma unroll

@@ -27,6 +27,7 @@ typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16_t __attribute__((__vector_size__(16 * sizeof(float))));
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kScoreThreads = 512;  // 8 waves
 constexpr float kSumLo = 8.673617379884035e-19f;  // 2^-60
 constexpr float kSumHi = 1.329227995784916e+36f;  // 2^120
@@ -565,12 +566,41 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(Geo g, SeqTab st, int3
         float2 p = part[(u * nkb_max + kb) * M + rho];
         if (p.x != -INFINITY) s += p.y * __builtin_amdgcn_exp2f(p.x - mt);
       }
-      lse2[u * M + rho] = mt + __builtin_amdgcn_logf(s);
+      const float r = mt + __builtin_amdgcn_logf(s);
+      if (!isfinite(r)) report_nonfinite(g);
+      lse2[u * M + rho] = r;
     }
   }
   if (SUM_FORMAT) {
     __syncthreads();
     if (threadIdx.x == 0) flag[u] = bad;
+  }
+}
+
+// Row log2-sums from a caller's natural-log log-sum-exp, [L][B*w][Hq]
+// (import), and back (export).  Row rho = q*G + gq of unit (l, b, h) is
+// window query q of sequence b, query head h*G + gq.
+template <bool IMPORT>
+__global__ __launch_bounds__(256) void lse_io_kernel(Geo g, SeqTab st, const float* __restrict__ lse_in,
+                                                      float* __restrict__ lse2,
+                                                      float* __restrict__ lse_out) {
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int M = g.w * g.G;
+  const int64_t u = unit_index(g, l, b, h);
+  for (int rho = threadIdx.x; rho < M; rho += blockDim.x) {
+    const int q = rho / g.G, gq = rho % g.G;
+    const int64_t i = (((int64_t)l * g.B + b) * g.w + q) * ((int64_t)g.H * g.G) + h * g.G + gq;
+    if (IMPORT) {
+      const float x = lse_in[i];
+      if (!isfinite(x)) report_nonfinite(g);
+      lse2[u * M + rho] = x * kLog2e;
+    } else {
+      lse_out[i] = lse2[u * M + rho] * kLn2;
+    }
   }
 }
 
@@ -713,19 +743,25 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
   }
   const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
   const uint16_t* k = static_cast<const uint16_t*>(a.k.ptr);
-  CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kPass1Sum>), grid,
-                dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
-                a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
-                (const int32_t*)nullptr);
-  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
-                s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
-  // fallback for flagged units (returns at once for the others)
-  CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kPass1Max>), grid,
-                dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
-                a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
-                (const int32_t*)a.flag);
-  CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
-                0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 1);
+  if (a.lse_in) {
+    CERTKV_LAUNCH("score_lse_import", lse_io_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
+                  s, g, st, a.lse_in, a.lse2, (float*)nullptr);
+  } else {
+    CERTKV_LAUNCH("score_pass1_mfma", (score_mfma_kernel<D, NQT, kPass1Sum>), grid,
+                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
+                  (const int32_t*)nullptr);
+    CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<true>, dim3(g.H * st.count, g.L), dim3(256),
+                  0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
+    // fallback for flagged units (returns at once for the others)
+    CERTKV_LAUNCH("score_pass1_fallback", (score_mfma_kernel<D, NQT, kPass1Max>), grid,
+                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, a.part,
+                  (const int32_t*)a.flag);
+    CERTKV_LAUNCH("score_lse_fallback", lse_combine_kernel<false>, dim3(g.H * st.count, g.L),
+                  dim3(256), 0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2,
+                  a.flag, 1);
+  }
   if (a.ksum)
     CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid, dim3(kScoreThreads),
                   smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
@@ -739,6 +775,9 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
                   s, g, st, a.keys_per_block, a.nkb_max, (const float*)a.kpart, a.ksum);
+  if (a.lse_out)
+    CERTKV_LAUNCH("score_lse_export", lse_io_kernel<false>, dim3(g.H * st.count, g.L), dim3(256), 0,
+                  s, g, st, (const float*)nullptr, a.lse2, a.lse_out);
   return CERTKV_OK;
 }
 
@@ -750,11 +789,16 @@ static certkv_status launch_f32(const ScoreArgs& a, const SeqTab& st, int max_le
   size_t smem = score_smem_bytes(g, CERTKV_F32);
   const float* q = static_cast<const float*>(a.q.ptr);
   const float* k = static_cast<const float*>(a.k.ptr);
-  CERTKV_LAUNCH("score_pass1_f32", (score_f32_kernel<D, false>), grid, dim3(256), smem, s, g, st, q,
-                a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token, a.k.s_head,
-                a.nkb_max, a.part, (const float*)nullptr, (float*)nullptr, (float*)nullptr);
-  CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<false>, dim3(g.H * st.count, g.L), dim3(256),
-                0, s, g, st, 256, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
+  if (a.lse_in) {
+    CERTKV_LAUNCH("score_lse_import", lse_io_kernel<true>, dim3(g.H * st.count, g.L), dim3(256), 0,
+                  s, g, st, a.lse_in, a.lse2, (float*)nullptr);
+  } else {
+    CERTKV_LAUNCH("score_pass1_f32", (score_f32_kernel<D, false>), grid, dim3(256), smem, s, g, st,
+                  q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token, a.k.s_head,
+                  a.nkb_max, a.part, (const float*)nullptr, (float*)nullptr, (float*)nullptr);
+    CERTKV_LAUNCH("score_lse_combine", lse_combine_kernel<false>, dim3(g.H * st.count, g.L),
+                  dim3(256), 0, s, g, st, 256, a.nkb_max, (const float2*)a.part, a.lse2, a.flag, 0);
+  }
   CERTKV_LAUNCH("score_pass2_f32", (score_f32_kernel<D, true>), grid, dim3(256), smem, s, g, st, q,
                 a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer, a.k.s_token, a.k.s_head,
                 a.nkb_max, (float2*)nullptr, (const float*)a.lse2, a.scores,
@@ -762,6 +806,9 @@ static certkv_status launch_f32(const ScoreArgs& a, const SeqTab& st, int max_le
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
                   s, g, st, 256, a.nkb_max, (const float*)a.kpart, a.ksum);
+  if (a.lse_out)
+    CERTKV_LAUNCH("score_lse_export", lse_io_kernel<false>, dim3(g.H * st.count, g.L), dim3(256), 0,
+                  s, g, st, (const float*)nullptr, a.lse2, a.lse_out);
   return CERTKV_OK;
 }
 

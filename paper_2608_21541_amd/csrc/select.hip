@@ -261,6 +261,48 @@ certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64
   return CERTKV_OK;
 }
 
+// Kept mask [L][H][T] uint8: cleared with 16-byte stores (the mask base is
+// 16-byte aligned; the tail of the buffer byte by byte), then the kept
+// positions of every unit set to 1.
+__global__ __launch_bounds__(256) void mask_clear_kernel(uint8_t* __restrict__ mask, int64_t bytes) {
+  const int64_t nvec = bytes / 16;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride)
+    reinterpret_cast<uint4*>(mask)[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (blockIdx.x == 0)
+    for (int64_t i = nvec * 16 + threadIdx.x; i < bytes; i += blockDim.x) mask[i] = 0;
+}
+
+__global__ __launch_bounds__(256) void mask_set_kernel(Geo g, SeqTab st,
+                                                        const int64_t* __restrict__ kept_offsets,
+                                                        const int32_t* __restrict__ kept_idx,
+                                                        uint8_t* __restrict__ mask) {
+  const int h = blockIdx.x % g.H;
+  const int bl = blockIdx.x / g.H;
+  const int l = blockIdx.y;
+  if (bl >= st.count) return;
+  const int n = st.len[bl];
+  const int64_t u = unit_index(g, l, st.first + bl, h);
+  const int64_t base = lht_base(g, l, h, st.start[bl]);
+  const int64_t k0 = kept_offsets[u], k1 = kept_offsets[u + 1];
+  for (int64_t i = k0 + threadIdx.x; i < k1; i += blockDim.x) {
+    const int j = kept_idx[i];
+    if (j >= 0 && j < n) mask[base + j] = 1;
+  }
+}
+
+certkv_status run_mask(const Geo& g, const std::vector<SeqTab>& tabs, const int64_t* kept_offsets,
+                       const int32_t* kept_idx, uint8_t* mask, hipStream_t s) {
+  const int64_t bytes = (int64_t)g.L * g.H * g.T;
+  const int64_t nvec = bytes / 16;
+  const unsigned blocks = (unsigned)(nvec / 256 + 1 < 4096 ? nvec / 256 + 1 : 4096);
+  CERTKV_LAUNCH("kept_mask_clear", mask_clear_kernel, dim3(blocks), dim3(256), 0, s, mask, bytes);
+  for (const SeqTab& t : tabs)
+    CERTKV_LAUNCH("kept_mask_set", mask_set_kernel, dim3(g.H * t.count, g.L), dim3(256), 0, s, g, t,
+                  kept_offsets, kept_idx, mask);
+  return CERTKV_OK;
+}
+
 certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s) {
   CERTKV_LAUNCH("select", select_kernel, dim3(a.g.H * st.count, a.g.L), dim3(kSelThreads), 0, s, a.g, st,
                 a.scores, a.sorted_keys, a.perm, (const int32_t*)a.budgets,

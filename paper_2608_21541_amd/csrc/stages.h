@@ -1,6 +1,8 @@
 // Argument blocks and host launchers of the kernel stages (internal).
 #pragma once
 
+#include <vector>
+
 #include "common.h"
 
 namespace certkv {
@@ -15,6 +17,8 @@ struct ScoreArgs {
   float* lse2;
   float* kpart;
   int32_t* flag;  // [U] units whose shift-free row sums left the safe range
+  const float* lse_in;  // optional caller row log-sum-exp [L][B*w][Hq]
+  float* lse_out;       // optional row log-sum-exp out, same layout
   int32_t keys_per_block;
   int32_t nkb_max;
 };
@@ -82,6 +86,8 @@ certkv_status run_clamp(const Geo& g, const SeqTab& st, int32_t* budgets, hipStr
 certkv_status run_offsets(int64_t U, const int32_t* budgets, int64_t* kept_offsets,
                           int64_t* packed_offsets, hipStream_t s);
 certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s);
+certkv_status run_mask(const Geo& g, const std::vector<SeqTab>& tabs, const int64_t* kept_offsets,
+                       const int32_t* kept_idx, uint8_t* mask, hipStream_t s);
 
 struct TailArgs {
   Geo g;

@@ -36,7 +36,7 @@ def problem(L=2, seqlens=(1000, 700), H=4, G=2, d=128, w=16, dtype=_lib.CERTKV_B
     arr = (ctypes.c_int64 * len(cu))(*cu)
     fl = (_lib.CERTKV_CAUSAL | _lib.CERTKV_DRY_RUN) if flags is None else flags
     p = _lib.Problem(L, len(seqlens), H, G, d, w, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int64)),
-                     dtype, dtype, 0.0, fl)
+                     dtype, dtype, 0.0, fl, None)
     p._keep = arr
     return p
 
@@ -55,7 +55,7 @@ def status_name(st):
 
 
 def test_status_strings():
-    for st in [0, -1, -2, -3, -5, -6, -99]:
+    for st in [0, -1, -2, -3, -4, -5, -6, -99]:
         assert isinstance(status_name(st), str) and status_name(st)
 
 
@@ -64,24 +64,25 @@ def test_dry_run_score_validation():
     p = problem()
     ws, n = ws_for(p, _lib.STAGE_SCORE)
     assert n > 0
-    ok = L.certkv_score(ctypes.byref(p), tensor(), tensor(), FAKE, None, ws, n, None)
-    assert ok == _lib.CERTKV_OK
-    assert L.certkv_score(ctypes.byref(p), tensor(), tensor(), FAKE, None, ws, n - 256, None) == \
-        _lib.CERTKV_EWORKSPACE
-    assert L.certkv_score(ctypes.byref(p), tensor(ptr=FAKE + 4), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EINVAL
-    assert L.certkv_score(ctypes.byref(p), tensor(st=4 * 128 + 4), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EINVAL
-    assert L.certkv_score(ctypes.byref(problem(d=96)), tensor(), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EUNSUPPORTED
-    assert L.certkv_score(ctypes.byref(problem(w=701)), tensor(), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EINVAL
-    assert L.certkv_score(ctypes.byref(problem(H=65)), tensor(), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EUNSUPPORTED
-    assert L.certkv_score(ctypes.byref(problem(w=64, G=9)), tensor(), tensor(), FAKE, None, ws, n,
-                          None) == _lib.CERTKV_EUNSUPPORTED  # 576 window rows > 512
-    assert L.certkv_score(ctypes.byref(problem(flags=_lib.CERTKV_DRY_RUN | 64)), tensor(),
-                          tensor(), FAKE, None, ws, n, None) == _lib.CERTKV_EINVAL
+
+    def call(pp, q=None, k=None, nbytes=n, lse_in=None, lse_out=None):
+        return L.certkv_score(ctypes.byref(pp), q or tensor(), k or tensor(), lse_in, FAKE, None,
+                              lse_out, ws, nbytes, None)
+
+    assert call(p) == _lib.CERTKV_OK
+    assert call(p, nbytes=n - 256) == _lib.CERTKV_EWORKSPACE
+    assert call(p, q=tensor(ptr=FAKE + 4)) == _lib.CERTKV_EINVAL
+    assert call(p, q=tensor(st=4 * 128 + 4)) == _lib.CERTKV_EINVAL
+    assert call(problem(d=96)) == _lib.CERTKV_EUNSUPPORTED
+    assert call(problem(w=701)) == _lib.CERTKV_EINVAL
+    assert call(problem(H=65)) == _lib.CERTKV_EUNSUPPORTED
+    assert call(problem(w=64, G=9)) == _lib.CERTKV_EUNSUPPORTED  # 576 window rows > 512
+    assert call(problem(flags=_lib.CERTKV_DRY_RUN | 64)) == _lib.CERTKV_EINVAL
+    # the caller's row log-sum-exp and the row log-sum-exp output are plain
+    # optional device pointers
+    assert call(p, lse_in=FAKE, lse_out=FAKE) == _lib.CERTKV_OK
+    assert L.certkv_score(ctypes.byref(p), tensor(), tensor(), None, None, None, None, ws, n,
+                          None) == _lib.CERTKV_EINVAL  # scores are required
 
 
 def test_dry_run_allocate_budget_checks():
@@ -108,20 +109,31 @@ def test_dry_run_compress_and_select():
     L = _lib.lib()
     p = problem()
     ws, n = ws_for(p, _lib.STAGE_COMPRESS)
-    out = _lib.Outputs(*([FAKE] * 11 + [None, None, None]))
+    out = _lib.Outputs(*([FAKE] * 11 + [None, None, None, None, None]))
     nk = (ctypes.c_int32 * 2)(101, 71)
-    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), nk, 0.2, 40,
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), None, nk, 0.2, 40,
+                             ctypes.byref(out), ws, n, None) == _lib.CERTKV_OK
+    out.kept_mask = FAKE + 8  # the kept mask must be 16-byte aligned
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), FAKE, nk, 0.2, 40,
+                             ctypes.byref(out), ws, n, None) == _lib.CERTKV_EINVAL
+    out.kept_mask = FAKE
+    out.lse = FAKE
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), FAKE, nk, 0.2, 40,
                              ctypes.byref(out), ws, n, None) == _lib.CERTKV_OK
     out.kept_idx = None
-    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), nk, 0.2, 40,
+    assert L.certkv_compress(ctypes.byref(p), tensor(), tensor(), tensor(), None, nk, 0.2, 40,
                              ctypes.byref(out), ws, n, None) == _lib.CERTKV_EINVAL
     ws2, n2 = ws_for(p, _lib.STAGE_SELECT)
-    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, 5, 0.9, FAKE, FAKE, 10, ws2, n2, None) == \
-        _lib.CERTKV_EINVAL  # bad mode
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, 5, 0.9, FAKE, FAKE, 10, None, ws2, n2,
+                           None) == _lib.CERTKV_EINVAL  # bad mode
     assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_COVERAGE, 1.5, FAKE,
-                           FAKE, 1 << 30, ws2, n2, None) == _lib.CERTKV_EINVAL
+                           FAKE, 1 << 30, None, ws2, n2, None) == _lib.CERTKV_EINVAL
     assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_COVERAGE, 0.9, FAKE,
-                           FAKE, 1 << 30, ws2, n2, None) == _lib.CERTKV_OK
+                           FAKE, 1 << 30, None, ws2, n2, None) == _lib.CERTKV_OK
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_BUDGET, 0.9, FAKE,
+                           FAKE, 10, FAKE, ws2, n2, None) == _lib.CERTKV_OK
+    assert L.certkv_select(ctypes.byref(p), FAKE, FAKE, _lib.CERTKV_SELECT_BUDGET, 0.9, FAKE,
+                           FAKE, 10, FAKE + 4, ws2, n2, None) == _lib.CERTKV_EINVAL
 
 
 def test_fp32_values_need_head_dim_64():

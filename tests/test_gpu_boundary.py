@@ -1,0 +1,139 @@
+"""GPU tests of the optional parts of the C ABI: the caller's row log-sum-exp
+(scoring without the row-sum pass), the row log-sum-exp output, the kept
+mask and the device status word for non-finite inputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_21541_amd as ck
+import synth
+from _parity import check_block_stages, score_rel_err, spec_of, unit_id
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+
+
+def _oracle_scores_and_lse(cfg, cache, li, b):
+    """Oracle scores [H][n] and the row log-sum-exp laid out [w][Hq] (fp64)."""
+    cu = cache["cu_seqlens"]
+    n = cu[b + 1] - cu[b]
+    H, G, D, w = cfg.kv_heads, cfg.group, cfg.head_dim, cfg.window
+    q = cache["q_win"][li, b * w:(b + 1) * w].double().numpy()      # [w][Hq][d]
+    k = cache["k"][li, cu[b]:cu[b + 1]].double().numpy()            # [n][H][d]
+    qpos = np.repeat(np.arange(n - w, n), G)
+    s = np.zeros((H, n))
+    lse = np.zeros((w, H * G))
+    for h in range(H):
+        Q = q[:, h * G:(h + 1) * G].reshape(w * G, D)               # row = q*G + gq
+        s[h], lr = oracle.scores(Q, qpos, k[:, h], 1.0 / math.sqrt(D), with_lse=True)
+        lse[:, h * G:(h + 1) * G] = lr.reshape(w, G)
+    return s, lse
+
+
+def test_lse_in_and_out_match_oracle():
+    cfg = synth.config("C2", seqlens=[4173, 2500])
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg)
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    w, Hq = cfg.window, cfg.kv_heads * cfg.group
+    lse_ref = np.zeros((1, cfg.batch * w, Hq))
+    s_ref = []
+    for b in range(cfg.batch):
+        s_b, lse_b = _oracle_scores_and_lse(cfg, cache, 0, b)
+        lse_ref[0, b * w:(b + 1) * w] = lse_b
+        s_ref.append(s_b)
+    # the row log-sum-exp the scorer forms itself
+    s_own, lse_out = ck.score(spec, q, k, with_lse=True)
+    lse_out = lse_out.cpu().double().numpy()
+    err = np.abs(lse_out - lse_ref) / np.maximum(1.0, np.abs(lse_ref))
+    log(f"lse_out max error {err.max():.2e}")
+    assert err.max() <= 1e-5
+    # scoring from the caller's row log-sum-exp (no row-sum pass)
+    lse_in = torch.from_numpy(lse_ref.astype(np.float32)).to(dev)
+    s_in, lse_echo = ck.score(spec, q, k, lse_in=lse_in, with_lse=True)
+    s_in = s_in.cpu().numpy()
+    cu = cache["cu_seqlens"]
+    for b in range(cfg.batch):
+        for h in range(cfg.kv_heads):
+            r, sm = score_rel_err(s_in[0, h, cu[b]:cu[b + 1]], s_ref[b][h])
+            assert r <= 1e-4 and sm <= 1e-4, (b, h, r, sm)
+    # the exported sums are the imported ones to within one rounding each way
+    np.testing.assert_allclose(lse_echo.cpu().numpy(), lse_ref.astype(np.float32), rtol=3e-7,
+                               atol=1e-7)
+    # the fused pass from the caller's row log-sum-exp: every stage against
+    # the oracle, end-to-end scores against the oracle's exact ones
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], lse_in=lse_in, with_curves=True,
+                       with_perm=True)
+    torch.cuda.synchronize()
+    out = {name: (t.cpu() if t is not None else None) for name, t in bufs.as_dict().items()}
+    for b in range(cfg.batch):
+        check_block_stages(spec, cfg, cache, out, 0, b, log=log)
+
+
+def test_kept_mask_marks_exactly_the_kept_positions():
+    cfg = synth.config("C4", seqlens=[3000, 8192 + 5, 1024], layers=2)
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg)
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], with_mask=True)
+    torch.cuda.synchronize()
+    mask = bufs.kept_mask.cpu().numpy()
+    ko = bufs.kept_offsets.cpu().numpy()
+    ki = bufs.kept_idx.cpu().numpy()
+    cu = cache["cu_seqlens"]
+    want = np.zeros_like(mask)
+    for li in range(2):
+        for b in range(cfg.batch):
+            for h in range(cfg.kv_heads):
+                u = unit_id(spec, li, b, h)
+                want[li, h, cu[b] + ki[ko[u]:ko[u + 1]]] = 1
+    assert np.array_equal(mask, want)
+    assert int(mask.sum()) == int(bufs.budgets.sum().item())
+    # the selection entry point produces the same mask from the same budgets
+    _, ko2, ki2, mask2 = ck.select(spec, bufs.scores, bufs.budgets, with_mask=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(mask2.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("where", ["clean", "k_nan", "v_inf", "lse_inf"])
+def test_nonfinite_inputs_set_the_status_word(where):
+    cfg = synth.config("C2", seqlens=[2000])
+    cache = synth.make_cache(cfg, "cpu")
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].clone().to(dev) for x in ("q_win", "k", "v"))
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    spec = ck.ProblemSpec(1, cfg.kv_heads, cfg.group, cfg.head_dim, cfg.window, cfg.seqlens,
+                          cfg.dtype, status=status)
+    lse_in = None
+    if where == "k_nan":
+        k[0, 1234, 3, 17] = float("nan")
+    elif where == "v_inf":
+        v[0, 77, 5, 0] = float("inf")
+    elif where == "lse_inf":
+        _, lse = ck.score(spec, q, k, with_lse=True)
+        lse_in = lse.clone()
+        lse_in[0, 5, 9] = float("inf")
+        torch.cuda.synchronize()
+        assert status.item() == 0
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], lse_in=lse_in)
+    torch.cuda.synchronize()
+    want = 0 if where == "clean" else ck.CERTKV_ENONFINITE
+    assert status.item() == want, (where, status.item())
+    # the pass ran to completion and kept its budget algebra
+    br, _ = oracle.budget_params(cfg.kv_heads, 2000, cache["n_keep"][0])
+    assert int(bufs.budgets.sum().item()) == br
