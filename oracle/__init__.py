@@ -46,6 +46,7 @@ def lib():
         L = ctypes.CDLL(path)
         L.ora_scores.argtypes = [_i64, _i32, _i32, _p, _p, _p, _dbl, _i32, _p, _p]
         L.ora_order.argtypes = [_i64, _p, _p]
+        L.ora_order_window.argtypes = [_i64, _p, _i64, _p]
         L.ora_normalize.argtypes = [_i64, _p, _p]
         L.ora_curves.argtypes = [_i64, _i32, _p, _p, _p, _p, _p]
         L.ora_budget_params.argtypes = [_i32, _i64, _i64, _dbl, _p, _p]
@@ -53,7 +54,7 @@ def lib():
         L.ora_argmin_penalized.restype = _i64
         L.ora_allocate.argtypes = [_i32, _i64, _p, _i64, _dbl, _i32, _p, _p, _p]
         L.ora_select.argtypes = [_i64, _p, _i64, _p]
-        L.ora_coverage.argtypes = [_i64, _p, _p, _dbl, _p]
+        L.ora_coverage.argtypes = [_i64, _p, _p, _dbl, _i64, _p]
         L.ora_tail.argtypes = [_i64, _i32, _p, _p, _i64, _p, _p, _p, _p, _p]
         L.ora_f32_to_bf16.argtypes = [ctypes.c_float]
         L.ora_f32_to_bf16.restype = ctypes.c_uint16
@@ -61,7 +62,7 @@ def lib():
         L.ora_row_error.restype = _dbl
         L.ora_compress_block.argtypes = [
             _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _dbl, _i32, _i64, _dbl,
-            _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
+            _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
         L.ora_num_threads.restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -105,10 +106,16 @@ def scores(q, qpos, k, scale, causal=True, with_lse=False):
     return (s, lse) if with_lse else s
 
 
-def order(s32):
+def order(s32, keep_window=0):
+    """Rank order (score descending, ties by position); keep_window = w puts the
+    last w positions first, in ascending position."""
     s32 = _f32(s32)
     perm = np.zeros(s32.shape[0], np.int32)
-    _check(lib().ora_order(s32.shape[0], _ptr(s32), _ptr(perm)), "order")
+    if keep_window:
+        _check(lib().ora_order_window(s32.shape[0], _ptr(s32), int(keep_window), _ptr(perm)),
+               "order_window")
+    else:
+        _check(lib().ora_order(s32.shape[0], _ptr(s32), _ptr(perm)), "order")
     return perm
 
 
@@ -164,11 +171,11 @@ def select(perm, b):
     return kept
 
 
-def coverage(s32, perm, retain):
+def coverage(s32, perm, retain, k_min=1):
     s32, perm = _f32(s32), _i32a(perm)
     k = np.zeros(1, np.int64)
-    _check(lib().ora_coverage(s32.shape[0], _ptr(s32), _ptr(perm), float(retain), _ptr(k)),
-           "coverage")
+    _check(lib().ora_coverage(s32.shape[0], _ptr(s32), _ptr(perm), float(retain), int(k_min),
+                              _ptr(k)), "coverage")
     return int(k[0])
 
 
@@ -202,11 +209,13 @@ def row_error(A, V, kept_mask, u=None):
                                      _ptr(uu)))
 
 
-def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32_in=None):
+def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32_in=None,
+                   keep_window=False):
     """One (layer, sequence) block end to end.
 
     q [w][H*G][d], k/v [n][H][d] (any float dtype; converted to fp64 exactly).
     s32_in [H][n] optional fp32 scores that replace the scoring step.
+    keep_window ranks the w window keys first, so every head keeps them.
     Returns a dict of every intermediate and output.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
@@ -228,7 +237,8 @@ def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32
     sin = _f32(s32_in) if s32_in is not None else None
     _check(lib().ora_compress_block(
         n, H, G, d, w, _ptr(q), _ptr(k), _ptr(v), float(scale), int(bool(causal)),
-        int(n_keep), float(alpha), int(steps), _ptr(sin), _ptr(s), _ptr(s32), _ptr(perm),
+        int(n_keep), float(alpha), int(steps), int(bool(keep_window)), _ptr(sin), _ptr(s),
+        _ptr(s32), _ptr(perm),
         _ptr(c32), _ptr(b), _ptr(kept), _ptr(kept_off), _ptr(ks), _ptr(vs), _ptr(m),
         _ptr(rep)), "compress_block")
     return dict(s=s, s32=s32, perm=perm, c32=c32, budgets=b,

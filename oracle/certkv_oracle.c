@@ -105,6 +105,29 @@ int ora_order(int64_t n, const float* s32, int32_t* perm) {
   return ORA_OK;
 }
 
+/* Ordering with the observation window kept (the option that never evicts
+ * the w window keys, which the unchanged window scorer leaves to the
+ * caller): the keys at positions n-w..n-1 take ranks 0..w-1 in ascending
+ * position, as if their scores were +infinity; the other keys follow in the
+ * plain order (score descending, ties by position).  w = 0 is the plain
+ * order. */
+int ora_order_window(int64_t n, const float* s32, int64_t w, int32_t* perm) {
+  if (n <= 0 || w < 0 || w > n) return ORA_EINVAL;
+  for (int64_t j = 0; j < n; ++j)
+    if (!isfinite(s32[j])) return ORA_ENONFINITE;
+  for (int64_t r = 0; r < w; ++r) perm[r] = (int32_t)(n - w + r);
+  int32_t* rest = perm + w;
+  for (int64_t j = 0; j < n - w; ++j) rest[j] = (int32_t)j;
+  if (n - w > 1) {
+#pragma omp critical(ora_sort)
+    {
+      g_sort_keys = s32;
+      qsort(rest, (size_t)(n - w), sizeof(int32_t), cmp_desc_then_index);
+    }
+  }
+  return ORA_OK;
+}
+
 /* Normalization, appendix "CertKV: implementation": a_j = (s_j)_+ /
  * sum_i (s_i)_+, normalized directly (no second softmax).  The sum runs in
  * position order.  An all-zero score vector gives the uniform a = 1/n. */
@@ -305,10 +328,13 @@ int ora_select(int64_t n, const int32_t* perm, int64_t b, int32_t* kept) {
 }
 
 /* Coverage budget, Section 3 Eq. coverage-def with retained fraction
- * retain = 1 - eta: the smallest k >= 1 whose top-k mass sum_{r<=k} a_(r),
- * summed in rank order, reaches retain; n if it never does. */
+ * retain = 1 - eta: the smallest k >= k_min whose top-k mass
+ * sum_{r<=k} a_(r), summed in rank order, reaches retain; n if it never
+ * does.  k_min = 1 is the definition; k_min = w keeps the whole observation
+ * window when it leads the order. */
 int ora_coverage(int64_t n, const float* s32, const int32_t* perm,
-                 double retain, int64_t* k_eta) {
+                 double retain, int64_t k_min, int64_t* k_eta) {
+  if (k_min < 1 || k_min > n) return ORA_EINVAL;
   double* a = (double*)malloc(sizeof(double) * (size_t)n);
   if (!a) return ORA_ENOMEM;
   int st = ora_normalize(n, s32, a);
@@ -320,7 +346,7 @@ int ora_coverage(int64_t n, const float* s32, const int32_t* perm,
   int64_t k = n;
   for (int64_t r = 0; r < n; ++r) {
     p += a[perm[r]];
-    if (p >= retain) {
+    if (r + 1 >= k_min && p >= retain) {
       k = r + 1;
       break;
     }
@@ -417,11 +443,14 @@ double ora_row_error(int64_t n, int32_t d, const double* A, const double* V,
  *   kept   [H*n] out, unit h's run at kept_off[h]; kept_off [H+1] out
  *   kstar, vstar [H][d] out; m [H] out
  * When s32_in is not NULL the scoring step is skipped and those fp32 scores
- * are used instead (stage parity: the oracle fed the GPU's scores). */
+ * are used instead (stage parity: the oracle fed the GPU's scores).
+ * keep_window != 0 ranks the w window keys first (ora_order_window), so
+ * every head keeps them; it needs b_min >= w. */
 int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
                        const double* q, const double* k, const double* v,
                        double scale, int32_t causal, int64_t n_keep,
-                       double alpha, int32_t T, const float* s32_in,
+                       double alpha, int32_t T, int32_t keep_window,
+                       const float* s32_in,
                        double* s, float* s32, int32_t* perm, float* c32,
                        int32_t* b, int32_t* kept, int64_t* kept_off,
                        double* kstar, double* vstar, double* m,
@@ -432,6 +461,8 @@ int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
   int64_t B_real, b_min;
   int st = ora_budget_params(H, n, n_keep, alpha, &B_real, &b_min);
   if (st != ORA_OK) return st;
+  /* with the window kept, every head must be able to hold it */
+  if (keep_window && b_min < w) return ORA_EINFEASIBLE;
 #pragma omp parallel for schedule(dynamic, 1)
   for (int32_t h = 0; h < H; ++h) {
     int lerr = ORA_OK;
@@ -467,7 +498,8 @@ int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
       }
     }
     if (lerr == ORA_OK)
-      lerr = ora_order(n, s32 + (size_t)h * n, perm + (size_t)h * n);
+      lerr = ora_order_window(n, s32 + (size_t)h * n, keep_window ? w : 0,
+                              perm + (size_t)h * n);
     if (lerr == ORA_OK)
       lerr = ora_curves(n, d, s32 + (size_t)h * n, perm + (size_t)h * n, vh,
                         NULL, c32 + (size_t)h * n);

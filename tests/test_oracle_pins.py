@@ -109,6 +109,31 @@ def test_order_exhaustive_small(n):
                     assert (rank[i] < rank[j]) == before
 
 
+@pytest.mark.parametrize("n,w", [(1, 1), (4, 2), (5, 5), (7, 3)])
+def test_order_keep_window_exhaustive_small(n, w):
+    # The keep-window order ranks the last w positions first as if their
+    # scores were +infinity: with t_j = +inf for the window and s_j otherwise,
+    # rank(i) < rank(j) iff t_i > t_j or (t_i == t_j and i < j), for every
+    # assignment of tied values.
+    vals = [0.0, 0.5, 2.0]
+    for combo in itertools.product(vals, repeat=n) if n <= 5 else [
+            tuple(np.random.default_rng(n).choice(vals, n)) for _ in range(200)]:
+        s = np.array(combo, np.float32)
+        perm = oracle.order(s, keep_window=w)
+        t = s.astype(np.float64)
+        t[n - w:] = np.inf
+        rank = np.empty(n, int)
+        rank[perm] = np.arange(n)
+        for i in range(n):
+            for j in range(n):
+                if i != j:
+                    before = t[i] > t[j] or (t[i] == t[j] and i < j)
+                    assert (rank[i] < rank[j]) == before
+    # keep_window = 0 is the plain order
+    s = np.random.default_rng(3).random(n).astype(np.float32)
+    assert np.array_equal(oracle.order(s, keep_window=0), oracle.order(s))
+
+
 def test_normalize_clips_and_sums_to_one():
     # appendix "CertKV: implementation": a = (s)_+ / sum (s)_+
     s = np.array([2.0, -1.0, 1.0, 0.0, 1.0], np.float32)
@@ -395,6 +420,23 @@ def test_coverage_threshold_is_inclusive():
     assert oracle.coverage(s, perm, 1.0) == 3
 
 
+def test_coverage_floor_counts_from_k_min():
+    # With a floor k_min the budget is the smallest k >= k_min reaching the
+    # retained mass: the definition's k when that is already >= k_min.
+    rng = np.random.default_rng(12)
+    for trial in range(50):
+        n = int(rng.integers(2, 40))
+        s = (rng.random(n) ** 3).astype(np.float32)
+        perm = oracle.order(s)
+        a = oracle.normalize(s)
+        retain = float(rng.uniform(0.05, 0.99))
+        k1 = oracle.coverage(s, perm, retain)
+        k_min = int(rng.integers(1, n + 1))
+        k = oracle.coverage(s, perm, retain, k_min=k_min)
+        assert k == max(k1, k_min)
+        assert a[perm[:k]].sum() >= retain - 1e-15
+
+
 def test_order_statistic_mass_bound():
     # 1 - p(k) <= (n - k)/(k + 1) for every row and k in [n-1].
     rng = np.random.default_rng(11)
@@ -588,6 +630,31 @@ def test_compress_block_invariants():
         qpos = np.repeat(n - w + np.arange(w), G)
         np.testing.assert_allclose(out["s"][h], oracle.scores(qh, qpos, k[:, h], 1 / math.sqrt(d)),
                                    rtol=1e-14)
+
+
+def test_compress_block_keep_window():
+    # Every head keeps the w window keys; the budget algebra is unchanged; a
+    # budget too small to hold the window is infeasible.
+    rng = np.random.default_rng(17)
+    n, H, G, d, w = 400, 3, 2, 8, 6
+    q = rng.standard_normal((w, H * G, d))
+    k = rng.standard_normal((n, H, d))
+    v = rng.standard_normal((n, H, d))
+    n_keep = 41
+    out = oracle.compress_block(q, k, v, n_keep, 1 / math.sqrt(d), keep_window=True)
+    plain = oracle.compress_block(q, k, v, n_keep, 1 / math.sqrt(d))
+    br, bm = oracle.budget_params(H, n, n_keep)
+    assert bm >= w and out["budgets"].sum() == br
+    np.testing.assert_array_equal(out["s"], plain["s"])
+    for h in range(H):
+        assert out["perm"][h, :w].tolist() == list(range(n - w, n))
+        assert set(range(n - w, n)) <= set(out["kept"][h].tolist())
+        # ranks after the window follow the plain order of the other keys
+        rest = [j for j in plain["perm"][h] if j < n - w]
+        assert out["perm"][h, w:].tolist() == rest
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.compress_block(q, k, v, 6, 1 / math.sqrt(d), keep_window=True)  # b_min = 1 < w
+    assert e.value.code == oracle.ORA_EINFEASIBLE
 
 
 # --------------------------------------------------------------------------
