@@ -59,7 +59,8 @@ enum {
   CERTKV_EINVAL = -1,       /* null pointer, bad size, stride or flag      */
   CERTKV_EUNSUPPORTED = -2, /* head_dim not 64/128, dtype not built, or a  */
                             /* per-head slice spanning 4 GiB or more      */
-  CERTKV_EINFEASIBLE = -3,  /* n_keep < 2 or n_keep > n_b (budget algebra) */
+  CERTKV_EINFEASIBLE = -3,  /* n_keep < 2 or n_keep > n_b (budget algebra), */
+                            /* or b_min < w under CERTKV_KEEP_WINDOW       */
   CERTKV_ENONFINITE = -4,   /* written to *dev_status by a kernel that met */
                             /* a non-finite input (never returned by a    */
                             /* call: the launches are asynchronous)        */
@@ -71,7 +72,17 @@ enum { CERTKV_F32 = 0, CERTKV_BF16 = 1 };
 
 enum {
   CERTKV_CAUSAL = 1u << 0,  /* window rows see only keys at or before them  */
-  CERTKV_DRY_RUN = 1u << 1  /* validate arguments, launch nothing           */
+  CERTKV_DRY_RUN = 1u << 1, /* validate arguments, launch nothing           */
+  CERTKV_KEEP_WINDOW = 1u << 2  /* the w window keys of each sequence take  */
+                            /* ranks 0..w-1 (ascending position), as if     */
+                            /* their scores were +infinity, so every head   */
+                            /* keeps them; their masses a_j are unchanged.  */
+                            /* Budget calls need b_min >= w (else           */
+                            /* CERTKV_EINFEASIBLE); a selection budget      */
+                            /* below w keeps the first b window keys;       */
+                            /* coverage budgets are at least w.  The paper  */
+                            /* ranks all n keys (the default); this is the  */
+                            /* option of never evicting the window.         */
 };
 
 /* Selection modes of certkv_select. */
@@ -113,7 +124,8 @@ typedef struct certkv_problem {
   int32_t q_dtype;               /* CERTKV_F32 or CERTKV_BF16                 */
   int32_t kv_dtype;              /* CERTKV_F32 or CERTKV_BF16; equal to q_dtype */
   float softmax_scale;           /* logit scale; 0 selects 1/sqrt(d)          */
-  uint32_t flags;                /* CERTKV_CAUSAL | CERTKV_DRY_RUN            */
+  uint32_t flags;                /* CERTKV_CAUSAL | CERTKV_DRY_RUN |
+                                    CERTKV_KEEP_WINDOW                        */
   int32_t* dev_status;           /* optional device int32: kernels that meet a
                                     non-finite value (a window row whose
                                     log-sum-exp is not finite, a caller log-sum

@@ -22,6 +22,7 @@ CERTKV_F32 = 0
 CERTKV_BF16 = 1
 CERTKV_CAUSAL = 1
 CERTKV_DRY_RUN = 2
+CERTKV_KEEP_WINDOW = 4
 CERTKV_SELECT_BUDGET = 0
 CERTKV_SELECT_COVERAGE = 1
 

@@ -28,6 +28,7 @@ class ProblemSpec:
     softmax_scale: float = 0.0
     causal: bool = True
     dry_run: bool = False
+    keep_window: bool = False   # window keys ranked first, never evicted
     status: Optional[torch.Tensor] = None  # device int32 [1]: CERTKV_ENONFINITE on non-finite input
     _cu: object = field(default=None, repr=False)
 
@@ -54,7 +55,8 @@ class ProblemSpec:
         self._cu = (ctypes.c_int64 * len(cu))(*cu)  # kept alive with the spec
         dt = _dtype_code(self.dtype)
         flags = (_lib.CERTKV_CAUSAL if self.causal else 0) | (
-            _lib.CERTKV_DRY_RUN if self.dry_run else 0)
+            _lib.CERTKV_DRY_RUN if self.dry_run else 0) | (
+            _lib.CERTKV_KEEP_WINDOW if self.keep_window else 0)
         st = self.status.data_ptr() if self.status is not None else None
         return _lib.Problem(self.layers, self.batch, self.kv_heads, self.group, self.head_dim,
                             self.window, ctypes.cast(self._cu, ctypes.POINTER(ctypes.c_int64)),

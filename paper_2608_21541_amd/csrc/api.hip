@@ -72,7 +72,8 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   if (!p->cu_seqlens_host) return CERTKV_EINVAL;
   if (p->q_dtype != p->kv_dtype) return CERTKV_EUNSUPPORTED;
   if (p->kv_dtype != CERTKV_F32 && p->kv_dtype != CERTKV_BF16) return CERTKV_EUNSUPPORTED;
-  if (p->flags & ~(uint32_t)(CERTKV_CAUSAL | CERTKV_DRY_RUN)) return CERTKV_EINVAL;
+  if (p->flags & ~(uint32_t)(CERTKV_CAUSAL | CERTKV_DRY_RUN | CERTKV_KEEP_WINDOW))
+    return CERTKV_EINVAL;
   if (!(p->softmax_scale >= 0.f) || isinf(p->softmax_scale)) return CERTKV_EINVAL;
   const int64_t* cu = p->cu_seqlens_host;
   if (cu[0] != 0) return CERTKV_EINVAL;
@@ -96,6 +97,7 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.g.scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / sqrtf((float)p->head_dim);
   P.g.causal = (p->flags & CERTKV_CAUSAL) ? 1 : 0;
   P.g.status = p->dev_status;
+  P.g.keep_w = (p->flags & CERTKV_KEEP_WINDOW) ? p->window : 0;
   P.dtype = p->kv_dtype;
   P.U = (int64_t)P.g.L * P.g.B * P.g.H;
   P.max_len = max_len;
@@ -166,6 +168,7 @@ static certkv_status check_budget(const Plan& P, const int32_t* n_keep, double a
     int64_t bm = (int64_t)floor(alpha * (double)br / (double)P.g.H);
     if (bm < 1) bm = 1;
     if (bm > nb - 1 || (int64_t)P.g.H * bm > br) return CERTKV_EINFEASIBLE;
+    if (P.g.keep_w && bm < P.g.keep_w) return CERTKV_EINFEASIBLE;
   }
   return CERTKV_OK;
 }
@@ -464,7 +467,7 @@ const char* certkv_status_string(certkv_status st) {
     case CERTKV_EUNSUPPORTED:
       return "unsupported configuration";
     case CERTKV_EINFEASIBLE:
-      return "infeasible budget (need 2 <= n_keep <= n)";
+      return "infeasible budget (need 2 <= n_keep <= n, and b_min >= w with a kept window)";
     case CERTKV_ENONFINITE:
       return "non-finite input";
     case CERTKV_EWORKSPACE:

@@ -28,6 +28,7 @@ struct Geo {
   int64_t T;                 // total tokens
   float scale;               // softmax scale (natural-log units)
   int32_t causal;
+  int32_t keep_w;            // window keys ranked first (w), or 0
   int32_t* status;           // optional: set to CERTKV_ENONFINITE on a non-finite value
 };
 

@@ -95,6 +95,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int64_t u = unit_index(g, l, b, h);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int bb = budgets[u];
+  const int wkeep = n - g.keep_w;  // first kept-window position (n: none)
   uint32_t kthr = 0u;
   int32_t ithr = -1;  // keep nothing when bb == 0
   if (bb > 0 && bb <= n) {
@@ -124,7 +125,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       const int j = jt + r;
       const bool valid = j < n;
       const uint32_t key = desc_key(cur[r]);
-      keep[r] = valid && (key < kthr || (key == kthr && j <= ithr));
+      // kept window keys hold ranks 0..w-1 in position order; the others
+      // are kept up to the threshold pair at rank bb-1
+      keep[r] = valid && (j >= wkeep ? (j - wkeep < bb)
+                                     : (bb > g.keep_w && (key < kthr || (key == kthr && j <= ithr))));
       if (valid) {
         const double sp = cur[r] > 0.f ? (double)cur[r] : 0.0;
         sa += sp;
@@ -222,6 +226,8 @@ __global__ __launch_bounds__(64) void coverage_kernel(Geo g, SeqTab st, const fl
       }
     }
   }
+  // a kept window leads the order and is never cut
+  if (g.keep_w) k = max(k, min(g.keep_w, n));
   if (lane == 0) budgets[unit_index(g, l, b, h)] = k;
 }
 

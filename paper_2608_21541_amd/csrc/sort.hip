@@ -95,6 +95,8 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   const int64_t u = unit_index(g, l, b, h);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  // positions from wkeep on are the kept window: key 0 ranks them first
+  const int wkeep = n - g.keep_w;
 
   for (int i = threadIdx.x; i < 4 * 256; i += kSortThreads) (&hist[0][0])[i] = 0u;
   if (threadIdx.x < 256) tile_tot[threadIdx.x] = 0u;
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
         const bool valid = e < n;
         if (valid && sv[r] > 0.f) psum += (double)sv[r];
-        const uint32_t key = desc_key(sv[r]);
+        const uint32_t key = e >= wkeep ? 0u : desc_key(sv[r]);
         if (valid) {
 #pragma unroll
           for (int p = 0; p < 4; ++p) atomicAdd(&hist[p][(key >> (8 * p)) & 255u], 1u);
@@ -154,7 +156,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         const bool ok = e < n;
         if (p == 0) {
           const float x = scores[base + min(e, n - 1)];
-          key[r] = desc_key(ok ? x : 0.f);
+          key[r] = e >= wkeep ? 0u : desc_key(ok ? x : 0.f);
           val[r] = e;
         } else {
           const uint32_t kx = kin[base + min(e, n - 1)];
@@ -263,6 +265,11 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   pass(std::integral_constant<int, 1>());
   pass(std::integral_constant<int, 2>());
   pass(std::integral_constant<int, 3>());
+  // Kept window: its keys sorted as 0 (ahead of every score) and so hold
+  // ranks 0..w-1 in position order; give them their score keys back, which
+  // the masses of the dispersion curves and the coverage prefix read.
+  for (int t = threadIdx.x; t < g.keep_w; t += kSortThreads)
+    keys_out[base + t] = desc_key(scores[base + n - g.keep_w + t]);
 }
 
 certkv_status run_sort(const SortArgs& a, const SeqTab& st, hipStream_t s) {

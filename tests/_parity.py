@@ -64,7 +64,8 @@ def vec_rel_err(x, ref, scale):
                                                                        1e-300))
 
 
-def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=print):
+def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=print,
+                       keep_window=False):
     """Compare one (layer, sequence) block of the GPU output with the oracle.
 
     Integer stages are compared against the oracle fed the GPU's own upstream
@@ -87,7 +88,7 @@ def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=prin
     res = {}
 
     # Stage parity: the oracle's steps fed the GPU scores.
-    st = oracle.compress_block(q, k, v, n_keep, scale, s32_in=s_gpu)
+    st = oracle.compress_block(q, k, v, n_keep, scale, s32_in=s_gpu, keep_window=keep_window)
     assert np.array_equal(st["perm"], perm_gpu), "order differs from the oracle's on the same scores"
     dc = np.abs(c_gpu.astype(np.float64) - st["c32"].astype(np.float64))
     cmax = float(st["c32"].max())
@@ -147,7 +148,7 @@ def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=prin
     assert blk == H * n_keep, "packed rows per (layer, sequence) must equal H * n_keep"
 
     if check_scores:
-        e2e = oracle.compress_block(q, k, v, n_keep, scale)
+        e2e = oracle.compress_block(q, k, v, n_keep, scale, keep_window=keep_window)
         worst = 0.0
         for h in range(H):
             r, sm = score_rel_err(s_gpu[h], e2e["s"][h])

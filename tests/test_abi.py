@@ -136,6 +136,21 @@ def test_dry_run_compress_and_select():
                            FAKE, 10, FAKE + 4, ws2, n2, None) == _lib.CERTKV_EINVAL
 
 
+def test_keep_window_needs_room_for_the_window():
+    L = _lib.lib()
+    p = problem(flags=_lib.CERTKV_CAUSAL | _lib.CERTKV_DRY_RUN | _lib.CERTKV_KEEP_WINDOW)
+    ws, n = ws_for(p, _lib.STAGE_ALLOCATE)
+
+    def call(nk):
+        arr = (ctypes.c_int32 * 2)(*nk)
+        return L.certkv_allocate(ctypes.byref(p), FAKE, tensor(), arr, 0.2, 40, FAKE, None,
+                                 None, None, ws, n, None)
+
+    # H = 4, w = 16: b_min = floor(0.2 * (4 n_keep - 4) / 4) must reach 16
+    assert call([101, 81]) == _lib.CERTKV_OK          # b_min = 20, 16
+    assert call([101, 71]) == _lib.CERTKV_EINFEASIBLE  # b_min = 14 < 16 for sequence 2
+
+
 def test_fp32_values_need_head_dim_64():
     L = _lib.lib()
     p = problem(dtype=_lib.CERTKV_F32, d=128, w=8, G=1)

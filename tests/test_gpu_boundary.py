@@ -137,3 +137,57 @@ def test_nonfinite_inputs_set_the_status_word(where):
     # the pass ran to completion and kept its budget algebra
     br, _ = oracle.budget_params(cfg.kv_heads, 2000, cache["n_keep"][0])
     assert int(bufs.budgets.sum().item()) == br
+
+
+def test_keep_window_matches_oracle():
+    # both lengths give b_min >= w = 64 (83 and 70)
+    cfg = synth.config("C2", seqlens=[4173, 3500])
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg)
+    spec.keep_window = True
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], with_curves=True, with_perm=True)
+    torch.cuda.synchronize()
+    out = {name: (t.cpu() if t is not None else None) for name, t in bufs.as_dict().items()}
+    w, cu = cfg.window, cache["cu_seqlens"]
+    ko, ki = out["kept_offsets"].numpy(), out["kept_idx"].numpy()
+    for b in range(cfg.batch):
+        n = cu[b + 1] - cu[b]
+        perm = out["perm"][0, :, cu[b]:cu[b + 1]].numpy()
+        assert (perm[:, :w] == np.arange(n - w, n)).all()
+        for h in range(cfg.kv_heads):
+            u = unit_id(spec, 0, b, h)
+            assert set(range(n - w, n)) <= set(ki[ko[u]:ko[u + 1]].tolist())
+        check_block_stages(spec, cfg, cache, out, 0, b, log=log, keep_window=True)
+
+
+def test_keep_window_selection_and_coverage():
+    cfg = synth.config("C1")
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg)
+    spec.keep_window = True
+    dev = torch.device("cuda:0")
+    q, k = cache["q_win"].to(dev), cache["k"].to(dev)
+    s = ck.score(spec, q, k)
+    s_np = s.cpu().numpy()
+    n, w, H = cfg.seqlens[0], cfg.window, cfg.kv_heads
+    for retain in [0.05, 0.5, 0.9]:
+        kb, ko, ki = ck.select(spec, s, mode="coverage", retain_mass=retain)
+        torch.cuda.synchronize()
+        for h in range(H):
+            perm = oracle.order(s_np[0, h], keep_window=w)
+            k_eta = oracle.coverage(s_np[0, h], perm, retain, k_min=w)
+            assert kb[h].item() == k_eta, (retain, h, kb[h].item(), k_eta)
+            kept = ki[ko[h].item():ko[h + 1].item()].cpu().numpy()
+            assert np.array_equal(kept, oracle.select(perm, k_eta))
+    # a caller budget below w keeps the first window keys; above it, the
+    # window plus the best of the rest
+    for bsel in [5, w, w + 37]:
+        bud = torch.full((H,), bsel, dtype=torch.int32, device=dev)
+        _, ko, ki = ck.select(spec, s, bud)
+        torch.cuda.synchronize()
+        for h in range(H):
+            perm = oracle.order(s_np[0, h], keep_window=w)
+            kept = ki[ko[h].item():ko[h + 1].item()].cpu().numpy()
+            assert np.array_equal(kept, oracle.select(perm, bsel)), (bsel, h)
