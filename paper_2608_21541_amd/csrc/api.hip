@@ -113,8 +113,10 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.nblk_max = (max_len + 255) / 256;
   P.nsub_max = (max_len + 15) / 16;
   P.bm_words = (max_len + 63) / 64;
-  P.nsplit = (max_len + 8191) / 8192;
-  if (P.nsplit > 64) P.nsplit = 64;
+  // tail gather: one workgroup per 2048 positions of the longest sequence
+  // (about 200 kept rows each at a tenth kept), at most 128 per unit
+  P.nsplit = (max_len + 2047) / 2048;
+  if (P.nsplit > 128) P.nsplit = 128;
   return CERTKV_OK;
 }
 
