@@ -65,6 +65,23 @@ __device__ __forceinline__ BestFB half_wave_min(double f, int b) {
   return BestFB{f, b};
 }
 
+// Lexicographic (f, b) minimum over `width` lanes (32: a half-wave, 64: the
+// wave), carrying the curve value c of the winning position.
+template <int WIDTH>
+__device__ __forceinline__ void lexmin_fbc(double& f, int& b, float& c) {
+#pragma unroll
+  for (int m = WIDTH / 2; m >= 1; m >>= 1) {
+    const double fo = __shfl_xor(f, m, 64);
+    const int bo = __shfl_xor(b, m, 64);
+    const float co = __shfl_xor(c, m, 64);
+    if (lex_less(fo, bo, f, b)) {
+      f = fo;
+      b = bo;
+      c = co;
+    }
+  }
+}
+
 __device__ __forceinline__ BestFB wave_lexmin(double f, int b) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -89,12 +106,14 @@ __device__ __forceinline__ double dval(uint64_t k) {
 }
 
 // Per-block statistics of the curves: minimum and maximum of c over each
-// 256-rank block, and the maximum marginal d(i) = c(i+1) - c(i) (fp64) over
-// the i of the block with i <= n-2.  One wave per block.
+// 256-rank block, the smallest position holding the minimum, and the maximum
+// marginal d(i) = c(i+1) - c(i) (fp64) over the i of the block with
+// i <= n-2.  One wave per block.
 __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st, int32_t nblk_max,
                                                                const float* __restrict__ curves,
                                                                float* __restrict__ cmin,
                                                                float* __restrict__ cmaxb,
+                                                               int32_t* __restrict__ cpos,
                                                                double* __restrict__ dmax) {
   const int per_unit = (nblk_max + 3) / 4;
   const int wb = blockIdx.x % per_unit;
@@ -115,29 +134,44 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
 #pragma unroll
   for (int e = 0; e < 5; ++e) c[e] = (i0 + e < n) ? ch[i0 + e] : 0.f;
   float mn = INFINITY, mx = -INFINITY;
+  int pmn = 0x7fffffff;
   double dm = -INFINITY;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     if (i0 + e < n) {
-      mn = fminf(mn, c[e]);
+      if (c[e] < mn) {
+        mn = c[e];
+        pmn = i0 + e;
+      }
       mx = fmaxf(mx, c[e]);
     }
     if (i0 + e <= n - 2) dm = fmax(dm, (double)c[e + 1] - (double)c[e]);
   }
-  mn = wave_min_f(mn);
+  // (min c, smallest position) over the wave
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float mo = __shfl_xor(mn, m, 64);
+    const int po = __shfl_xor(pmn, m, 64);
+    if (mo < mn || (mo == mn && po < pmn)) {
+      mn = mo;
+      pmn = po;
+    }
+  }
   mx = wave_max(mx);
   dm = wave_max(dm);
   if (lane == 0) {
     cmin[u * nblk_max + k] = mn;
     cmaxb[u * nblk_max + k] = mx;
+    cpos[u * nblk_max + k] = pmn;
     dmax[u * nblk_max + k] = dm;
   }
 }
 
 __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     Geo g, SeqTab st, const float* __restrict__ curves, const float* __restrict__ cmin,
-    const float* __restrict__ cmaxb, const double* __restrict__ dmax, int32_t nblk_max,
-    int32_t steps, int32_t* __restrict__ budgets, int64_t* __restrict__ stats) {
+    const float* __restrict__ cmaxb, const int32_t* __restrict__ cpos,
+    const double* __restrict__ dmax, int32_t nblk_max, int32_t steps,
+    int32_t* __restrict__ budgets, int64_t* __restrict__ stats) {
   // 64 KB of LDS: block minima + candidate lists during the bisection, the
   // block-level running maxima of the marginals during the repair.
   __shared__ __align__(16) unsigned char pool[kLdsItems * 8];
@@ -146,12 +180,17 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   double* pbm = reinterpret_cast<double*>(pool);
   __shared__ double fbest[64];
   __shared__ int32_t bbest[64], kstar[64];
+  __shared__ float cbest[64], cprev[64];  // curve values at bbest and bprev
+  __shared__ int32_t bprev[64];           // previous argmin (-1: none)
+  __shared__ int32_t mpos[kLdsItems];     // smallest position of each block's minimum
+  __shared__ float cres_c[kCandCap];
   __shared__ int32_t bcur[64], bhi[64];
   __shared__ double redf[kAllocWaves];
   __shared__ double cres_f[kCandCap];
   __shared__ int32_t cres_b[kCandCap];
   __shared__ int32_t ncand, scan_pos;
   __shared__ int64_t cnt_lt[64], cnt_le[64];
+  __shared__ int64_t cnt_j[kHeadGroup];  // per (threshold, head) counts of the repair search
   __shared__ float win[64][kRepairWin + 1];
 
   const int bl = blockIdx.x;
@@ -184,8 +223,10 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     for (int i = tid; i < H * nblk; i += kAllocThreads) {
       const int h = i / nblk, k = i % nblk;
       mcache[i] = cmin[unit_index(g, l, b, h) * nblk_max + k];
+      mpos[i] = cpos[unit_index(g, l, b, h) * nblk_max + k];
     }
   }
+  if (tid < 64) bprev[tid] = -1;
   __syncthreads();
   for (int w = 0; w < kAllocWaves; ++w) cm = fmax(cm, redf[w]);
   double lo = 0.0, hi = 2.0 * cm + 1.0;
@@ -283,7 +324,8 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     __syncthreads();
   };
 
-  // The same argmin with the block minima in LDS.
+  // The same argmin with the block minima in LDS, in rounds of at most
+  // kCandCap candidate blocks (used when one round cannot hold them all).
   //  1. per head, the block with the smallest bound is evaluated exactly
   //     (32 threads per head): an exact upper bound (f*, b*) of the minimum;
   //  2. every other block whose bound undercuts (f*, b*) is a candidate;
@@ -292,7 +334,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   //  3. per head, the smallest (f, b) over its candidates and (f*, b*).
   // Blocks left out cannot hold the answer (ties favour smaller b), so the
   // result is the full scan's.
-  auto evaluate_fast = [&](double lam, int32_t* out) {
+  auto evaluate_rounds = [&](double lam, int32_t* out) {
     best_bound(lam);
     if (tid == 0) scan_pos = 0;
     __syncthreads();
@@ -398,7 +440,165 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       __syncthreads();
       if (stop >= nitems) break;
     }
-    if (tid < H) out[tid] = bbest[tid];
+    if (tid < H) {
+      out[tid] = bbest[tid];
+      bprev[tid] = -1;
+    }
+    __syncthreads();
+  };
+
+  // The argmin with an upper bound that needs no global load: per head the
+  // best of (a) the first position of each block's minimum, for blocks whose
+  // minimum lies at or after b_min (an actual point of the curve, its value
+  // in LDS), and (b) the previous argmin with its curve value.  Every block
+  // whose bound undercuts it is a candidate, gathered in one sweep and
+  // evaluated one block per wave; if more than kCandCap qualify, the rounds
+  // above take over.  As there, blocks left out cannot hold the answer.
+  auto evaluate_fast = [&](double lam, int32_t* out) {
+    for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+      const int h = h0 + hg;
+      if (h < H) {
+        double f = INFINITY;
+        int bb = 0x7fffffff;
+        float cb = 0.f;
+        for (int k = kfirst + sub; k < nblk; k += 32) {
+          const int p = mpos[h * nblk + k];
+          if (p >= bmin) {
+            const float cv = mcache[h * nblk + k];
+            const double v = fma(lam, (double)p, (double)cv);
+            if (lex_less(v, p, f, bb)) {
+              f = v;
+              bb = p;
+              cb = cv;
+            }
+          }
+        }
+        if (sub == 0 && bprev[h] >= 0) {
+          const double v = fma(lam, (double)bprev[h], (double)cprev[h]);
+          if (lex_less(v, bprev[h], f, bb)) {
+            f = v;
+            bb = bprev[h];
+            cb = cprev[h];
+          }
+        }
+        lexmin_fbc<32>(f, bb, cb);
+        if (sub == 0) {
+          fbest[h] = f;
+          bbest[h] = bb;
+          cbest[h] = cb;
+        }
+      }
+    }
+    if (tid == 0) ncand = 0;
+    __syncthreads();
+    const int nitems = H * nblk;
+    for (int i0 = 0; i0 < nitems; i0 += kAllocThreads) {
+      const int i = i0 + tid;
+      bool take = false;
+      int h = 0, k = 0;
+      if (i < nitems) {
+        h = i / nblk;
+        k = i - h * nblk;
+        if (k >= kfirst) {
+          const int b0 = max(k * kBlk, bmin);
+          const double lb = fma(lam, (double)b0, (double)mcache[i]);
+          take = lex_less(lb, b0, fbest[h], bbest[h]);
+        }
+      }
+      const uint64_t m = __ballot(take);
+      int slot0 = 0;
+      if (lane == 0 && m) slot0 = atomicAdd(&ncand, __popcll(m));
+      slot0 = __shfl(slot0, 0, 64);
+      const int slot = slot0 + (int)count_below64(m);
+      if (take && slot < kCandCap) cand[slot] = (h << 16) | k;
+    }
+    __syncthreads();
+    const int C = ncand;
+    if (C > kCandCap) {
+      evaluate_rounds(lam, out);
+      return;
+    }
+    // evaluate: each wave takes runs of 8 consecutive candidates (all loads
+    // of a run in flight); the sweep lists them in (head, block) order, so a
+    // run mostly belongs to one head: lanes keep a running best over the
+    // run's positions and the wave reduces once per head change, recording
+    // the result at that head's last candidate of the run (the others get
+    // +inf)
+    constexpr int QB = 8;
+    for (int c0 = wave * QB; c0 < C; c0 += QB * kAllocWaves) {
+      float cv[QB][kBlk / 64];
+      int it[QB];
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        const int c = c0 + q;
+        it[q] = c < C ? cand[c] : -1;
+        const int hq = it[q] < 0 ? 0 : (it[q] >> 16), kq = it[q] < 0 ? 0 : (it[q] & 0xffff);
+        const float* ch = curves + lht_base(g, l, hq, tok0);
+#pragma unroll
+        for (int e = 0; e < kBlk / 64; ++e) {
+          const int x = kq * kBlk + lane + 64 * e;
+          cv[q][e] = (it[q] >= 0 && x >= bmin && x <= n - 1) ? ch[x] : 0.f;
+        }
+      }
+      double f = INFINITY;
+      int bb = 0x7fffffff;
+      float cb = 0.f;
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        if (it[q] < 0) break;
+        const int kq = it[q] & 0xffff;
+#pragma unroll
+        for (int e = 0; e < kBlk / 64; ++e) {
+          const int x = kq * kBlk + lane + 64 * e;
+          if (x >= bmin && x <= n - 1) {
+            const double v = fma(lam, (double)x, (double)cv[q][e]);
+            if (lex_less(v, x, f, bb)) {
+              f = v;
+              bb = x;
+              cb = cv[q][e];
+            }
+          }
+        }
+        const bool last = q + 1 == QB || it[q + 1] < 0 || (it[q + 1] >> 16) != (it[q] >> 16);
+        if (last) {
+          lexmin_fbc<64>(f, bb, cb);
+          if (lane == 0) {
+            cres_f[c0 + q] = f;
+            cres_b[c0 + q] = bb;
+            cres_c[c0 + q] = cb;
+          }
+          f = INFINITY;
+          bb = 0x7fffffff;
+          cb = 0.f;
+        } else if (lane == 0) {
+          cres_f[c0 + q] = INFINITY;
+          cres_b[c0 + q] = 0x7fffffff;
+        }
+      }
+    }
+    __syncthreads();
+    // per head: fold the candidates' minima into (f*, b*), 32 threads a head
+    for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
+      const int h = h0 + hg;
+      if (h < H) {
+        double f = fbest[h];
+        int bb = bbest[h];
+        float cb = cbest[h];
+        for (int c = sub; c < C; c += 32) {
+          if ((cand[c] >> 16) == h && lex_less(cres_f[c], cres_b[c], f, bb)) {
+            f = cres_f[c];
+            bb = cres_b[c];
+            cb = cres_c[c];
+          }
+        }
+        lexmin_fbc<32>(f, bb, cb);
+        if (sub == 0) {
+          out[h] = bb;
+          bprev[h] = bb;
+          cprev[h] = cb;
+        }
+      }
+    }
     __syncthreads();
   };
   auto evaluate = [&](double lam, int32_t* out) {
@@ -472,7 +672,15 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
 
   if (R > 0 && fast) {
     // pbm[h*nblk + k] = running max of d_h over [s_h, end of block k] for the
-    // blocks k >= block of s_h (s_h = bhi[h]); -inf before it.
+    // blocks k >= block of s_h (s_h = bhi[h]); -inf before it.  The block
+    // maxima come into LDS with all threads; each head's running maximum is
+    // then a prefix maximum over its blocks by one half-wave (a run of
+    // blocks per thread, then a scan of the runs).
+    for (int i = tid; i < H * nblk; i += kAllocThreads) {
+      const int h = i / nblk, k = i - h * nblk;
+      pbm[i] = dmax[unit_index(g, l, b, h) * nblk_max + k];
+    }
+    __syncthreads();
     for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
       const int h = h0 + hg;
       if (h < H) {
@@ -486,24 +694,70 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         }
 #pragma unroll
         for (int m = 16; m >= 1; m >>= 1) dm = fmax(dm, __shfl_xor(dm, m, 64));
-        if (sub == 0) {
-          double run = dm;
-          for (int k = 0; k < nblk; ++k) {
-            if (k > ks && k <= kmax) run = fmax(run, dmax[unit_index(g, l, b, h) * nblk_max + k]);
-            pbm[h * nblk + k] = (k < ks || s > n - 2) ? -INFINITY : run;
-          }
+        // block values: the partial first block, then the block maxima up to
+        // the last block holding an increment; -inf elsewhere
+        double* ph = pbm + h * nblk;
+        const bool none = s > n - 2;
+        auto val = [&](int k) -> double {
+          if (none || k < ks) return -INFINITY;
+          if (k == ks) return dm;
+          return k <= kmax ? ph[k] : -INFINITY;
+        };
+        const int per = (nblk + 31) / 32;
+        const int k0 = sub * per, k1 = min(nblk, k0 + per);
+        double run = -INFINITY;
+        for (int k = k0; k < k1; ++k) run = fmax(run, val(k));
+        // exclusive prefix maximum of the runs over the half-wave
+        double incl = run;
+#pragma unroll
+        for (int off = 1; off < 32; off <<= 1) {
+          const double y = __shfl_up(incl, off, 32);
+          if (sub >= off) incl = fmax(incl, y);
+        }
+        double acc = __shfl_up(incl, 1, 32);
+        if (sub == 0) acc = -INFINITY;
+        // each thread reads and rewrites only its own blocks, each block's
+        // value read just before it is overwritten
+        for (int k = k0; k < k1; ++k) {
+          acc = fmax(acc, val(k));
+          ph[k] = (none || k < ks) ? -INFINITY : acc;
         }
       }
     }
     __syncthreads();
-    // smallest key x in [-inf, +inf] with count(P <= x) >= R, by bisection
-    // over the ordered bit patterns (count(P <= +inf) covers every increment)
+    // smallest key x in [-inf, +inf] with count(P <= x) >= R, by a (J+1)-ary
+    // search over the ordered bit patterns (count(P <= +inf) covers every
+    // increment): each step counts at J interior points of [klo, khi) at once,
+    // one half-wave per (point, head).
     uint64_t klo = dkey(-INFINITY), khi = dkey(INFINITY);
+    const int J = kHeadGroup / H < 1 ? 1 : (kHeadGroup / H > 7 ? 7 : kHeadGroup / H);
+    // interior point j: klo + floor(span (j+1) / (J+1)), < khi, without overflow
+    auto point = [&](uint64_t lo_k, uint64_t span, int j) -> uint64_t {
+      const uint64_t q = span / (uint64_t)(J + 1), r = span % (uint64_t)(J + 1);
+      return lo_k + q * (uint64_t)(j + 1) + (r * (uint64_t)(j + 1)) / (uint64_t)(J + 1);
+    };
     while (klo < khi) {
-      const uint64_t mid = klo + ((khi - klo) >> 1);
-      const int64_t c = total_count(dval(mid), true, cnt_le);
-      if (c >= R) khi = mid;
-      else klo = mid + 1;
+      const uint64_t span = khi - klo;
+      if (hg < J * H) {
+        const int j = hg / H, h = hg % H;
+        const int64_t c = count_head(h, dval(point(klo, span, j)), true);
+        if (sub == 0) cnt_j[hg] = c;
+      }
+      __syncthreads();
+      int first = J;  // first point whose count reaches R
+      for (int j = J - 1; j >= 0; --j) {
+        int64_t c = 0;
+        for (int h = 0; h < H; ++h) c += cnt_j[j * H + h];
+        if (c >= R) first = j;
+      }
+      __syncthreads();
+      if (first < J) {
+        const uint64_t nlo = first > 0 ? point(klo, span, first - 1) + 1 : klo;
+        khi = point(klo, span, first);
+        klo = nlo;
+      } else {
+        klo = point(klo, span, J - 1) + 1;
+      }
     }
     const double pstar = dval(klo);
     total_count(pstar, false, cnt_lt);
@@ -563,10 +817,10 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) {
   const int per_unit = (a.nblk_max + 3) / 4;
   CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
-                dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.dmax);
+                dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.cpos, a.dmax);
   CERTKV_LAUNCH("allocate", allocate_kernel, dim3(st.count, a.g.L), dim3(kAllocThreads), 0, s, a.g,
-                st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb, (const double*)a.dmax,
-                a.nblk_max, a.steps, a.budgets, a.repairs);
+                st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb, (const int32_t*)a.cpos,
+                (const double*)a.dmax, a.nblk_max, a.steps, a.budgets, a.repairs);
   return CERTKV_OK;
 }
 

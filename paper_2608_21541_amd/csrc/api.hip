@@ -203,6 +203,7 @@ struct Bufs {
   float* curves = nullptr;
   float* cmin = nullptr;
   float* cmaxb = nullptr;
+  int32_t* cpos = nullptr;
   double* dmax = nullptr;
   double* vsum = nullptr;
   int64_t* repairs = nullptr;
@@ -253,6 +254,7 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
   if (need & (NEED_CURVES | NEED_MINMAX)) {
     b->cmin = w.take<float>((size_t)P.U * P.nblk_max);
     b->cmaxb = w.take<float>((size_t)P.U * P.nblk_max);
+    b->cpos = w.take<int32_t>((size_t)P.U * P.nblk_max);
     b->dmax = w.take<double>((size_t)P.U * P.nblk_max);
     b->repairs = w.take<int64_t>((size_t)P.g.L * P.g.B * 3);
   }
@@ -371,6 +373,7 @@ static certkv_status do_allocate(const Plan& P, const float* curves, const int32
   a.curves = curves;
   a.cmin = w.cmin;
   a.cmaxb = w.cmaxb;
+  a.cpos = w.cpos;
   a.dmax = w.dmax;
   a.nblk_max = P.nblk_max;
   a.steps = steps;

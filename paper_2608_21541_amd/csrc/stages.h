@@ -56,6 +56,7 @@ struct AllocArgs {
   const float* curves;
   float* cmin;      // [U][nblk_max] block minima of c
   float* cmaxb;     // [U][nblk_max] block maxima of c
+  int32_t* cpos;    // [U][nblk_max] smallest position of the block minimum
   double* dmax;     // [U][nblk_max] block maxima of c(i+1) - c(i)
   int32_t nblk_max;
   int32_t steps;
