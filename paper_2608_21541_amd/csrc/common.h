@@ -64,6 +64,10 @@ __device__ __forceinline__ uint2 buf_load_u64(BufRsrc r, uint32_t off) {
   auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
   return make_uint2(v[0], v[1]);
 }
+__device__ __forceinline__ uint4 buf_load_u128(BufRsrc r, uint32_t off) {
+  auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
 // The same loads with a wave-uniform byte offset `soff` (held in the
 // instruction's scalar offset; only `off` is range-checked, so the caller
 // keeps soff + off inside the buffer).
