@@ -78,7 +78,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
     double* __restrict__ ssum_out) {
   __shared__ uint32_t hist[4][256];
   __shared__ uint32_t bucket[256];      // running start of each digit's bucket
-  __shared__ uint32_t tile_tot[256];    // digit counts of the tile
+  __shared__ uint32_t tile_tot[2][256]; // digit counts of the tile, by tile parity
   __shared__ uint32_t tile_start[256];  // digit-major start inside the tile
   __shared__ uint32_t wave_cnt[kSortWaves][256];
   __shared__ uint32_t stage_key[kSortTile];
@@ -99,20 +99,25 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
   const int wkeep = n - g.keep_w;
 
   for (int i = threadIdx.x; i < 4 * 256; i += kSortThreads) (&hist[0][0])[i] = 0u;
-  if (threadIdx.x < 256) tile_tot[threadIdx.x] = 0u;
+  for (int i = threadIdx.x; i < 2 * 256; i += kSortThreads) (&tile_tot[0][0])[i] = 0u;
   __syncthreads();
 
-  // Counting pass: four digit histograms and the fp64 sum of (s)_+.
+  // Counting pass: four digit histograms and the fp64 sum of (s)_+.  The
+  // next tile's scores are loaded while the current one is counted.
   {
     double psum = 0.0;
-    for (int t0 = 0; t0 < n; t0 += kSortTile) {
-      float sv[kSortRounds];
+    auto load_scores = [&](int t0, float (&x)[kSortRounds]) {
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
-        const float x = scores[base + min(e, n - 1)];  // clamped: no branch around the load
-        sv[r] = e < n ? x : 0.f;
+        const float v = scores[base + min(e, n - 1)];  // clamped: no branch around the load
+        x[r] = e < n ? v : 0.f;
       }
+    };
+    float sv[kSortRounds], sn[kSortRounds];
+    load_scores(0, sv);
+    for (int t0 = 0; t0 < n; t0 += kSortTile) {
+      if (t0 + kSortTile < n) load_scores(t0 + kSortTile, sn);
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
@@ -121,9 +126,23 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         const uint32_t key = e >= wkeep ? 0u : desc_key(sv[r]);
         if (valid) {
 #pragma unroll
-          for (int p = 0; p < 4; ++p) atomicAdd(&hist[p][(key >> (8 * p)) & 255u], 1u);
+          for (int p = 0; p < 3; ++p) atomicAdd(&hist[p][(key >> (8 * p)) & 255u], 1u);
+        }
+        // The top digit holds the score's sign and upper exponent bits, so a
+        // wave sees few distinct values: one atomic per distinct digit
+        // instead of one per lane on a handful of addresses.
+        const uint32_t d3 = key >> 24;
+        uint64_t todo = __ballot(valid);
+        while (todo) {
+          const int leader = __builtin_ctzll(todo);
+          const uint32_t dl = __builtin_amdgcn_readlane(d3, leader);
+          const uint64_t same = __ballot(d3 == dl) & todo;
+          if (lane == leader) atomicAdd(&hist[3][dl], (uint32_t)__popcll(same));
+          todo &= ~same;
         }
       }
+#pragma unroll
+      for (int r = 0; r < kSortRounds; ++r) sv[r] = sn[r];
     }
     psum = wave_sum(psum);
     if (lane == 0) dred[wave] = psum;
@@ -170,6 +189,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
     int32_t val[kSortRounds], nval[kSortRounds];
     load(0, key, val);
     for (int t0 = 0; t0 < n; t0 += kSortTile) {
+      const int tp = (t0 / kSortTile) & 1;  // tile parity
 #pragma unroll
       for (int j = 0; j < 4; ++j) wave_cnt[wave][lane * 4 + j] = 0u;
       if (t0 + kSortTile < n) load(t0 + kSortTile, nkey, nval);  // prefetch
@@ -188,15 +208,22 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         if (ok && below == 0) {
           const uint32_t c = (uint32_t)__popcll(peers);
           wave_cnt[wave][dg] = pre + c;
-          atomicAdd(&tile_tot[dg], c);
+          atomicAdd(&tile_tot[tp][dg], c);
         }
       }
       __syncthreads();
-      // per digit: exclusive scan over the waves (waves 1-4) and over the
-      // digits of the tile counts (wave 0), concurrently
+      // per digit: exclusive scan over the waves (waves 1-4), over the digits
+      // of the tile counts (wave 0) and the previous tile's advance of the
+      // bucket offsets (waves 5-8; every wave is past that tile's writes),
+      // concurrently.  The previous tile's counts are cleared for the tile
+      // after this one.
       if (wave == 0) {
-        for (int j = 0; j < 4; ++j) tile_start[lane * 4 + j] = tile_tot[lane * 4 + j];
+        for (int j = 0; j < 4; ++j) tile_start[lane * 4 + j] = tile_tot[tp][lane * 4 + j];
         wave_scan256(tile_start, lane);
+      } else if (threadIdx.x >= 320 && threadIdx.x < 320 + 256) {
+        const int d = threadIdx.x - 320;
+        if (t0 > 0) bucket[d] += tile_tot[tp ^ 1][d];
+        tile_tot[tp ^ 1][d] = 0u;
       } else if (threadIdx.x < 256 + 64) {
         const int d = threadIdx.x - 64;
         uint32_t c[kSortWaves];
@@ -248,17 +275,14 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
           }
         }
       }
-      __syncthreads();
-      if (threadIdx.x < 256) {
-        bucket[threadIdx.x] += tile_tot[threadIdx.x];
-        tile_tot[threadIdx.x] = 0u;
-      }
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         key[r] = nkey[r];
         val[r] = nval[r];
       }
     }
+    // the last tile's counts (the other parity is already clear)
+    if (threadIdx.x < 256) tile_tot[((n - 1) / kSortTile) & 1][threadIdx.x] = 0u;
     __syncthreads();  // the pass's output is the next pass's input
   };
   pass(std::integral_constant<int, 0>());
