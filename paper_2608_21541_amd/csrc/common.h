@@ -68,6 +68,9 @@ __device__ __forceinline__ uint4 buf_load_u128(BufRsrc r, uint32_t off) {
   auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
+__device__ __forceinline__ void buf_store_u32(BufRsrc r, uint32_t off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, 0);
+}
 // The same loads with a wave-uniform byte offset `soff` (held in the
 // instruction's scalar offset; only `off` is range-checked, so the caller
 // keeps soff + off inside the buffer).

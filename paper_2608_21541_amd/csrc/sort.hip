@@ -33,15 +33,22 @@ constexpr int kSortRounds = 8;
 constexpr int kSortTile = kSortThreads * kSortRounds;  // 8192 elements
 
 // Lanes of the wave whose 8-bit digit equals this lane's (among `valid`).
+// Per bit, the lanes agreeing with this lane are the ballot of the bit when
+// it is set here and its complement when it is clear: ballot ^ m with m the
+// bit sign-extended from ~digit (0 or all ones), which keeps the selection a
+// per-lane xor of a wave-uniform mask.
 __device__ __forceinline__ uint64_t match_digit(uint32_t digit, bool valid) {
-  uint64_t peers = __ballot(valid);
+  const uint64_t v = __ballot(valid);
+  uint32_t plo = (uint32_t)v, phi = (uint32_t)(v >> 32);
+  const uint32_t nd = ~digit;
 #pragma unroll
   for (int bit = 0; bit < 8; ++bit) {
-    const bool set = (digit >> bit) & 1u;
-    const uint64_t bb = __ballot(valid && set);
-    peers &= set ? bb : ~bb;
+    const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)nd, bit, 1);
+    const uint64_t bb = __ballot(m == 0u);
+    plo &= (uint32_t)bb ^ m;
+    phi &= (uint32_t)(bb >> 32) ^ m;
   }
-  return peers;
+  return ((uint64_t)phi << 32) | plo;
 }
 
 __device__ __forceinline__ uint32_t count_below(uint64_t mask) {
@@ -168,20 +175,27 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
       for (int j = 0; j < 4; ++j) bucket[lane * 4 + j] = hist[p][lane * 4 + j];
       wave_scan256(bucket, lane);
     }
+    // Loads through range-checked buffers: elements at or beyond n read as
+    // zero, so no clamp or branch sits around them (the asm keeps the score
+    // loads from being sunk into the window test).
+    const BufRsrc kin_r = make_rsrc(p == 0 ? (const void*)(scores + base) : (const void*)(kin + base),
+                                    (uint32_t)n * 4u);
+    const BufRsrc vin_r = make_rsrc(vin + base, (uint32_t)n * 4u);
+    const BufRsrc kout_r = make_rsrc(kout + base, (uint32_t)n * 4u);
+    const BufRsrc vout_r = make_rsrc(vout + base, (uint32_t)n * 4u);
     auto load = [&](int t0, uint32_t (&key)[kSortRounds], int32_t (&val)[kSortRounds]) {
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
-        const bool ok = e < n;
+        const uint32_t off = (uint32_t)e * 4u;
         if (p == 0) {
-          const float x = scores[base + min(e, n - 1)];
-          key[r] = e >= wkeep ? 0u : desc_key(ok ? x : 0.f);
+          uint32_t xb = buf_load_u32(kin_r, off);
+          __asm__ volatile("" : "+v"(xb));
+          key[r] = e >= wkeep ? 0u : desc_key(__uint_as_float(xb));
           val[r] = e;
         } else {
-          const uint32_t kx = kin[base + min(e, n - 1)];
-          const int32_t vx = vin[base + min(e, n - 1)];
-          key[r] = ok ? kx : 0u;
-          val[r] = ok ? vx : 0;
+          key[r] = buf_load_u32(kin_r, off);
+          val[r] = (int32_t)buf_load_u32(vin_r, off);
         }
       }
     };
@@ -269,9 +283,9 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
 #pragma unroll
         for (int r = 0; r < kSortRounds; ++r) {
           const int i = threadIdx.x + r * kSortThreads;
-          if (i < cnt && dst[r] < (uint32_t)n) {  // always true when the counts are right
-            kout[base + dst[r]] = kk[r];
-            vout[base + dst[r]] = vv[r];
+          if (i < cnt) {
+            buf_store_u32(kout_r, dst[r] * 4u, kk[r]);
+            buf_store_u32(vout_r, dst[r] * 4u, (uint32_t)vv[r]);
           }
         }
       }
