@@ -54,8 +54,10 @@ struct Plan {
   int64_t U;         // units
   int max_len;
   int M;             // window rows per unit
-  int kpb;           // keys per scoring block
-  int nkb_max;       // scoring blocks per unit (max over sequences)
+  int kpb;           // keys per scoring block, pass 1
+  int nkb_max;       // pass-1 scoring blocks per unit (max over sequences)
+  int kpb2;          // keys per scoring block, pass 2
+  int nkb2_max;      // pass-2 scoring blocks per unit
   int nblk_max;      // 256-rank allocation blocks per unit
   int nsub_max;      // 16-rank allocation sub-blocks per unit
   int bm_words;      // 64-bit bitmap words per unit
@@ -103,13 +105,25 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.max_len = max_len;
   P.M = M;
   P.cu = cu;
-  int kpb = 256;
+  // Scoring blocks: as long as the grid keeps about four workgroups per
+  // resident slot (pass 1 holds two 8-wave workgroups per CU, pass 2 with
+  // its key-sum registers one), larger blocks amortize the staging of the
+  // window queries and the per-block reduction.
+  int kpb = 256, kpb2 = 256;
   if (P.dtype == CERTKV_BF16) {
-    kpb = 512;
-    while (kpb < 4096 && P.U * ((max_len + 2 * kpb - 1) / (2 * kpb)) >= 2048) kpb *= 2;
+    constexpr int64_t kCUs = 256;
+    auto grow = [&](int64_t min_wgs) {
+      int k = 512;
+      while (k < 65536 && P.U * ((max_len + 2 * k - 1) / (2 * k)) >= min_wgs) k *= 2;
+      return k;
+    };
+    kpb = grow(4 * 2 * kCUs);
+    kpb2 = grow(4 * kCUs);
   }
   P.kpb = kpb;
   P.nkb_max = (max_len + kpb - 1) / kpb;
+  P.kpb2 = kpb2;
+  P.nkb2_max = (max_len + kpb2 - 1) / kpb2;
   P.nblk_max = (max_len + 255) / 256;
   P.nsub_max = (max_len + 15) / 16;
   P.bm_words = (max_len + 63) / 64;
@@ -235,7 +249,7 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
   if (need & NEED_SCORE) {
     b->part = w.take<float2>((size_t)P.U * P.nkb_max * P.M);
     b->lse2 = w.take<float>((size_t)P.U * P.M);
-    b->kpart = w.take<float>((size_t)P.U * P.nkb_max * P.g.D);
+    b->kpart = w.take<float>((size_t)P.U * P.nkb2_max * P.g.D);
     b->flag = w.take<int32_t>((size_t)P.U);
   }
   if (need & NEED_KSUM) {
@@ -326,6 +340,8 @@ static certkv_status do_score(const Plan& P, certkv_tensor q, certkv_tensor k,
   a.flag = w.flag;
   a.keys_per_block = P.dtype == CERTKV_BF16 ? P.kpb : 256;
   a.nkb_max = P.dtype == CERTKV_BF16 ? P.nkb_max : (P.max_len + 255) / 256;
+  a.keys_per_block2 = P.dtype == CERTKV_BF16 ? P.kpb2 : 256;
+  a.nkb2_max = P.dtype == CERTKV_BF16 ? P.nkb2_max : (P.max_len + 255) / 256;
   for (const SeqTab& t : make_tabs(P, nullptr, 0.f)) {
     int ml = 0;
     for (int i = 0; i < t.count; ++i) ml = t.len[i] > ml ? t.len[i] : ml;

@@ -727,7 +727,9 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                                  hipStream_t s) {
   const Geo& g = a.g;
   const int nkb = (max_len + a.keys_per_block - 1) / a.keys_per_block;
+  const int nkb2 = (max_len + a.keys_per_block2 - 1) / a.keys_per_block2;
   dim3 grid(nkb, g.H * st.count, g.L);
+  dim3 grid2(nkb2, g.H * st.count, g.L);
   size_t smem = score_smem_bytes(g, CERTKV_BF16);
   static bool attr_set = false;
   if (!attr_set) {
@@ -763,18 +765,18 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                   a.flag, 1);
   }
   if (a.ksum)
-    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid, dim3(kScoreThreads),
-                  smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
-                  a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2,
-                  a.scores, a.kpart);
+    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid2,
+                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                  (const float*)a.lse2, a.scores, a.kpart);
   else
-    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, false>), grid, dim3(kScoreThreads),
-                  smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k, a.k.s_layer,
-                  a.k.s_token, a.k.s_head, a.keys_per_block, a.nkb_max, (const float*)a.lse2,
-                  a.scores, (float*)nullptr);
+    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, false>), grid2,
+                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                  (const float*)a.lse2, a.scores, (float*)nullptr);
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
-                  s, g, st, a.keys_per_block, a.nkb_max, (const float*)a.kpart, a.ksum);
+                  s, g, st, a.keys_per_block2, a.nkb2_max, (const float*)a.kpart, a.ksum);
   if (a.lse_out)
     CERTKV_LAUNCH("score_lse_export", lse_io_kernel<false>, dim3(g.H * st.count, g.L), dim3(256), 0,
                   s, g, st, (const float*)nullptr, a.lse2, a.lse_out);

@@ -19,8 +19,10 @@ struct ScoreArgs {
   int32_t* flag;  // [U] units whose shift-free row sums left the safe range
   const float* lse_in;  // optional caller row log-sum-exp [L][B*w][Hq]
   float* lse_out;       // optional row log-sum-exp out, same layout
-  int32_t keys_per_block;
+  int32_t keys_per_block;   // pass 1 (and its partials)
   int32_t nkb_max;
+  int32_t keys_per_block2;  // pass 2 (and its key-sum partials)
+  int32_t nkb2_max;
 };
 // Query tiles of 32 rows covering the M window rows, rounded up to a power of two.
 inline int score_nqt(int M) {
