@@ -259,22 +259,37 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       }
     }
     __syncthreads();
+    // Exclusive prefix over the waves of the totals, from the chunk carry, in
+    // place: one (lane, field) column per thread, added in wave order.
+    {
+      constexpr int C = kLPR * NR;
+      if (threadIdx.x < C) {
+        const int col = threadIdx.x;
+        double* t = &tR[0][0][0];
+        double run = (&cR[par][0][0])[col];
+#pragma unroll
+        for (int w0 = 0; w0 < kCurveWaves; w0 += 4) {
+          double x[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) x[j] = t[(w0 + j) * C + col];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            t[(w0 + j) * C + col] = run;
+            run += x[j];
+          }
+        }
+      }
+    }
+    __syncthreads();
     // carry of this sub-range: chunk carry + totals of the waves above it
     // (+ the upper half of its own wave for the lower half)
     double W[DP], q, m;
     {
-      const double* c = cR[par][li];
+      const double* c = tR[wave][li];
 #pragma unroll
       for (int t = 0; t < DP; ++t) W[t] = c[t];
       q = c[DP];
       m = c[DP + 1];
-      for (int w2 = 0; w2 < wave; ++w2) {
-        const double* x = tR[w2][li];
-#pragma unroll
-        for (int t = 0; t < DP; ++t) W[t] += x[t];
-        q += x[DP];
-        m += x[DP + 1];
-      }
       if (hf) {
         const double* x = uR[wave][li];
 #pragma unroll
