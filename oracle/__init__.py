@@ -56,6 +56,8 @@ def lib():
         L.ora_select.argtypes = [_i64, _p, _i64, _p]
         L.ora_coverage.argtypes = [_i64, _p, _p, _dbl, _i64, _p]
         L.ora_tail.argtypes = [_i64, _i32, _p, _p, _i64, _p, _p, _p, _p, _p]
+        L.ora_decode.argtypes = [_i64, _i32, _i32, _p, _p, _p, _dbl, _p, _p]
+        L.ora_lift_terms.argtypes = [_i64, _i32, _p, _p, _p, _p, _p, _p, _p, _dbl, _p]
         L.ora_f32_to_bf16.argtypes = [ctypes.c_float]
         L.ora_f32_to_bf16.restype = ctypes.c_uint16
         L.ora_row_error.argtypes = [_i64, _i32, _p, _p, _p, _p]
@@ -244,3 +246,32 @@ def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32
     return dict(s=s, s32=s32, perm=perm, c32=c32, budgets=b,
                 kept=[kept[kept_off[h]:kept_off[h + 1]].copy() for h in range(H)],
                 k_star=ks, v_star=vs, tail_mass=m, repairs=int(rep[0]))
+
+
+def decode(q, kp, vp, scale):
+    """Attention of query rows q [m][d] over a packed segment (kept rows and
+    the slot row, kp/vp [nk][d]) with the plain softmax of Section 4.1's
+    live rows: returns (out [m][d], lse [m]) in fp64."""
+    q = _f64(np.atleast_2d(q))
+    kp, vp = _f64(kp), _f64(vp)
+    m, d = q.shape
+    out = np.zeros((m, d))
+    lse = np.zeros(m)
+    _check(lib().ora_decode(kp.shape[0], m, d, _ptr(q), _ptr(kp), _ptr(vp), float(scale),
+                            _ptr(out), _ptr(lse)), "decode")
+    return out, lse
+
+
+def lift_terms(q, k, v, kept_mask, r, kslot, vslot, scale):
+    """Terms of the future-query lift theorem for one query row q [d] over the
+    original keys k, v [n][d] with retained set kept_mask and slot (kslot,
+    vslot), the slot value being sum_T r_j v_j: a dict with p, q (slot
+    weight), l1 = ||a - r||_1, lam_T, z_slot, v_max and err = ||O - Ohat||_2."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    kept = np.ascontiguousarray(kept_mask, dtype=np.uint8)
+    r, kslot, vslot = _f64(r), _f64(kslot), _f64(vslot)
+    n, d = k.shape
+    out = np.zeros(7)
+    _check(lib().ora_lift_terms(n, d, _ptr(q), _ptr(k), _ptr(v), _ptr(kept), _ptr(r),
+                                _ptr(kslot), _ptr(vslot), float(scale), _ptr(out)), "lift_terms")
+    return dict(zip(["p", "q", "l1", "lam_T", "z_slot", "v_max", "err"], out.tolist()))

@@ -550,3 +550,119 @@ int ora_num_threads(void) {
   return 1;
 #endif
 }
+
+/* ------------------------------------------------------------------------ */
+/* Decode over the packed cache.  Section 4.1: after eviction each head keeps
+ * its b_h real tokens and one charged centroid pair (k*, v*), and a later
+ * query attends over these b_h + 1 rows as ordinary keys; the plain slot
+ * carries no logit bias.  For query row r:
+ *   z_i = scale <q_r, k_i>,  out_r = sum_i softmax(z)_i v_i,
+ *   lse_r = log sum_i exp z_i  (evaluated with the maximum factored out).
+ *   q [m][d], kp [nk][d], vp [nk][d], out [m][d], lse [m] or NULL. */
+int ora_decode(int64_t nk, int32_t m, int32_t d, const double* q, const double* kp,
+               const double* vp, double scale, double* out, double* lse) {
+  if (nk < 1 || m < 0 || d < 1) return ORA_EINVAL;
+  double* z = (double*)malloc((size_t)nk * sizeof(double));
+  if (!z) return ORA_ENOMEM;
+  int err = ORA_OK;
+  for (int32_t r = 0; r < m; ++r) {
+    double zmax = -INFINITY;
+    for (int64_t i = 0; i < nk; ++i) {
+      double dot = 0.0;
+      for (int32_t t = 0; t < d; ++t) dot += q[(int64_t)r * d + t] * kp[i * d + t];
+      z[i] = scale * dot;
+      if (isnan(z[i])) err = ORA_ENONFINITE;
+      if (z[i] > zmax) zmax = z[i];
+    }
+    double zsum = 0.0;
+    for (int64_t i = 0; i < nk; ++i) zsum += exp(z[i] - zmax);
+    for (int32_t t = 0; t < d; ++t) out[(int64_t)r * d + t] = 0.0;
+    for (int64_t i = 0; i < nk; ++i) {
+      const double a = exp(z[i] - zmax) / zsum;
+      for (int32_t t = 0; t < d; ++t) out[(int64_t)r * d + t] += a * vp[i * d + t];
+    }
+    if (lse) lse[r] = zmax + log(zsum);
+  }
+  free(z);
+  return err;
+}
+
+/* Theorem "future-query lift and summary mismatch" (section "Scoped
+ * guarantees behind CertKV"): one future query row over the original n keys,
+ * split into the retained set S (kept[j] != 0) and the evicted set T, with a
+ * slot whose value is v* = sum_T r_j v_j.
+ *   A     exact attention over S u T, O = sum_j A_j v_j;
+ *   Ahat  attention over S u {slot}, slot logit z* = scale <q, k*>,
+ *         Ohat = sum_S Ahat_i v_i + Ahat_* v*.
+ *   out[0] p = A(T)      out[1] q = Ahat_*
+ *   out[2] ||a - r||_1 with a = A_T / p (0 when p = 0)
+ *   out[3] Lambda_T = log sum_T exp z_j (-inf for an empty T)
+ *   out[4] z*            out[5] V_max = max_j ||v_j||_2 over S u T
+ *   out[6] ||O - Ohat||_2
+ * The theorem bounds out[6] by V_max (2 |p - q| + min(p, q) ||a - r||_1) and
+ * |p - q| by tanh(|Lambda_T - z*| / 4). */
+int ora_lift_terms(int64_t n, int32_t d, const double* q, const double* k, const double* v,
+                   const uint8_t* kept, const double* r, const double* kslot,
+                   const double* vslot, double scale, double* out) {
+  if (n < 1 || d < 1) return ORA_EINVAL;
+  double* z = (double*)malloc((size_t)n * sizeof(double));
+  double* O = (double*)calloc((size_t)d, sizeof(double));
+  double* Oh = (double*)calloc((size_t)d, sizeof(double));
+  if (!z || !O || !Oh) {
+    free(z);
+    free(O);
+    free(Oh);
+    return ORA_ENOMEM;
+  }
+  double zs = 0.0;
+  for (int32_t t = 0; t < d; ++t) zs += q[t] * kslot[t];
+  zs *= scale;
+  double zmax = zs, vmax = 0.0;
+  for (int64_t j = 0; j < n; ++j) {
+    double dot = 0.0, vv = 0.0;
+    for (int32_t t = 0; t < d; ++t) {
+      dot += q[t] * k[j * d + t];
+      vv += v[j * d + t] * v[j * d + t];
+    }
+    z[j] = scale * dot;
+    if (z[j] > zmax) zmax = z[j];
+    if (sqrt(vv) > vmax) vmax = sqrt(vv);
+  }
+  double ZS = 0.0, ZT = 0.0;
+  for (int64_t j = 0; j < n; ++j) {
+    const double e = exp(z[j] - zmax);
+    if (kept[j])
+      ZS += e;
+    else
+      ZT += e;
+  }
+  const double es = exp(zs - zmax);
+  const double Z = ZS + ZT, Zh = ZS + es;
+  const double p = ZT / Z, qs = es / Zh;
+  double l1 = 0.0;
+  for (int64_t j = 0; j < n; ++j) {
+    const double e = exp(z[j] - zmax);
+    const double A = e / Z;
+    for (int32_t t = 0; t < d; ++t) O[t] += A * v[j * d + t];
+    if (kept[j]) {
+      const double Ah = e / Zh;
+      for (int32_t t = 0; t < d; ++t) Oh[t] += Ah * v[j * d + t];
+    } else if (p > 0.0) {
+      l1 += fabs(A / p - r[j]);
+    }
+  }
+  for (int32_t t = 0; t < d; ++t) Oh[t] += qs * vslot[t];
+  double err2 = 0.0;
+  for (int32_t t = 0; t < d; ++t) err2 += (O[t] - Oh[t]) * (O[t] - Oh[t]);
+  out[0] = p;
+  out[1] = qs;
+  out[2] = l1;
+  out[3] = ZT > 0.0 ? zmax + log(ZT) : -INFINITY;
+  out[4] = zs;
+  out[5] = vmax;
+  out[6] = sqrt(err2);
+  free(z);
+  free(O);
+  free(Oh);
+  return ORA_OK;
+}
