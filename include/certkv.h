@@ -308,6 +308,30 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
                               const certkv_outputs* out, void* ws,
                               size_t ws_bytes, void* stream);
 
+/* Decode over the packed cache (Section 4.1: after eviction each head keeps
+ * its b_h real tokens and one charged centroid pair, and a later query
+ * attends over these b_h + 1 rows as ordinary keys; the plain slot carries no
+ * logit bias).  For the tq new queries of every sequence, query row
+ * (t, head h*G + g) of layer l attends over the packed segment of unit
+ * (l, b, h):
+ *   z_i = scale <q, k_i>, out = sum_i softmax(z)_i v_i, lse = log sum_i e^z_i.
+ *   q_new          [L][B*tq][Hq][d] in (kv_dtype), same stride rules as q_win
+ *   k_packed, v_packed, packed_offsets  the packed cache of certkv_compact or
+ *                  certkv_compress (device; segments of at most n_b rows)
+ *   out            [L][B*tq][Hq][d] fp32 out (contiguous)
+ *   lse            optional [L][B*tq][Hq] fp32 out (natural log)
+ * Every packed row is visible to every new query (they follow the whole
+ * cache).  bf16 caches only (CERTKV_EUNSUPPORTED for fp32); tq * G <= 512.
+ * The workspace is certkv_decode_workspace_size(p, tq) bytes, 256-byte
+ * aligned; a non-finite output sets the status word. */
+size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq);
+certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,
+                            int32_t tq, const void* k_packed,
+                            const void* v_packed,
+                            const int64_t* packed_offsets, float* out,
+                            float* lse, void* ws, size_t ws_bytes,
+                            void* stream);
+
 /* Per-kernel timing.  While enabled, every kernel the library launches is
  * bracketed by two hipEvents on its launch stream; certkv_profile_read
  * synchronises those events and reports, per kernel name, the launch count

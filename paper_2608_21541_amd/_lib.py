@@ -36,7 +36,8 @@ STAGE_COMPRESS = 6
 EXPORTS = [
     "certkv_status_string", "certkv_workspace_size", "certkv_score", "certkv_allocate",
     "certkv_allocate_curves", "certkv_select", "certkv_tail_summary", "certkv_compact",
-    "certkv_compress", "certkv_profile_enable", "certkv_profile_read", "certkv_profile_reset",
+    "certkv_compress", "certkv_decode_workspace_size", "certkv_decode", "certkv_profile_enable",
+    "certkv_profile_read", "certkv_profile_reset",
 ]
 
 
@@ -107,13 +108,17 @@ def lib():
     L.certkv_compact.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.certkv_compress.argtypes = [P, Tensor, Tensor, Tensor, vp, vp, dbl, i32,
                                   ctypes.POINTER(Outputs), vp, sz, vp]
+    L.certkv_decode_workspace_size.argtypes = [P, i32]
+    L.certkv_decode_workspace_size.restype = sz
+    L.certkv_decode.argtypes = [P, Tensor, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_profile_enable.argtypes = [i32]
     L.certkv_profile_read.argtypes = [vp, vp, vp, i32]
     L.certkv_profile_read.restype = i32
     L.certkv_profile_reset.argtypes = []
     L.certkv_profile_reset.restype = None
     for name in EXPORTS:
-        if name not in ("certkv_status_string", "certkv_workspace_size", "certkv_profile_read",
+        if name not in ("certkv_status_string", "certkv_workspace_size",
+                        "certkv_decode_workspace_size", "certkv_profile_read",
                         "certkv_profile_reset"):
             getattr(L, name).restype = i32
     _LIB = L

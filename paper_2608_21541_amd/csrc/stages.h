@@ -121,6 +121,30 @@ certkv_status run_bitmap(const TailArgs& a, const SeqTab& st, int64_t words_tota
 certkv_status run_tail(const TailArgs& a, const SeqTab& st, hipStream_t s);
 size_t score_smem_bytes(const Geo& g, int32_t dtype);
 
+struct DecodeArgs {
+  Geo g;
+  int64_t U;
+  int32_t tq;                   // new queries per sequence
+  int32_t nsplit;               // 1024-key chunks of the longest segment
+  certkv_tensor q;              // [L][B*tq][Hq][d] bf16
+  const void* k_packed;         // [P][d] bf16
+  const void* v_packed;
+  const int64_t* packed_offsets;
+  float* part_o;                // [U][nsplit][mp][d]
+  float2* part_ml;              // [U][nsplit][mp]
+  float* out;                   // [L][B*tq][Hq][d]
+  float* lse;                   // optional [L][B*tq][Hq]
+};
+// Query tiles of 32 rows for M decode rows, rounded up to a power of two.
+inline int decode_nqt(int M) {
+  int t = 1;
+  while (t * 32 < M) t *= 2;
+  return t;
+}
+certkv_status run_decode(const DecodeArgs& a, hipStream_t s);
+size_t decode_partial_rows(int64_t U, int nsplit, int tq, int G);
+int decode_nsplit(int max_len);
+
 certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64_t* packed_offsets,
                                    hipStream_t s);
 }  // namespace certkv

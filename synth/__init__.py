@@ -167,3 +167,17 @@ def make_cache(cfg: CacheConfig, device="cpu", layers=None):
         needles.append(ndl_l)
     return dict(q_win=q_all, k=k_all, v=v_all, cu_seqlens=cu, n_keep=cfg.n_keep(),
                 retrieval=retrieval, needles=needles, layers=lay, cfg=cfg)
+
+
+def make_queries(cfg: CacheConfig, tq: int, device="cpu", layers=None, seed_offset=7919):
+    """`tq` new (future) queries per sequence, [L][B*tq][Hq][d] in cfg.dtype:
+    standard normal like the window queries, from a stream of their own keyed
+    by (seed, layer)."""
+    L, H, G, d = cfg.layers, cfg.kv_heads, cfg.group, cfg.head_dim
+    lay = list(range(L)) if layers is None else list(layers)
+    out = torch.empty((len(lay), cfg.batch * tq, H * G, d), dtype=cfg.dtype, device=device)
+    for li, l in enumerate(lay):
+        gen = torch.Generator(device=device)
+        gen.manual_seed((cfg.seed + seed_offset) * 1_000_003 + l)
+        out[li] = torch.randn((cfg.batch * tq, H * G, d), generator=gen, device=device).to(cfg.dtype)
+    return out

@@ -177,3 +177,32 @@ def test_profile_api_without_launches():
     assert L.certkv_profile_read(names, None, None, 8) == 0
     L.certkv_profile_reset()
     assert L.certkv_profile_enable(0) == 0
+
+
+def test_dry_run_decode_validation():
+    L = _lib.lib()
+    p = problem()
+    n = L.certkv_decode_workspace_size(ctypes.byref(p), 8)
+    assert n > 0
+    # the partials grow with the number of new queries and never shrink
+    assert L.certkv_decode_workspace_size(ctypes.byref(p), 64) >= n
+    assert L.certkv_decode_workspace_size(ctypes.byref(p), 0) == 0
+
+    def call(pp=p, tq=8, q=None, kp=FAKE, vp=FAKE, off=FAKE, out=FAKE, ws=FAKE, nbytes=n):
+        q = tensor() if q is None else q
+        return L.certkv_decode(ctypes.byref(pp), q, tq, kp, vp, off, out, None, ws, nbytes, None)
+
+    assert call() == _lib.CERTKV_OK
+    assert call(tq=0) == _lib.CERTKV_EINVAL
+    assert call(tq=257) == _lib.CERTKV_EUNSUPPORTED          # tq * G = 514 rows > 512
+    assert call(q=tensor(ptr=FAKE + 2)) == _lib.CERTKV_EINVAL
+    assert call(q=tensor(st=4 * 128 + 4)) == _lib.CERTKV_EINVAL
+    assert call(kp=FAKE + 8) == _lib.CERTKV_EINVAL
+    assert call(off=None) == _lib.CERTKV_EINVAL
+    assert call(out=None) == _lib.CERTKV_EINVAL
+    assert call(ws=None) == _lib.CERTKV_EWORKSPACE
+    assert call(nbytes=n - 1) == _lib.CERTKV_EWORKSPACE
+    assert call(ws=FAKE + 64) == _lib.CERTKV_EINVAL
+    pf = problem(dtype=_lib.CERTKV_F32)
+    nf = L.certkv_decode_workspace_size(ctypes.byref(pf), 8)
+    assert call(pp=pf, nbytes=nf) == _lib.CERTKV_EUNSUPPORTED
