@@ -35,7 +35,7 @@ KERNEL_SOURCES = {
     "curve_blockstats": "allocate.hip", "allocate": "allocate.hip", "select": "select.hip",
     "kept_offsets": "select.hip", "clamp_budgets": "select.hip", "packed_offsets": "select.hip",
     "coverage_budget": "select.hip", "tail_": "tail.hip", "compact_": "tail.hip",
-    "kept_bitmap": "tail.hip",
+    "kept_bitmap": "tail.hip", "decode": "decode.hip",
 }
 
 
@@ -209,6 +209,73 @@ def summarize_traffic(fetch_csv, write_csv, kernel_regex, kernel, workload, out,
         fh.write("\n".join(lines) + "\n")
 
 
+def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
+    """Decode over the packed cache: one compression pass (untimed) builds it,
+    then `steps` decodes of `tq` new queries per sequence are timed.  The
+    algorithmic bytes of one decode are the packed K and V rows, the new
+    queries and the fp32 outputs; the split partials are overhead."""
+    import torch
+    import paper_2608_21541_amd as ck
+    import synth
+
+    ck.compress(spec, cache["q_win"], cache["k"], cache["v"], n_keep, bufs=bufs)
+    torch.cuda.synchronize()
+    rows = int(bufs.packed_offsets[-1].item())
+    # the budgets are known once compression has run: the longest segment
+    # bounds the split partials (set before the timed region)
+    max_rows = int((bufs.packed_offsets[1:] - bufs.packed_offsets[:-1]).max().item())
+    e = 2 if cfg.dtype_name == "bf16" else 4
+    hq = cfg.kv_heads * cfg.group
+    stream = torch.cuda.current_stream(dev)
+
+    def time_tq(tq, steps, warmup):
+        qn = synth.make_queries(cfg, tq, dev)
+        db = ck.DecodeBuffers(spec, tq, dev, max_rows=max_rows)
+        for _ in range(warmup):
+            ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq, bufs=db)
+        torch.cuda.synchronize()
+        ck.profile_reset()
+        ck.profile_enable(True)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(steps):
+            ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq, bufs=db)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        prof = ck.profile_read()
+        ck.profile_enable(False)
+        ck.profile_reset()
+        ms = t0.elapsed_time(t1) / steps
+        qrows = cfg.layers * cfg.batch * tq * hq
+        alg = rows * cfg.head_dim * e * 2 + qrows * cfg.head_dim * (e + 4)
+        kern = {n: {"launches_per_step": c / steps, "avg_ms": t / max(c, 1)}
+                for n, (c, t) in prof.items()}
+        kms = kern["decode"]["avg_ms"]
+        roof = {"bound": "hbm", "achieved": alg / (kms / 1e3) / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": alg / (kms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                "traffic": recorded_traffic("decode", f"{args.config}-decode{tq}"), "kernel": "decode",
+                "alg_bytes_per_launch": alg}
+        return ms, kern, roof
+
+    ms, kern, roof = time_tq(args.tq, args.steps, args.warmup)
+    ms1, kern1, roof1 = time_tq(1, args.steps, args.warmup)
+    log(f"decode tq={args.tq}: {ms:.3f} ms; tq=1: {ms1:.3f} ms")
+    tokens = cfg.batch * args.tq
+    rec = {
+        "metric": "decode over the packed cache: new tokens per second (all layers and heads)",
+        "value": tokens / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype_name, "data": "synthetic",
+        "config": {"workload": f"{args.config} packed cache ({rows} rows of {cfg.layers} layers x "
+                               f"{cfg.kv_heads} KV heads, n_keep {n_keep[0]}), {args.tq} new "
+                               f"queries per sequence x {hq} query heads",
+                   "tq": args.tq, "packed_rows": rows, "max_segment_rows": max_rows},
+        "roofline": roof, "kernels": kern,
+        "tq1": {"ms_per_step": ms1, "roofline": roof1, "kernels": kern1},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,6 +284,9 @@ def main():
     ap.add_argument("--config", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--decode", action="store_true",
+                    help="time decode over the packed cache instead of the pass")
+    ap.add_argument("--tq", type=int, default=32, help="new queries per sequence (--decode)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("CSV", "OUT", "COMMAND"),
@@ -260,6 +330,9 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream(dev)
+    if args.decode:
+        run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log)
+        return
     if args.calibrate_copy:
         # A plain device copy of known size: its FETCH_SIZE / WRITE_SIZE
         # readings scale the counters of the pass's kernels to bytes.

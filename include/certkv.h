@@ -65,7 +65,10 @@ enum {
                             /* a non-finite input (never returned by a    */
                             /* call: the launches are asynchronous)        */
   CERTKV_EWORKSPACE = -5,   /* workspace smaller than required             */
-  CERTKV_EHIP = -6          /* a HIP runtime call or launch failed         */
+  CERTKV_EHIP = -6,         /* a HIP runtime call or launch failed         */
+  CERTKV_ERANGE = -7        /* written to *dev_status by certkv_decode     */
+                            /* when a packed segment holds more rows than */
+                            /* its max_rows bound allowed for              */
 };
 
 enum { CERTKV_F32 = 0, CERTKV_BF16 = 1 };
@@ -316,17 +319,22 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
  * (l, b, h):
  *   z_i = scale <q, k_i>, out = sum_i softmax(z)_i v_i, lse = log sum_i e^z_i.
  *   q_new          [L][B*tq][Hq][d] in (kv_dtype), same stride rules as q_win
+ *   max_rows       bound on the rows of any head's segment (b_h + 1), or 0 for
+ *                  n_b of the longest sequence; it sizes the workspace. A
+ *                  longer segment stores CERTKV_ERANGE in *dev_status and its
+ *                  rows past the next multiple of 1024 are left out
  *   k_packed, v_packed, packed_offsets  the packed cache of certkv_compact or
- *                  certkv_compress (device; segments of at most n_b rows)
+ *                  certkv_compress (device)
  *   out            [L][B*tq][Hq][d] fp32 out (contiguous)
  *   lse            optional [L][B*tq][Hq] fp32 out (natural log)
  * Every packed row is visible to every new query (they follow the whole
  * cache).  bf16 caches only (CERTKV_EUNSUPPORTED for fp32); tq * G <= 512.
- * The workspace is certkv_decode_workspace_size(p, tq) bytes, 256-byte
- * aligned; a non-finite output sets the status word. */
-size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq);
+ * The workspace is certkv_decode_workspace_size(p, tq, max_rows) bytes,
+ * 256-byte aligned; a non-finite output sets the status word. */
+size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq,
+                                    int32_t max_rows);
 certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,
-                            int32_t tq, const void* k_packed,
+                            int32_t tq, int32_t max_rows, const void* k_packed,
                             const void* v_packed,
                             const int64_t* packed_offsets, float* out,
                             float* lse, void* ws, size_t ws_bytes,

@@ -17,6 +17,7 @@ CERTKV_EINFEASIBLE = -3
 CERTKV_ENONFINITE = -4
 CERTKV_EWORKSPACE = -5
 CERTKV_EHIP = -6
+CERTKV_ERANGE = -7
 
 CERTKV_F32 = 0
 CERTKV_BF16 = 1
@@ -108,9 +109,9 @@ def lib():
     L.certkv_compact.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.certkv_compress.argtypes = [P, Tensor, Tensor, Tensor, vp, vp, dbl, i32,
                                   ctypes.POINTER(Outputs), vp, sz, vp]
-    L.certkv_decode_workspace_size.argtypes = [P, i32]
+    L.certkv_decode_workspace_size.argtypes = [P, i32, i32]
     L.certkv_decode_workspace_size.restype = sz
-    L.certkv_decode.argtypes = [P, Tensor, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.certkv_decode.argtypes = [P, Tensor, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_profile_enable.argtypes = [i32]
     L.certkv_profile_read.argtypes = [vp, vp, vp, i32]
     L.certkv_profile_read.restype = i32

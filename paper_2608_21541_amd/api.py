@@ -231,38 +231,40 @@ def compact(spec: ProblemSpec, k, v, kept_offsets, kept_idx, k_star, v_star):
     return k_packed, v_packed, pos_packed, packed_offsets
 
 
-def decode_workspace_size(spec: ProblemSpec, tq: int) -> int:
+def decode_workspace_size(spec: ProblemSpec, tq: int, max_rows: int = 0) -> int:
     p = spec.c_problem()
-    return int(_lib.lib().certkv_decode_workspace_size(ctypes.byref(p), int(tq)))
+    return int(_lib.lib().certkv_decode_workspace_size(ctypes.byref(p), int(tq), int(max_rows)))
 
 
 class DecodeBuffers:
     """Preallocated outputs and workspace of certkv_decode (reusable)."""
 
-    def __init__(self, spec: ProblemSpec, tq: int, device, with_lse=False):
+    def __init__(self, spec: ProblemSpec, tq: int, device, with_lse=False, max_rows=0):
         self.tq = int(tq)
+        self.max_rows = int(max_rows)
         rows = spec.layers * spec.batch * self.tq
         hq = spec.kv_heads * spec.group
         self.out = torch.empty((spec.layers, spec.batch * self.tq, hq, spec.head_dim),
                                dtype=torch.float32, device=device)
         self.lse = torch.empty((spec.layers, spec.batch * self.tq, hq), dtype=torch.float32,
                                device=device) if with_lse else None
-        self.ws_bytes = decode_workspace_size(spec, self.tq)
+        self.ws_bytes = decode_workspace_size(spec, self.tq, self.max_rows)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         assert self.ws.data_ptr() % 256 == 0 and rows > 0
 
 
 def decode(spec: ProblemSpec, q_new, k_packed, v_packed, packed_offsets, tq, with_lse=False,
-           bufs=None):
+           bufs=None, max_rows=0):
     """Attention of tq new queries per sequence (q_new [L][B*tq][Hq][d]) over the packed
-    cache: out [L][B*tq][Hq][d] fp32 (and the natural-log lse [L][B*tq][Hq] with_lse)."""
+    cache: out [L][B*tq][Hq][d] fp32 (and the natural-log lse [L][B*tq][Hq] with_lse).
+    max_rows bounds the rows of any head's segment (0: the longest sequence)."""
     L = _lib.lib()
     dev = q_new.device
     if bufs is None:
-        bufs = DecodeBuffers(spec, tq, dev, with_lse=with_lse)
+        bufs = DecodeBuffers(spec, tq, dev, with_lse=with_lse, max_rows=max_rows)
     assert k_packed.is_contiguous() and v_packed.is_contiguous()
     p = spec.c_problem()
-    _check(L.certkv_decode(ctypes.byref(p), _tensor(q_new), int(tq), _ptr(k_packed),
+    _check(L.certkv_decode(ctypes.byref(p), _tensor(q_new), int(tq), bufs.max_rows, _ptr(k_packed),
                            _ptr(v_packed), _ptr(packed_offsets), _ptr(bufs.out), _ptr(bufs.lse),
                            _ptr(bufs.ws), bufs.ws_bytes, _stream(dev)), "certkv_decode")
     return (bufs.out, bufs.lse) if with_lse else bufs.out

@@ -495,6 +495,8 @@ const char* certkv_status_string(certkv_status st) {
       return "workspace too small";
     case CERTKV_EHIP:
       return "HIP runtime error";
+    case CERTKV_ERANGE:
+      return "packed segment longer than the decode row bound";
     default:
       return "unknown status";
   }
@@ -628,25 +630,32 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k, certkv_te
 
 // Decode partials: [rows][d] fp32 outputs, then (on a 256-byte boundary) the
 // rows' (max, sum) pairs.
-static size_t decode_ml_offset(const Plan& P, int32_t tq) {
-  const size_t rows = decode_partial_rows(P.U, decode_nsplit(P.max_len), tq, P.g.G);
+// A segment holds b_h <= n_b - 1 kept rows plus the slot row.
+static int decode_rows_bound(const Plan& P, int32_t max_rows) {
+  return (max_rows > 0 && max_rows < P.max_len) ? max_rows : P.max_len;
+}
+
+static size_t decode_ml_offset(const Plan& P, int32_t tq, int32_t max_rows) {
+  const size_t rows =
+      decode_partial_rows(P.U, decode_nsplit(decode_rows_bound(P, max_rows)), tq, P.g.G);
   return (rows * (size_t)P.g.D * sizeof(float) + 255) & ~(size_t)255;
 }
 
-size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq) {
+size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq, int32_t max_rows) {
   Plan P;
-  if (make_plan(p, &P) != CERTKV_OK || tq < 1) return 0;
-  const size_t rows = decode_partial_rows(P.U, decode_nsplit(P.max_len), tq, P.g.G);
-  return decode_ml_offset(P, tq) + rows * sizeof(float2);
+  if (make_plan(p, &P) != CERTKV_OK || tq < 1 || max_rows < 0) return 0;
+  const size_t rows =
+      decode_partial_rows(P.U, decode_nsplit(decode_rows_bound(P, max_rows)), tq, P.g.G);
+  return decode_ml_offset(P, tq, max_rows) + rows * sizeof(float2);
 }
 
 certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
-                            const void* k_packed, const void* v_packed,
+                            int32_t max_rows, const void* k_packed, const void* v_packed,
                             const int64_t* packed_offsets, float* out, float* lse, void* ws,
                             size_t ws_bytes, void* stream) {
   Plan P;
   TRY(make_plan(p, &P));
-  if (tq < 1) return CERTKV_EINVAL;
+  if (tq < 1 || max_rows < 0) return CERTKV_EINVAL;
   if (P.dtype != CERTKV_BF16) return CERTKV_EUNSUPPORTED;
   if ((int64_t)tq * P.g.G > 512) return CERTKV_EUNSUPPORTED;
   if (!q_new.ptr || ((uintptr_t)q_new.ptr & 15u)) return CERTKV_EINVAL;
@@ -654,22 +663,24 @@ certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_
   if (q_new.s_layer < 0 || q_new.s_token < 0 || q_new.s_head < 0) return CERTKV_EINVAL;
   if (!k_packed || !v_packed || !packed_offsets || !out) return CERTKV_EINVAL;
   if (((uintptr_t)k_packed & 15u) || ((uintptr_t)v_packed & 15u)) return CERTKV_EINVAL;
-  const size_t need = certkv_decode_workspace_size(p, tq);
+  const size_t need = certkv_decode_workspace_size(p, tq, max_rows);
   if (!ws) return CERTKV_EWORKSPACE;
   if (((uintptr_t)ws & 255u) != 0) return CERTKV_EINVAL;
   if (ws_bytes < need) return CERTKV_EWORKSPACE;
+  if (decode_nsplit(decode_rows_bound(P, max_rows)) > 65535) return CERTKV_EUNSUPPORTED;
   if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
   DecodeArgs a;
   a.g = P.g;
   a.U = P.U;
   a.tq = tq;
-  a.nsplit = decode_nsplit(P.max_len);
+  a.nsplit = decode_nsplit(decode_rows_bound(P, max_rows));
   a.q = q_new;
   a.k_packed = k_packed;
   a.v_packed = v_packed;
   a.packed_offsets = packed_offsets;
   a.part_o = static_cast<float*>(ws);
-  a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(ws) + decode_ml_offset(P, tq));
+  a.part_ml =
+      reinterpret_cast<float2*>(static_cast<char*>(ws) + decode_ml_offset(P, tq, max_rows));
   a.out = out;
   a.lse = lse;
   return run_decode(a, (hipStream_t)stream);

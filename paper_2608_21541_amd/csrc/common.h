@@ -38,6 +38,11 @@ __device__ __forceinline__ void report_nonfinite(const Geo& g) {
   if (g.status) *g.status = CERTKV_ENONFINITE;
 }
 
+// Record a segment longer than a caller's row bound (same racing-store rule).
+__device__ __forceinline__ void report_range(const Geo& g) {
+  if (g.status) *g.status = CERTKV_ERANGE;
+}
+
 __device__ __forceinline__ int64_t unit_index(const Geo& g, int l, int b, int h) {
   return ((int64_t)l * g.B + b) * g.H + h;
 }

@@ -182,15 +182,21 @@ def test_profile_api_without_launches():
 def test_dry_run_decode_validation():
     L = _lib.lib()
     p = problem()
-    n = L.certkv_decode_workspace_size(ctypes.byref(p), 8)
+    n = L.certkv_decode_workspace_size(ctypes.byref(p), 8, 0)
     assert n > 0
-    # the partials grow with the number of new queries and never shrink
-    assert L.certkv_decode_workspace_size(ctypes.byref(p), 64) >= n
-    assert L.certkv_decode_workspace_size(ctypes.byref(p), 0) == 0
+    # the partials grow with the number of new queries and never shrink; a
+    # segment bound below the longest sequence shrinks them
+    assert L.certkv_decode_workspace_size(ctypes.byref(p), 64, 0) >= n
+    plong = problem(seqlens=(5000, 700))
+    assert 0 < L.certkv_decode_workspace_size(ctypes.byref(plong), 8, 100) < \
+        L.certkv_decode_workspace_size(ctypes.byref(plong), 8, 0)
+    assert L.certkv_decode_workspace_size(ctypes.byref(p), 0, 0) == 0
+    assert L.certkv_decode_workspace_size(ctypes.byref(p), 8, -1) == 0
 
-    def call(pp=p, tq=8, q=None, kp=FAKE, vp=FAKE, off=FAKE, out=FAKE, ws=FAKE, nbytes=n):
+    def call(pp=p, tq=8, q=None, kp=FAKE, vp=FAKE, off=FAKE, out=FAKE, ws=FAKE, nbytes=n, mr=0):
         q = tensor() if q is None else q
-        return L.certkv_decode(ctypes.byref(pp), q, tq, kp, vp, off, out, None, ws, nbytes, None)
+        return L.certkv_decode(ctypes.byref(pp), q, tq, mr, kp, vp, off, out, None, ws, nbytes,
+                               None)
 
     assert call() == _lib.CERTKV_OK
     assert call(tq=0) == _lib.CERTKV_EINVAL
@@ -203,6 +209,9 @@ def test_dry_run_decode_validation():
     assert call(ws=None) == _lib.CERTKV_EWORKSPACE
     assert call(nbytes=n - 1) == _lib.CERTKV_EWORKSPACE
     assert call(ws=FAKE + 64) == _lib.CERTKV_EINVAL
+    assert call(mr=-1) == _lib.CERTKV_EINVAL
+    assert call(mr=100, nbytes=L.certkv_decode_workspace_size(ctypes.byref(p), 8, 100)) == \
+        _lib.CERTKV_OK
     pf = problem(dtype=_lib.CERTKV_F32)
-    nf = L.certkv_decode_workspace_size(ctypes.byref(pf), 8)
+    nf = L.certkv_decode_workspace_size(ctypes.byref(pf), 8, 0)
     assert call(pp=pf, nbytes=nf) == _lib.CERTKV_EUNSUPPORTED

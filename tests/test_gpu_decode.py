@@ -157,3 +157,42 @@ def test_future_query_lift_bound_on_gpu_outputs():
                 abs(terms["lam_T"] - terms["z_slot"]) / 4) + 1e-12
             worst_ratio = max(worst_ratio, err_gpu / bound)
     log(f"lift bound: worst ||O - Ohat|| / bound = {worst_ratio:.3f}")
+
+
+def test_keep_all_segment_of_exactly_one_chunk():
+    # n = 1024 with n_keep = n: every head's segment (n - 1 kept rows and the
+    # slot) fills exactly one 1024-key chunk, which is also the default row
+    # bound of the workspace.
+    cfg = synth.config("C2", seqlens=[1024])
+    cache = synth.make_cache(cfg, "cpu")
+    n = cfg.seqlens[0]
+    spec, bufs = _compress(cfg, cache, n_keep=[n])
+    po = bufs.packed_offsets.cpu().numpy()
+    log(f"segment rows {np.diff(po).max()}")
+    _check_against_oracle(cfg, cache, spec, bufs, tq=2)
+
+
+def test_decode_row_bound_gives_same_output_and_flags_overflow():
+    cfg = synth.config("C4", seqlens=[3000, 5000])
+    cache = synth.make_cache(cfg, "cpu")
+    spec, bufs = _compress(cfg, cache)
+    dev = torch.device("cuda:0")
+    tq = 8
+    qn = synth.make_queries(cfg, tq, "cpu").to(dev)
+    seg = int(np.diff(bufs.packed_offsets.cpu().numpy()).max())
+    log(f"longest segment {seg} rows")
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    spec.status = status
+    ref = ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq)
+    tight = ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq,
+                      max_rows=seg)
+    torch.cuda.synchronize()
+    assert int(status.item()) == ck.CERTKV_OK
+    # the same 1024-key chunks in the same order: the same bits
+    assert torch.equal(ref, tight)
+    assert ck.decode_workspace_size(spec, tq, seg) < ck.decode_workspace_size(spec, tq)
+    # a bound below the longest segment (by more than a chunk) is reported
+    ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq,
+              max_rows=seg - 1024)
+    torch.cuda.synchronize()
+    assert int(status.item()) == ck.CERTKV_ERANGE
