@@ -282,44 +282,90 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
     for (int v = 0; v < 16; ++v) po[32 * db + 8 * (v >> 2) + 4 * hh + (v & 3)] = O[db][v];
 }
 
-// Combine the chunk partials of each (unit, row) in split order: one thread
-// per output dim, 256 / D rows per workgroup.
+// Combine the chunk partials of each (unit, row): one workgroup per row, the
+// partial slots dealt round-robin to groups of D/4 threads (four output dims
+// per thread, 16-byte loads).  Each group folds its slots in order with an
+// online maximum; the groups are then merged in group order through LDS, so
+// the result does not depend on timing.  Slots of wave groups that saw no
+// key carry max -inf and are skipped.
+constexpr int kCombThreads = 256;
+
 template <int D>
-__global__ __launch_bounds__(256) void decode_combine_kernel(
+__global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
     Geo g, int32_t tq, int32_t nsub, int32_t kgroups, int32_t mp, const int64_t* __restrict__ poff,
     const float* __restrict__ part_o, const float2* __restrict__ part_ml, float* __restrict__ out,
     float* __restrict__ lse) {
-  constexpr int RPB = 256 / D;
-  const int64_t u = blockIdx.y;
-  const int row = blockIdx.x * RPB + threadIdx.x / D;
-  const int dd = threadIdx.x % D;
-  const int M = tq * g.G;
-  if (row >= M) return;
+  constexpr int C4 = D / 4;                // threads per slot row
+  constexpr int S = kCombThreads / C4;     // slot groups
+  __shared__ float4 acc_s[S][C4];
+  __shared__ float2 ml_s[S];
+  const int64_t u = blockIdx.x;
+  const int row = blockIdx.y;
+  const int sg = threadIdx.x / C4;
+  const int c4 = threadIdx.x % C4;
+  const int len = (int)(poff[u + 1] - poff[u]);
+  const int nv = min(nsub, kgroups * ((len + kDecKeys - 1) / kDecKeys));
+  if (len > (nsub / kgroups) * kDecKeys && row == 0 && threadIdx.x == 0) report_range(g);
+  const int64_t base = (int64_t)u * nsub * mp + row;  // + slot * mp
+  float m = -INFINITY, L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto fold = [&](float2 ml, float4 o) {
+    if (ml.x == -INFINITY) return;
+    if (ml.x > m) {
+      const float a = __builtin_amdgcn_exp2f(m - ml.x);  // 0 while m is -inf
+      L *= a;
+      acc.x *= a; acc.y *= a; acc.z *= a; acc.w *= a;
+      m = ml.x;
+    }
+    const float w = __builtin_amdgcn_exp2f(ml.x - m);
+    L += ml.y * w;
+    acc.x += o.x * w; acc.y += o.y * w; acc.z += o.z * w; acc.w += o.w * w;
+  };
+  int sp = sg;
+  for (; sp + 3 * S < nv; sp += 4 * S) {  // four slots in flight
+    float2 ml[4];
+    float4 o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t pr = base + (int64_t)(sp + i * S) * mp;
+      ml[i] = part_ml[pr];
+      o[i] = reinterpret_cast<const float4*>(part_o + pr * D)[c4];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fold(ml[i], o[i]);
+  }
+  for (; sp < nv; sp += S) {
+    const int64_t pr = base + (int64_t)sp * mp;
+    fold(part_ml[pr], reinterpret_cast<const float4*>(part_o + pr * D)[c4]);
+  }
+  acc_s[sg][c4] = acc;
+  if (c4 == 0) ml_s[sg] = make_float2(m, L);
+  __syncthreads();
+  if (threadIdx.x >= D) return;
+  const int dd = threadIdx.x;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < S; ++k) mx = fmaxf(mx, ml_s[k].x);
+  float Lt = 0.f, at = 0.f;
+#pragma unroll
+  for (int k = 0; k < S; ++k) {
+    const float2 mk = ml_s[k];
+    if (mk.x == -INFINITY) continue;
+    const float w = __builtin_amdgcn_exp2f(mk.x - mx);
+    Lt += mk.y * w;
+    at += reinterpret_cast<const float*>(&acc_s[k][0])[dd] * w;
+  }
+  const int Hq = g.H * g.G;
   const int h = (int)(u % g.H);
   const int64_t lb = u / g.H;
   const int b = (int)(lb % g.B);
   const int l = (int)(lb / g.B);
-  const int len = (int)(poff[u + 1] - poff[u]);
-  const int nv = min(nsub, kgroups * ((len + kDecKeys - 1) / kDecKeys));
-  if (len > (nsub / kgroups) * kDecKeys && row == 0 && dd == 0) report_range(g);
-  const int64_t base = (int64_t)u * nsub * mp + row;  // + slot * mp
-  float mx = -INFINITY;
-  for (int sp = 0; sp < nv; ++sp) mx = fmaxf(mx, part_ml[base + (int64_t)sp * mp].x);
-  float L = 0.f, acc = 0.f;
-  for (int sp = 0; sp < nv; ++sp) {
-    const int64_t pr = base + (int64_t)sp * mp;
-    const float2 ml = part_ml[pr];
-    const float w = __builtin_amdgcn_exp2f(ml.x - mx);
-    L += ml.y * w;
-    acc += part_o[pr * D + dd] * w;
-  }
-  const int Hq = g.H * g.G;
   const int t = row / g.G, gq = row % g.G;
   const int64_t orow = ((int64_t)l * g.B * tq + (int64_t)b * tq + t) * Hq + h * g.G + gq;
-  const float o = acc / L;
+  const float o = at / Lt;
   if (!isfinite(o)) report_nonfinite(g);
   out[orow * D + dd] = o;
-  if (lse && dd == 0) lse[orow] = (mx + __builtin_amdgcn_logf(L)) * kDecLn2;
+  if (lse && dd == 0) lse[orow] = (mx + __builtin_amdgcn_logf(Lt)) * kDecLn2;
 }
 
 template <int D, int NQT>
@@ -336,8 +382,8 @@ static certkv_status launch_decode(const DecodeArgs& a, hipStream_t s) {
                 a.tq, nsub, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
                 a.packed_offsets, a.part_o, a.part_ml);
   const int M = a.tq * g.G;
-  CERTKV_LAUNCH("decode_combine", decode_combine_kernel<D>,
-                dim3((unsigned)((M + 256 / D - 1) / (256 / D)), (unsigned)a.U), dim3(256), 0, s,
+  CERTKV_LAUNCH("decode_combine", decode_combine_kernel<D>, dim3((unsigned)a.U, (unsigned)M),
+                dim3(kCombThreads), 0, s,
                 g, a.tq, nsub, KG, mp, a.packed_offsets, (const float*)a.part_o,
                 (const float2*)a.part_ml, a.out, a.lse);
   return CERTKV_OK;
