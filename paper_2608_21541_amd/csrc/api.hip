@@ -635,18 +635,28 @@ static int decode_rows_bound(const Plan& P, int32_t max_rows) {
   return (max_rows > 0 && max_rows < P.max_len) ? max_rows : P.max_len;
 }
 
-static size_t decode_ml_offset(const Plan& P, int32_t tq, int32_t max_rows) {
-  const size_t rows =
-      decode_partial_rows(P.U, decode_nsplit(decode_rows_bound(P, max_rows)), tq, P.g.G);
-  return (rows * (size_t)P.g.D * sizeof(float) + 255) & ~(size_t)255;
+// Decode workspace: split partials (output rows, then (max, sum) pairs), the
+// work-item list and its length, each 256-byte aligned.
+struct DecodeWs {
+  int nsplit;
+  size_t ml_off, items_off, count_off, total;
+};
+static DecodeWs decode_ws_layout(const Plan& P, int32_t tq, int32_t max_rows) {
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  DecodeWs w;
+  w.nsplit = decode_nsplit(decode_rows_bound(P, max_rows));
+  const size_t rows = decode_partial_rows(P.U, w.nsplit, tq, P.g.G);
+  w.ml_off = up(rows * (size_t)P.g.D * sizeof(float));
+  w.items_off = up(w.ml_off + rows * sizeof(float2));
+  w.count_off = up(w.items_off + (size_t)P.U * w.nsplit * sizeof(int2));
+  w.total = w.count_off + 256;
+  return w;
 }
 
 size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq, int32_t max_rows) {
   Plan P;
   if (make_plan(p, &P) != CERTKV_OK || tq < 1 || max_rows < 0) return 0;
-  const size_t rows =
-      decode_partial_rows(P.U, decode_nsplit(decode_rows_bound(P, max_rows)), tq, P.g.G);
-  return decode_ml_offset(P, tq, max_rows) + rows * sizeof(float2);
+  return decode_ws_layout(P, tq, max_rows).total;
 }
 
 certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
@@ -667,20 +677,22 @@ certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_
   if (!ws) return CERTKV_EWORKSPACE;
   if (((uintptr_t)ws & 255u) != 0) return CERTKV_EINVAL;
   if (ws_bytes < need) return CERTKV_EWORKSPACE;
-  if (decode_nsplit(decode_rows_bound(P, max_rows)) > 65535) return CERTKV_EUNSUPPORTED;
+  const DecodeWs W = decode_ws_layout(P, tq, max_rows);
+  if ((int64_t)P.U * W.nsplit > INT32_MAX) return CERTKV_EUNSUPPORTED;
   if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
   DecodeArgs a;
   a.g = P.g;
   a.U = P.U;
   a.tq = tq;
-  a.nsplit = decode_nsplit(decode_rows_bound(P, max_rows));
+  a.nsplit = W.nsplit;
   a.q = q_new;
   a.k_packed = k_packed;
   a.v_packed = v_packed;
   a.packed_offsets = packed_offsets;
   a.part_o = static_cast<float*>(ws);
-  a.part_ml =
-      reinterpret_cast<float2*>(static_cast<char*>(ws) + decode_ml_offset(P, tq, max_rows));
+  a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(ws) + W.ml_off);
+  a.items = reinterpret_cast<int2*>(static_cast<char*>(ws) + W.items_off);
+  a.item_count = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + W.count_off);
   a.out = out;
   a.lse = lse;
   return run_decode(a, (hipStream_t)stream);

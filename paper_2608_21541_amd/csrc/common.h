@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "certkv.h"
 
 namespace certkv {
@@ -11,6 +13,20 @@ namespace certkv {
 // Per-launch table of up to kMaxSeq sequences, passed by value as a kernel
 // argument so that no host-to-device copy is needed for ragged batches.
 constexpr int kMaxSeq = 48;
+constexpr int kMaxDevices = 64;  // devices whose properties are cached
+
+// Compute units of device dev (queried once; 0 if the query fails).
+inline int device_cus(int dev) {
+  static std::atomic<int> cus[kMaxDevices];
+  if (dev < 0 || dev >= kMaxDevices) return 0;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 struct SeqTab {
   int32_t count;             // sequences in this launch

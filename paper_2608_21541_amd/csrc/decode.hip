@@ -65,33 +65,142 @@ struct DecShape {
   static constexpr int NW = NQT < 4 ? 4 : NQT;  // waves per workgroup
   static constexpr int KG = NW / NQT;            // wave groups over the key tiles
 };
-constexpr int kDecBatch = 2;  // key tiles staged per iteration
 
-// Two waves per SIMD: the register cap keeps the accumulators out of AGPRs
-// without spilling (three waves would spill).
+// LDS pipeline: a stage is one key tile per wave group; NBUF stage buffers
+// (up to 64 KiB of K and V tiles, at least two), filled NBUF - 1 stages
+// ahead of the one being consumed.
+template <int D, int NQT>
+struct DecPipe {
+  static constexpr int TPS = DecShape<NQT>::KG;                  // tiles per stage
+  static constexpr int STAGE_BYTES = TPS * 2 * kDecTile * D * 2;
+  static constexpr int NB0 = 65536 / STAGE_BYTES;
+  static constexpr int NBUF = NB0 > 4 ? 4 : (NB0 < 2 ? 2 : NB0);
+};
+
+// LDS layout of a stage: [tile][K, V][32 rows][D/8 chunks of 16 bytes], rows
+// in natural (key-major) order.  Chunks are XOR-swizzled within a row so that
+// both fragment reads are free of bank conflicts: the key-tile read (one
+// 16-byte chunk per lane, 16 consecutive rows per pass) and the transposing
+// value-tile read (8 bytes per lane, four consecutive rows and eight
+// consecutive 32-byte segments per half-wave).  The map is an involution:
+// the slot of chunk c is c ^ f(r) and the chunk in slot s is s ^ f(r).
+template <int D>
+__device__ __forceinline__ int dec_swz_k(int r, int c) {
+  return c ^ ((D == 128 ? r : (r >> 1)) & (D / 8 - 1));
+}
+template <int D>
+__device__ __forceinline__ int dec_swz_v(int r, int c) {
+  return c ^ (D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1));
+}
+
+// One wave-wide 16-byte load straight into LDS: lane L's 16 bytes from src
+// land at LDS byte address lds + 16 L (lds wave-uniform, through M0).  Issued
+// as inline assembly so that the compiler does not treat the load as a
+// pending LDS write (which would make it wait for every load in flight at
+// each barrier); the caller waits for it with dec_wait_vm0 before the
+// barrier that publishes the stage.
+__device__ __forceinline__ void dec_dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory", "m0");
+}
+
+// Wait until at most N vector-memory accesses of this wave are in flight
+// (the other counters at their maximum; a builtin, so the compiler's own
+// bookkeeping of outstanding loads sees it).
+template <int N>
+__device__ __forceinline__ void dec_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void dec_wait_vm0() { dec_wait_vm<0>(); }
+
+// dec_wait_vm<PER * n> for a wave-uniform n in [0, NMAX].
+template <int PER, int NMAX>
+__device__ __forceinline__ void dec_wait_stages(int n) {
+  if constexpr (NMAX == 0) {
+    dec_wait_vm<0>();
+  } else {
+    if (n >= NMAX)
+      dec_wait_vm<PER * NMAX>();
+    else
+      dec_wait_stages<PER, NMAX - 1>(n);
+  }
+}
+
+__device__ __forceinline__ uint32_t dec_lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+typedef short dec_s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) dec_s16x4 dec_lds_s16x4;
+
+// The work items of a decode: every (unit, chunk) pair whose chunk starts
+// inside the unit's segment (at most nsplit chunks per unit), unit-major.  One
+// workgroup scans the per-unit chunk counts in rounds of kItemThreads units.
+constexpr int kItemThreads = 1024;
+__global__ __launch_bounds__(kItemThreads) void decode_items_kernel(
+    int64_t U, int32_t nsplit, const int64_t* __restrict__ poff, int2* __restrict__ items,
+    int32_t* __restrict__ count) {
+  __shared__ int scan[kItemThreads];
+  const int t = threadIdx.x;
+  int base = 0;  // items of the earlier rounds
+  for (int64_t u0 = 0; u0 < U; u0 += kItemThreads) {
+    const int64_t u = u0 + t;
+    int n = 0;
+    if (u < U) {
+      const int64_t len = poff[u + 1] - poff[u];
+      n = (int)min((int64_t)nsplit, (len + kDecKeys - 1) / kDecKeys);
+    }
+    scan[t] = n;
+    __syncthreads();
+    for (int d = 1; d < kItemThreads; d <<= 1) {  // inclusive scan
+      const int x = t >= d ? scan[t - d] : 0;
+      __syncthreads();
+      scan[t] += x;
+      __syncthreads();
+    }
+    const int start = base + scan[t] - n;
+    for (int k = 0; k < n; ++k) items[start + k] = make_int2((int)u, k);
+    base += scan[kItemThreads - 1];
+    __syncthreads();  // scan[] is rewritten by the next round
+  }
+  if (t == 0) *count = base;
+}
+
+// Two waves per SIMD: the register cap keeps the accumulators out of AGPRs.
 template <int D, int NQT>
 __global__ __launch_bounds__(64 * DecShape<NQT>::NW)
 __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
-    Geo g, int32_t tq, int32_t nsub, int32_t mp, const uint16_t* __restrict__ qn,
-    int64_t q_sl, int64_t q_st, int64_t q_sh, const uint16_t* __restrict__ kp,
-    const uint16_t* __restrict__ vp, const int64_t* __restrict__ poff,
-    float* __restrict__ part_o, float2* __restrict__ part_ml) {
+    Geo g, const int2* __restrict__ items, const int32_t* __restrict__ item_count,
+    int32_t tq, int32_t nsub, int32_t mp,
+    const uint16_t* __restrict__ qn, int64_t q_sl, int64_t q_st, int64_t q_sh,
+    const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
+    const int64_t* __restrict__ poff, float* __restrict__ part_o, float2* __restrict__ part_ml) {
   constexpr int NW = DecShape<NQT>::NW;
   constexpr int KG = DecShape<NQT>::KG;
+  constexpr int TPS = DecPipe<D, NQT>::TPS;
+  constexpr int NBUF = DecPipe<D, NQT>::NBUF;
+  constexpr int PD = NBUF - 1;     // stages in flight ahead of the consumed one
   constexpr int KS = D / 16;       // MFMA k-steps of S^T
   constexpr int HD = D / 2;        // dims per lane half in S^T
   constexpr int NDB = D / 32;      // 32-dim blocks of the output
-  constexpr int RE = D + 8;        // padded LDS row of a key tile, bf16 elements
-  constexpr int VT = kDecTile + 4; // padded LDS row of a transposed value tile
   constexpr int CH = D / 8;        // 16-byte chunks per row
-  // the batch's key tiles [key][dim] and transposed value tiles [dim][key]
-  __shared__ __align__(16) uint16_t k_lds[kDecBatch][kDecTile * RE];
-  __shared__ __align__(16) uint16_t v_lds[kDecBatch][D * VT];
+  constexpr int TILE = kDecTile * D;          // bf16 elements of one K (or V) tile
+  constexpr int TILE_CH = kDecTile * CH;      // its 16-byte chunks
+  constexpr int NINS = TPS * 2 * TILE_CH / 64;  // wave-wide 16-byte loads per stage
+  constexpr int PERW = NINS >= NW ? NINS / NW : 1;  // of them per wave (or none)
+  static_assert((NINS % NW == 0 || NINS < NW) && TILE_CH % 64 == 0, "stage split");
+  __shared__ __align__(16) uint16_t lds[NBUF][TPS][2][TILE];
 
-  // units along x, chunks along y: every unit's first chunks are dispatched
-  // before any unit's later (possibly empty) ones
-  const int64_t u = blockIdx.x;
-  const int split = blockIdx.y;
+  // A persistent grid over the work items (unit, chunk), taken in a fixed
+  // stride: consecutive chunks of a long segment go to different workgroups.
+  const int nitems = *item_count;
+  for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
+  const int2 it = items[item];
+  const int64_t u = it.x;
+  const int split = it.y;
   const int h = (int)(u % g.H);
   const int64_t lb = u / g.H;
   const int b = (int)(lb % g.B);
@@ -99,10 +208,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   const int64_t p0 = poff[u];
   const int len = (int)(poff[u + 1] - p0);
   const int c0 = split * kDecKeys;
-  if (c0 >= len) return;  // whole workgroup: this unit has fewer chunks
+  if (c0 >= len) continue;  // whole workgroup: this unit has fewer chunks
   const int c1 = min(len, c0 + kDecKeys);
   const int ntiles = (c1 - c0 + kDecTile - 1) / kDecTile;
-  const int nbatch = (ntiles + kDecBatch - 1) / kDecBatch;
+  const int nstage = (ntiles + TPS - 1) / TPS;
   const int M = tq * g.G;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -113,64 +222,31 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   const int row = qt * 32 + c32;    // this lane's query row
   const float c2 = g.scale * kDecLog2e;
 
-  // The query row as B fragments of S^T (zero for padding rows); lane half hh
-  // owns the dims hh*HD .. hh*HD + HD - 1 (the contraction order is free).
+  // A stage goes from memory straight into LDS: wave-wide 16-byte loads, lane
+  // L of load n filling chunk slot 64 n + L of the stage.  The chunk a slot
+  // holds is chosen by the swizzle; rows past the segment are clamped to its
+  // last row (their keys are masked, so they only ever meet zero weights).
+  const uint16_t* kseg = kp + p0 * D;
+  const uint16_t* vseg = vp + p0 * D;
+  auto issue_stage = [&](int st) {
+    const int tile0 = st * TPS;
+#pragma unroll
+    for (int i = 0; i < PERW; ++i) {
+      const int n = wave * PERW + i;
+      const int tile = n / (2 * TILE_CH / 64);              // uniform over the wave
+      const int kv = (n / (TILE_CH / 64)) & 1;
+      if (n < NINS && tile0 + tile < ntiles) {
+        const int pos = (n % (TILE_CH / 64)) * 64 + lane;   // slot within the tile
+        const int r = pos / CH;
+        const int chunk = kv ? dec_swz_v<D>(r, pos % CH) : dec_swz_k<D>(r, pos % CH);
+        const int key = min(c0 + (tile0 + tile) * kDecTile + r, len - 1);
+        const uint16_t* src = (kv ? vseg : kseg) + (int64_t)key * D + chunk * 8;
+        dec_dma16(src, dec_lds_addr(&lds[st % NBUF][tile][kv][(n % (TILE_CH / 64)) * 512]));
+      }
+    }
+  };
+
   DecFrag qf[KS];
-  if (row < M) {
-    const int t = row / g.G, gq = row % g.G;
-    const uint4* src = reinterpret_cast<const uint4*>(
-        qn + (int64_t)l * q_sl + (int64_t)(b * tq + t) * q_st + (int64_t)(h * g.G + gq) * q_sh +
-        hh * HD);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s].u = src[s];
-  } else {
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s].u = make_uint4(0u, 0u, 0u, 0u);
-  }
-
-  // Cooperative staging of a batch in 16-byte chunks.  Within a tile, key
-  // chunk e is row e / CH, chunk e % CH (coalesced rows); value chunk e is
-  // key e % 32, chunk e / 32 (its transposed 2-byte writes then fall on
-  // consecutive keys).  The loads go through range-checked buffers over the
-  // unit's segment, unconditionally (a conditional load would make the
-  // compiler wait for the whole prefetch at the branch join): rows past the
-  // segment read as zero, rows past the chunk are masked from the softmax.
-  const uint32_t seg_bytes = (uint32_t)len * D * 2u;
-  const BufRsrc krs = make_rsrc(kp + p0 * D, seg_bytes);
-  const BufRsrc vrs = make_rsrc(vp + p0 * D, seg_bytes);
-  constexpr int NTHR = 64 * NW;
-  constexpr int HCH = kDecBatch * kDecTile * CH;  // key (or value) chunks of a batch
-  constexpr int PER = (HCH + NTHR - 1) / NTHR;    // of each per thread
-  uint4 stage_k[PER], stage_v[PER];
-  auto load_batch = [&](int tb) {
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int e = threadIdx.x + j * NTHR;
-      if (HCH % NTHR == 0 || e < HCH) {
-        const int tile = e / (kDecTile * CH), et = e % (kDecTile * CH);
-        const int rk = et / CH, chk = et % CH;        // key tile: row-major chunks
-        const int rv = et % kDecTile, chv = et / kDecTile;  // value tile: key-fastest
-        const int tk = tb - c0 + tile * kDecTile;     // tile start within the chunk
-        stage_k[j] = buf_load_u128(krs, ((uint32_t)(c0 + tk + rk) * D + chk * 8) * 2u);
-        stage_v[j] = buf_load_u128(vrs, ((uint32_t)(c0 + tk + rv) * D + chv * 8) * 2u);
-      }
-    }
-  };
-  auto store_batch = [&]() {
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int e = threadIdx.x + j * NTHR;
-      if (HCH % NTHR == 0 || e < HCH) {
-        const int tile = e / (kDecTile * CH), et = e % (kDecTile * CH);
-        *reinterpret_cast<uint4*>(&k_lds[tile][(et / CH) * RE + (et % CH) * 8]) = stage_k[j];
-        const int rv = et % kDecTile, chv = et / kDecTile;
-        const uint16_t* x = reinterpret_cast<const uint16_t*>(&stage_v[j]);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) v_lds[tile][(chv * 8 + q) * VT + rv] = x[q];
-      }
-    }
-  };
-
   float m_run = -INFINITY, l_run = 0.f;
   dec_f32x16 O[NDB];
 #pragma unroll
@@ -178,10 +254,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
 #pragma unroll
     for (int v = 0; v < 16; ++v) O[db][v] = 0.f;
 
-  // One key tile (LDS slot j, first key t0) for this wave's query tile.
-  auto process_tile = [&](int j, int t0) {
-    const uint16_t* kt = k_lds[j];
-    const uint16_t* vt = v_lds[j];
+  // One key tile (stage buffer sb, slot j, first key t0) for this wave's
+  // query tile.
+  auto process_tile = [&](int sb, int j, int t0) {
+    const uint16_t* kt = lds[sb][j][0];
+    const uint16_t* vt = lds[sb][j][1];
     // S^T = K Q^T: lane (hh, c32) holds query row c32 and keys
     // 8*(v/4) + 4*hh + v%4 of the tile
     dec_f32x16 s;
@@ -190,7 +267,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       DecFrag kf;
-      kf.u = *reinterpret_cast<const uint4*>(kt + c32 * RE + hh * HD + ks * 8);
+      kf.u = *reinterpret_cast<const uint4*>(kt + c32 * D +
+                                             dec_swz_k<D>(c32, hh * (CH / 2) + ks) * 8);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf.v, qf[ks].v, s, 0, 0, 0);
     }
     // Online softmax of the row in log2 units (z = c2 * s, c2 > 0, so the
@@ -206,7 +284,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
     float mt = s[0];
 #pragma unroll
     for (int v = 1; v < 16; ++v) mt = fmaxf(mt, s[v]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * c2;
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt),
+                                                       false, false);
+      mt = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;
+    }
     // Lazy rescaling: the reference maximum m_run moves only when some row of
     // the wave would otherwise see a weight above 2^kDecSlack; the weights
     // exp2(z - m_run) then stay below 2^kDecSlack and the partial (m_run,
@@ -236,37 +318,68 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
       reinterpret_cast<uint32_t*>(&ph[v >> 3].u)[(v & 7) >> 1] = hi;
       reinterpret_cast<uint32_t*>(&pl[v >> 3].u)[(v & 7) >> 1] = dec_pack_bf16(r0, r1);
     }
-    // O^T += V^T P^T per 32-dim block; V^T lane (hh, c32) = dim 32 db + c32
-    // over the same keys: keys 16 kk + 4 hh + 0..3 and 16 kk + 8 + 4 hh + 0..3
+    // O^T += V^T P^T per 32-dim block.  V^T (A operand): lane (hh, c32) needs
+    // dim 32 db + c32 at the keys of its k-slots.  A transposing read serves
+    // them from the key-major tile: in each group of 16 lanes, lane a
+    // addresses key 16 kk + 8 rd + 4 hh + a/4 at dims 4 (a%4) .. 4 (a%4) + 3
+    // of its group's 16 dims, and lane i receives dim i of keys
+    // 16 kk + 8 rd + 4 hh + 0..3, which are its k-slots 4 rd .. 4 rd + 3.
+    const int a = c32 & 15;
+    const int vdim = 16 * (c32 >> 4) + 4 * (a & 3);  // + 32 db
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         DecFrag vf;
-        const uint16_t* vrow = vt + (32 * db + c32) * VT + 16 * kk + 4 * hh;
-        const uint2 lo4 = *reinterpret_cast<const uint2*>(vrow);
-        const uint2 hi4 = *reinterpret_cast<const uint2*>(vrow + 8);
-        vf.u = make_uint4(lo4.x, lo4.y, hi4.x, hi4.y);
+#pragma unroll
+        for (int rd = 0; rd < 2; ++rd) {
+          const int r = 16 * kk + 8 * rd + 4 * hh + (a >> 2);
+          const int dim = 32 * db + vdim;
+          const uint16_t* src = vt + r * D + dec_swz_v<D>(r, dim >> 3) * 8 + (dim & 7);
+          const dec_s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (dec_lds_s16x4*)(__attribute__((address_space(3))) uint16_t*)src);
+          reinterpret_cast<uint2*>(&vf.u)[rd] = __builtin_bit_cast(uint2, x);
+        }
         O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, ph[kk].v, O[db], 0, 0, 0);
         O[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pl[kk].v, O[db], 0, 0, 0);
       }
     }
   };
 
-  load_batch(c0);
-  store_batch();
-  __syncthreads();
-  for (int bi = 0; bi < nbatch; ++bi) {
-    const int tb = c0 + bi * kDecBatch * kDecTile;
-    if (bi + 1 < nbatch) load_batch(tb + kDecBatch * kDecTile);  // in flight meanwhile
-    for (int j = kg; j < kDecBatch; j += KG) {
-      const int t0 = tb + j * kDecTile;
-      if (t0 < c1) process_tile(j, t0);
-    }
-    __syncthreads();  // the batch is consumed
-    if (bi + 1 < nbatch) {
-      store_batch();
-      __syncthreads();
+  // Stage 0 and the query fragments are awaited together; then up to PD
+  // stages are in flight.  At the top of stage st each wave waits until its
+  // loads of st have landed: loads complete in order, so it may leave in
+  // flight those of the later stages already issued, counting only whole
+  // stages (a short last stage is waited for with the rest, which is safe).
+  // The barrier then publishes stage st and certifies that every wave is done
+  // with stage st - 1, whose buffer the loads of stage st + PD overwrite.
+  issue_stage(0);
+  // The query row as B fragments of S^T (zero for padding rows); lane half hh
+  // owns the dims hh*HD .. hh*HD + HD - 1 (the contraction order is free).
+  if (row < M) {
+    const int t = row / g.G, gq = row % g.G;
+    const uint4* src = reinterpret_cast<const uint4*>(
+        qn + (int64_t)l * q_sl + (int64_t)(b * tq + t) * q_st + (int64_t)(h * g.G + gq) * q_sh +
+        hh * HD);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qf[s].u = src[s];
+  } else {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qf[s].u = make_uint4(0u, 0u, 0u, 0u);
+  }
+
+  dec_wait_vm0();
+  for (int st = 1; st < PD && st < nstage; ++st) issue_stage(st);
+  const bool short_last = (ntiles % TPS) != 0;
+  for (int st = 0; st < nstage; ++st) {
+    int ahead = min(PD - 1, nstage - 1 - st);         // later stages in flight
+    if (short_last && st + ahead == nstage - 1 && ahead > 0) --ahead;
+    dec_wait_stages<PERW, PD - 1>(ahead);
+    __syncthreads();
+    if (st + PD < nstage) issue_stage(st + PD);
+    for (int j = kg; j < TPS; j += KG) {
+      const int t0 = c0 + (st * TPS + j) * kDecTile;
+      if (t0 < c1) process_tile(st % NBUF, j, t0);
     }
   }
 
@@ -280,6 +393,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) po[32 * db + 8 * (v >> 2) + 4 * hh + (v & 3)] = O[db][v];
+  __syncthreads();  // every wave is done with the stage buffers of this item
+  }
 }
 
 // Combine the chunk partials of each (unit, row): one workgroup per row, the
@@ -374,12 +489,32 @@ static certkv_status launch_decode(const DecodeArgs& a, hipStream_t s) {
   const int mp = NQT * 32;
   constexpr int KG = DecShape<NQT>::KG;
   const int nsub = a.nsplit * KG;
-  dim3 grid((unsigned)a.U, a.nsplit);
+  // as many workgroups as stay resident at once (the occupancy query is made
+  // once per device and kernel instance)
+  constexpr int NT = 64 * DecShape<NQT>::NW;
+  static std::atomic<int> per_cu[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CERTKV_EHIP;
+  int nb = per_cu[dev].load(std::memory_order_relaxed);
+  if (nb == 0) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_kernel<D, NQT>, NT, 0) !=
+        hipSuccess)
+      return CERTKV_EHIP;
+    nb = nb > 0 ? nb : 1;
+    per_cu[dev].store(nb, std::memory_order_relaxed);
+  }
+  const int cus = device_cus(dev);
+  if (cus <= 0) return CERTKV_EHIP;
+  const int64_t max_items = a.U * a.nsplit;
+  const int64_t want = (int64_t)cus * nb;
+  const unsigned grid = (unsigned)(max_items < want ? max_items : want);
   const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
   const uint16_t* kp = static_cast<const uint16_t*>(a.k_packed);
   const uint16_t* vp = static_cast<const uint16_t*>(a.v_packed);
-  CERTKV_LAUNCH("decode", (decode_kernel<D, NQT>), grid, dim3(64 * DecShape<NQT>::NW), 0, s, g,
-                a.tq, nsub, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
+  CERTKV_LAUNCH("decode_items", decode_items_kernel, dim3(1), dim3(kItemThreads), 0, s, a.U,
+                a.nsplit, a.packed_offsets, a.items, a.item_count);
+  CERTKV_LAUNCH("decode", (decode_kernel<D, NQT>), dim3(grid), dim3(NT), 0, s, g, a.items,
+                a.item_count, a.tq, nsub, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
                 a.packed_offsets, a.part_o, a.part_ml);
   const int M = a.tq * g.G;
   CERTKV_LAUNCH("decode_combine", decode_combine_kernel<D>, dim3((unsigned)a.U, (unsigned)M),

@@ -125,13 +125,15 @@ struct DecodeArgs {
   Geo g;
   int64_t U;
   int32_t tq;                   // new queries per sequence
-  int32_t nsplit;               // 1024-key chunks of the longest segment
+  int32_t nsplit;               // 1024-key chunks of the longest segment allowed
   certkv_tensor q;              // [L][B*tq][Hq][d] bf16
   const void* k_packed;         // [P][d] bf16
   const void* v_packed;
   const int64_t* packed_offsets;
   float* part_o;                // [U][nsplit][mp][d]
   float2* part_ml;              // [U][nsplit][mp]
+  int2* items;                  // [U * nsplit] work items (unit, chunk), built on device
+  int32_t* item_count;          // their number
   float* out;                   // [L][B*tq][Hq][d]
   float* lse;                   // optional [L][B*tq][Hq]
 };
