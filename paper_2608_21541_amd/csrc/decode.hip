@@ -7,14 +7,14 @@
 // over the unit's packed segment:
 //   z_i = scale <q, k_i>,  out = sum_i softmax(z)_i v_i,  lse = log sum e^z.
 //
-// Split over keys: one workgroup per (unit, 1024-key chunk), the grid ordered
-// unit-fastest so that the chunks of every unit are dispatched before the
-// empty tail of the grid (which is sized for the longest segment the caller
-// allows).  One wave per 32-row query tile; with fewer than four tiles the
-// spare waves form groups that take alternate key tiles.  Key and value tiles
-// of 32 rows are staged through LDS two at a time (16-byte range-checked
-// loads prefetched into registers during the previous batch; the value tile
-// is stored transposed, [dim][key]).  Per tile and wave:
+// Split over keys: the work items are (unit, 1024-key chunk) pairs, listed on
+// the device and taken in a fixed stride by a persistent grid of as many
+// workgroups as stay resident.  A workgroup holds the unit's query tiles of
+// 32 rows, one wave each; with fewer than four tiles, two or four waves share
+// a tile and split its output dims.  Key and value tiles of 32 rows go from
+// memory straight into LDS (wave-wide 16-byte LDS-DMA loads into a ring of
+// five tile buffers, XOR-swizzled chunks, rows in natural order).  Per tile
+// and wave:
 //   S^T = K Q^T on v_mfma_f32_32x32x16_bf16 with the key tile as the A
 //     operand, so lane (hh, c) holds query row c and 16 of the tile's keys;
 //   online softmax in log2 units, the row maximum shared by the two lanes of
@@ -23,8 +23,8 @@
 //   O^T += V^T P^T on the same MFMA: P^T (B operand) comes straight from the
 //     lane's registers, split into a bf16 high part and the bf16 of the
 //     remainder (two MFMAs, about 16 bits of the fp32 weight), and V^T (A
-//     operand) is two 8-byte reads of the transposed value tile along the
-//     same key order.
+//     operand) comes from transposing LDS reads of the key-major value tile
+//     along the same key order.
 // The chunk partials (reference max, sum, unnormalized output) are combined
 // in split order by a second kernel (deterministic).
 #include "stages.h"
@@ -57,24 +57,27 @@ __device__ __forceinline__ uint32_t dec_pack_bf16(float a, float b) {
 }
 
 
-// Workgroup shape: one wave per 32-row query tile, at least four waves; with
-// fewer query tiles the KG = NW / NQT wave groups take different key tiles of
-// a batch, each with its own softmax state and partial slot.
-template <int NQT>
+// Workgroup shape: every wave takes one 32-row query tile and all keys; with
+// fewer than four query tiles, DS waves share a query tile and split the
+// output dims (each computes the tile's scores and softmax, and P V for its
+// D / DS dims), down to 32 dims per wave.
+template <int D, int NQT>
 struct DecShape {
-  static constexpr int NW = NQT < 4 ? 4 : NQT;  // waves per workgroup
-  static constexpr int KG = NW / NQT;            // wave groups over the key tiles
+  static constexpr int DS0 = NQT >= 4 ? 1 : 4 / NQT;
+  static constexpr int DS = DS0 < D / 32 ? DS0 : D / 32;  // dim splits per query tile
+  static constexpr int NW = NQT * DS;                      // waves per workgroup
+  static constexpr int NDBW = D / 32 / DS;                 // 32-dim blocks per wave
 };
 
-// LDS pipeline: a stage is one key tile per wave group; NBUF stage buffers
-// (up to 64 KiB of K and V tiles, at least two), filled NBUF - 1 stages
-// ahead of the one being consumed.
-template <int D, int NQT>
+// LDS pipeline: a stage is one key tile (K and V); NBUF stage buffers, up to
+// kDecLdsBytes and at most five (two workgroups per compute unit).
+constexpr int kDecLdsBytes = 80 * 1024;
+template <int D>
 struct DecPipe {
-  static constexpr int TPS = DecShape<NQT>::KG;                  // tiles per stage
-  static constexpr int STAGE_BYTES = TPS * 2 * kDecTile * D * 2;
-  static constexpr int NB0 = 65536 / STAGE_BYTES;
-  static constexpr int NBUF = NB0 > 4 ? 4 : (NB0 < 2 ? 2 : NB0);
+  static constexpr int STAGE_BYTES = 2 * kDecTile * D * 2;
+  static constexpr int NB0 = kDecLdsBytes / STAGE_BYTES;
+  static constexpr int NBUF = NB0 > 5 ? 5 : NB0;
+  static_assert(NBUF >= 3, "three stage buffers at least");
 };
 
 // LDS layout of a stage: [tile][K, V][32 rows][D/8 chunks of 16 bytes], rows
@@ -171,28 +174,25 @@ __global__ __launch_bounds__(kItemThreads) void decode_items_kernel(
 
 // Two waves per SIMD: the register cap keeps the accumulators out of AGPRs.
 template <int D, int NQT>
-__global__ __launch_bounds__(64 * DecShape<NQT>::NW)
+__global__ __launch_bounds__((64 * DecShape<D, NQT>::NW))
 __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
     Geo g, const int2* __restrict__ items, const int32_t* __restrict__ item_count,
-    int32_t tq, int32_t nsub, int32_t mp,
+    int32_t tq, int32_t nsplit, int32_t mp,
     const uint16_t* __restrict__ qn, int64_t q_sl, int64_t q_st, int64_t q_sh,
     const uint16_t* __restrict__ kp, const uint16_t* __restrict__ vp,
     const int64_t* __restrict__ poff, float* __restrict__ part_o, float2* __restrict__ part_ml) {
-  constexpr int NW = DecShape<NQT>::NW;
-  constexpr int KG = DecShape<NQT>::KG;
-  constexpr int TPS = DecPipe<D, NQT>::TPS;
-  constexpr int NBUF = DecPipe<D, NQT>::NBUF;
-  constexpr int PD = NBUF - 1;     // stages in flight ahead of the consumed one
+  constexpr int NW = DecShape<D, NQT>::NW;
+  constexpr int NDBW = DecShape<D, NQT>::NDBW;
+  constexpr int NBUF = DecPipe<D>::NBUF;
   constexpr int KS = D / 16;       // MFMA k-steps of S^T
   constexpr int HD = D / 2;        // dims per lane half in S^T
-  constexpr int NDB = D / 32;      // 32-dim blocks of the output
   constexpr int CH = D / 8;        // 16-byte chunks per row
   constexpr int TILE = kDecTile * D;          // bf16 elements of one K (or V) tile
   constexpr int TILE_CH = kDecTile * CH;      // its 16-byte chunks
-  constexpr int NINS = TPS * 2 * TILE_CH / 64;  // wave-wide 16-byte loads per stage
+  constexpr int NINS = 2 * TILE_CH / 64;      // wave-wide 16-byte loads per stage
   constexpr int PERW = NINS >= NW ? NINS / NW : 1;  // of them per wave (or none)
   static_assert((NINS % NW == 0 || NINS < NW) && TILE_CH % 64 == 0, "stage split");
-  __shared__ __align__(16) uint16_t lds[NBUF][TPS][2][TILE];
+  __shared__ __align__(16) uint16_t lds[NBUF][2][TILE];
 
   // A persistent grid over the work items (unit, chunk), taken in a fixed
   // stride: consecutive chunks of a long segment go to different workgroups.
@@ -211,12 +211,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   if (c0 >= len) continue;  // whole workgroup: this unit has fewer chunks
   const int c1 = min(len, c0 + kDecKeys);
   const int ntiles = (c1 - c0 + kDecTile - 1) / kDecTile;
-  const int nstage = (ntiles + TPS - 1) / TPS;
   const int M = tq * g.G;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int qt = wave % NQT;        // query tile of this wave
-  const int kg = wave / NQT;        // its wave group over the key tiles
+  const int dsi = wave / NQT;       // its share of the output dims
+  const int db0 = dsi * NDBW;       // first 32-dim block of that share
   const int hh = lane >> 5;
   const int c32 = lane & 31;
   const int row = qt * 32 + c32;    // this lane's query row
@@ -229,38 +229,33 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   const uint16_t* kseg = kp + p0 * D;
   const uint16_t* vseg = vp + p0 * D;
   auto issue_stage = [&](int st) {
-    const int tile0 = st * TPS;
 #pragma unroll
     for (int i = 0; i < PERW; ++i) {
       const int n = wave * PERW + i;
-      const int tile = n / (2 * TILE_CH / 64);              // uniform over the wave
-      const int kv = (n / (TILE_CH / 64)) & 1;
-      if (n < NINS && tile0 + tile < ntiles) {
+      const int kv = n / (TILE_CH / 64);                    // uniform over the wave
+      if (n < NINS) {
         const int pos = (n % (TILE_CH / 64)) * 64 + lane;   // slot within the tile
         const int r = pos / CH;
         const int chunk = kv ? dec_swz_v<D>(r, pos % CH) : dec_swz_k<D>(r, pos % CH);
-        const int key = min(c0 + (tile0 + tile) * kDecTile + r, len - 1);
+        const int key = min(c0 + st * kDecTile + r, len - 1);
         const uint16_t* src = (kv ? vseg : kseg) + (int64_t)key * D + chunk * 8;
-        dec_dma16(src, dec_lds_addr(&lds[st % NBUF][tile][kv][(n % (TILE_CH / 64)) * 512]));
+        dec_dma16(src, dec_lds_addr(&lds[st % NBUF][kv][(n % (TILE_CH / 64)) * 512]));
       }
     }
   };
 
   DecFrag qf[KS];
   float m_run = -INFINITY, l_run = 0.f;
-  dec_f32x16 O[NDB];
+  dec_f32x16 O[NDBW];  // O^T of the wave's 32-dim blocks db0 ..
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int db = 0; db < NDBW; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) O[db][v] = 0.f;
 
-  // One key tile (stage buffer sb, slot j, first key t0) for this wave's
-  // query tile.
-  auto process_tile = [&](int sb, int j, int t0) {
-    const uint16_t* kt = lds[sb][j][0];
-    const uint16_t* vt = lds[sb][j][1];
-    // S^T = K Q^T: lane (hh, c32) holds query row c32 and keys
-    // 8*(v/4) + 4*hh + v%4 of the tile
+  // S^T = K Q^T of the key tile in stage buffer sb: lane (hh, c32) holds
+  // query row c32 and keys 8*(v/4) + 4*hh + v%4 of the tile.
+  auto score_tile = [&](int sb) {
+    const uint16_t* kt = lds[sb][0];
     dec_f32x16 s;
 #pragma unroll
     for (int v = 0; v < 16; ++v) s[v] = 0.f;
@@ -271,6 +266,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
                                              dec_swz_k<D>(c32, hh * (CH / 2) + ks) * 8);
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf.v, qf[ks].v, s, 0, 0, 0);
     }
+    return s;
+  };
+
+  // Softmax and O^T += V^T P^T of the tile (first key t0) whose scores are s.
+  auto finish_tile = [&](int sb, int t0, dec_f32x16 s) {
+    const uint16_t* vt = lds[sb][1];
     // Online softmax of the row in log2 units (z = c2 * s, c2 > 0, so the
     // maximum is taken on the raw products).  Keys past the chunk occur only
     // in its last tile.
@@ -299,7 +300,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
       m_run = mnew;
       l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDBW; ++db)
 #pragma unroll
         for (int v = 0; v < 16; ++v) O[db][v] *= alpha;
     }
@@ -329,12 +330,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
+      for (int db = 0; db < NDBW; ++db) {
         DecFrag vf;
 #pragma unroll
         for (int rd = 0; rd < 2; ++rd) {
           const int r = 16 * kk + 8 * rd + 4 * hh + (a >> 2);
-          const int dim = 32 * db + vdim;
+          const int dim = 32 * (db0 + db) + vdim;
           const uint16_t* src = vt + r * D + dec_swz_v<D>(r, dim >> 3) * 8 + (dim & 7);
           const dec_s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (dec_lds_s16x4*)(__attribute__((address_space(3))) uint16_t*)src);
@@ -346,13 +347,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
     }
   };
 
-  // Stage 0 and the query fragments are awaited together; then up to PD
-  // stages are in flight.  At the top of stage st each wave waits until its
-  // loads of st have landed: loads complete in order, so it may leave in
-  // flight those of the later stages already issued, counting only whole
-  // stages (a short last stage is waited for with the rest, which is safe).
-  // The barrier then publishes stage st and certifies that every wave is done
-  // with stage st - 1, whose buffer the loads of stage st + PD overwrite.
+  // Stage 0 and the query fragments are awaited together; then stages up to
+  // NBUF - 2 ahead of the one consumed are in flight.  Before stage st each
+  // wave waits until its own loads of st have landed (loads complete in
+  // order, so those of the later stages already issued may stay in flight);
+  // the barrier then publishes stage st and certifies that every wave is done
+  // with stage st - 1, whose buffer the loads of stage st + NBUF - 1
+  // overwrite.
   issue_stage(0);
   // The query row as B fragments of S^T (zero for padding rows); lane half hh
   // owns the dims hh*HD .. hh*HD + HD - 1 (the contraction order is free).
@@ -369,30 +370,25 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
   }
 
   dec_wait_vm0();
-  for (int st = 1; st < PD && st < nstage; ++st) issue_stage(st);
-  const bool short_last = (ntiles % TPS) != 0;
-  for (int st = 0; st < nstage; ++st) {
-    int ahead = min(PD - 1, nstage - 1 - st);         // later stages in flight
-    if (short_last && st + ahead == nstage - 1 && ahead > 0) --ahead;
-    dec_wait_stages<PERW, PD - 1>(ahead);
+  for (int st = 1; st < NBUF - 1 && st < ntiles; ++st) issue_stage(st);
+  for (int st = 0; st < ntiles; ++st) {
+    dec_wait_stages<PERW, NBUF - 2>(min(NBUF - 2, ntiles - 1 - st));
     __syncthreads();
-    if (st + PD < nstage) issue_stage(st + PD);
-    for (int j = kg; j < TPS; j += KG) {
-      const int t0 = c0 + (st * TPS + j) * kDecTile;
-      if (t0 < c1) process_tile(st % NBUF, j, t0);
-    }
+    if (st + NBUF - 1 < ntiles) issue_stage(st + NBUF - 1);
+    finish_tile(st % NBUF, c0 + st * kDecTile, score_tile(st % NBUF));
   }
-
-  // partials of this chunk and wave group: the row's (max, sum) and
-  // unnormalized output (a group without tiles leaves max -inf, sum 0)
+  // partials of this chunk: the row's (max, sum), from the first wave of the
+  // query tile (every wave of it holds the same), and the unnormalized output
+  // of each wave's dims
   const float l_row = l_run + __shfl_xor(l_run, 32, 64);
-  const int64_t pr = ((int64_t)u * nsub + split * KG + kg) * mp + row;
-  if (hh == 0) part_ml[pr] = make_float2(m_run, l_row);
+  const int64_t pr = ((int64_t)u * nsplit + split) * mp + row;
+  if (dsi == 0 && hh == 0) part_ml[pr] = make_float2(m_run, l_row);
   float* po = part_o + pr * D;
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+  for (int db = 0; db < NDBW; ++db)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) po[32 * db + 8 * (v >> 2) + 4 * hh + (v & 3)] = O[db][v];
+    for (int v = 0; v < 16; ++v)
+      po[32 * (db0 + db) + 8 * (v >> 2) + 4 * hh + (v & 3)] = O[db][v];
   __syncthreads();  // every wave is done with the stage buffers of this item
   }
 }
@@ -401,13 +397,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
 // partial slots dealt round-robin to groups of D/4 threads (four output dims
 // per thread, 16-byte loads).  Each group folds its slots in order with an
 // online maximum; the groups are then merged in group order through LDS, so
-// the result does not depend on timing.  Slots of wave groups that saw no
-// key carry max -inf and are skipped.
+// the result does not depend on timing.
 constexpr int kCombThreads = 256;
 
 template <int D>
 __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
-    Geo g, int32_t tq, int32_t nsub, int32_t kgroups, int32_t mp, const int64_t* __restrict__ poff,
+    Geo g, int32_t tq, int32_t nsplit, int32_t mp, const int64_t* __restrict__ poff,
     const float* __restrict__ part_o, const float2* __restrict__ part_ml, float* __restrict__ out,
     float* __restrict__ lse) {
   constexpr int C4 = D / 4;                // threads per slot row
@@ -419,9 +414,9 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
   const int sg = threadIdx.x / C4;
   const int c4 = threadIdx.x % C4;
   const int len = (int)(poff[u + 1] - poff[u]);
-  const int nv = min(nsub, kgroups * ((len + kDecKeys - 1) / kDecKeys));
-  if (len > (nsub / kgroups) * kDecKeys && row == 0 && threadIdx.x == 0) report_range(g);
-  const int64_t base = (int64_t)u * nsub * mp + row;  // + slot * mp
+  const int nv = min(nsplit, (len + kDecKeys - 1) / kDecKeys);
+  if (len > nsplit * kDecKeys && row == 0 && threadIdx.x == 0) report_range(g);
+  const int64_t base = (int64_t)u * nsplit * mp + row;  // + slot * mp
   float m = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   auto fold = [&](float2 ml, float4 o) {
@@ -487,11 +482,9 @@ template <int D, int NQT>
 static certkv_status launch_decode(const DecodeArgs& a, hipStream_t s) {
   const Geo& g = a.g;
   const int mp = NQT * 32;
-  constexpr int KG = DecShape<NQT>::KG;
-  const int nsub = a.nsplit * KG;
   // as many workgroups as stay resident at once (the occupancy query is made
   // once per device and kernel instance)
-  constexpr int NT = 64 * DecShape<NQT>::NW;
+  constexpr int NT = 64 * DecShape<D, NQT>::NW;
   static std::atomic<int> per_cu[kMaxDevices];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CERTKV_EHIP;
@@ -514,12 +507,12 @@ static certkv_status launch_decode(const DecodeArgs& a, hipStream_t s) {
   CERTKV_LAUNCH("decode_items", decode_items_kernel, dim3(1), dim3(kItemThreads), 0, s, a.U,
                 a.nsplit, a.packed_offsets, a.items, a.item_count);
   CERTKV_LAUNCH("decode", (decode_kernel<D, NQT>), dim3(grid), dim3(NT), 0, s, g, a.items,
-                a.item_count, a.tq, nsub, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
+                a.item_count, a.tq, a.nsplit, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
                 a.packed_offsets, a.part_o, a.part_ml);
   const int M = a.tq * g.G;
   CERTKV_LAUNCH("decode_combine", decode_combine_kernel<D>, dim3((unsigned)a.U, (unsigned)M),
                 dim3(kCombThreads), 0, s,
-                g, a.tq, nsub, KG, mp, a.packed_offsets, (const float*)a.part_o,
+                g, a.tq, a.nsplit, mp, a.packed_offsets, (const float*)a.part_o,
                 (const float2*)a.part_ml, a.out, a.lse);
   return CERTKV_OK;
 }
@@ -540,9 +533,7 @@ certkv_status run_decode(const DecodeArgs& a, hipStream_t s) {
 }
 
 size_t decode_partial_rows(int64_t U, int nsplit, int tq, int G) {
-  const int nqt = decode_nqt(tq * G);
-  const int kg = nqt < 4 ? 4 / nqt : 1;  // wave groups per workgroup (DecShape)
-  return (size_t)U * nsplit * kg * nqt * 32;
+  return (size_t)U * nsplit * decode_nqt(tq * G) * 32;
 }
 
 int decode_nsplit(int max_len) { return (max_len + kDecKeys - 1) / kDecKeys; }

@@ -75,11 +75,23 @@ def _check_against_oracle(cfg, cache, spec, bufs, tq, seed_offset=7919):
     return out
 
 
-@pytest.mark.parametrize("tq", [1, 8, 33])
+@pytest.mark.parametrize("tq", [1, 8, 33, 65])
 def test_decode_matches_oracle_ragged_batch(tq):
     # ragged lengths (several 1024-key chunks and a ragged last tile), two
-    # layers; tq = 33 gives 132 query rows: a padded fifth 32-row tile
+    # layers; tq = 33 gives 132 query rows (a padded fifth 32-row tile), tq = 65
+    # gives 260 rows (sixteen query tiles, the largest workgroup)
     cfg = synth.config("C4", seqlens=[3000, 8192 + 5, 1024], layers=2)
+    cache = synth.make_cache(cfg, "cpu")
+    spec, bufs = _compress(cfg, cache)
+    _check_against_oracle(cfg, cache, spec, bufs, tq)
+
+
+@pytest.mark.parametrize("tq", [1, 40, 130])
+def test_decode_head_dim_64_without_grouping(tq):
+    # head_dim 64, one query head per KV head (G = 1): one, two and eight
+    # query tiles (the first two split the output dims over two waves)
+    cfg = synth.config("C1", seqlens=[3000, 1500])
+    cfg.dtype = torch.bfloat16
     cache = synth.make_cache(cfg, "cpu")
     spec, bufs = _compress(cfg, cache)
     _check_against_oracle(cfg, cache, spec, bufs, tq)
