@@ -300,7 +300,8 @@ def main():
         return
     if args.summarize_traffic:
         fc, wc, rx, kn, out, c1, c2 = args.summarize_traffic
-        summarize_traffic(fc, wc, rx, kn, args.config, out, [c1, c2])
+        workload = args.config + (f"-decode{args.tq}" if args.decode else "")
+        summarize_traffic(fc, wc, rx, kn, workload, out, [c1, c2])
         return
 
     def log(msg):
@@ -330,18 +331,18 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream(dev)
-    if args.decode:
-        run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log)
-        return
     if args.calibrate_copy:
         # A plain device copy of known size: its FETCH_SIZE / WRITE_SIZE
-        # readings scale the counters of the pass's kernels to bytes.
+        # readings scale the counters of the timed kernels to bytes.
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.decode:
+        run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log)
+        return
     for _ in range(args.warmup):
         ck.compress(spec, q, k, v, n_keep, bufs=bufs)
     torch.cuda.synchronize()
