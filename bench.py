@@ -209,6 +209,62 @@ def summarize_traffic(fetch_csv, write_csv, kernel_regex, kernel, workload, out,
         fh.write("\n".join(lines) + "\n")
 
 
+def lift_diagnostic(cfg, cache, bufs, qn, out, tq, layers):
+    """The future-query lift theorem's a-posteriori bound on a sample of the
+    decode: for each sampled (layer, head) and new query row, the exact output
+    O over the uncompressed cache (torch fp64 on the GPU, beside the HIP path),
+    the decode output Ohat, and the bound V_max (2 |p - q| + min(p, q)
+    |a - r|_1) + q |v*_stored - sum_E r v| (the last term: the bf16 rounding of
+    the stored slot value), with p = sigmoid(Lambda_E - log Z_S), q =
+    sigmoid(z* - log Z_S), a the query's attention over the evicted set E and r
+    the slot's charge (the clipped window scores over E, normalized)."""
+    import torch
+    H, G, D = cfg.kv_heads, cfg.group, cfg.head_dim
+    n = cfg.seqlens[0]
+    scale = 1.0 / math.sqrt(D)
+    ko = bufs.kept_offsets.cpu()
+    po = bufs.packed_offsets.cpu()
+    ratios, errs, bounds, ps, qs = [], [], [], [], []
+    for li in layers:
+        for h in range(H):
+            u = li * H + h  # one sequence
+            K = cache["k"][li, :n, h].double()
+            V = cache["v"][li, :n, h].double()
+            Q = qn[li, :tq, h * G:(h + 1) * G].double().reshape(-1, D)
+            Z = torch.matmul(Q, K.t().contiguous()) * scale
+            kept = torch.zeros(n, dtype=torch.bool, device=K.device)
+            kept[bufs.kept_idx[int(ko[u]):int(ko[u + 1])].long()] = True
+            ev = ~kept
+            r = torch.clamp(bufs.scores[li, h, :n].double(), min=0.0)[ev]
+            r = r / r.sum()
+            o_full = torch.matmul(torch.softmax(Z, dim=1), V)
+            o_hat = out[li, :tq, h * G:(h + 1) * G].double().reshape(-1, D)
+            err = torch.linalg.vector_norm(o_full - o_hat, dim=1)
+            lam_e = torch.logsumexp(Z[:, ev], dim=1)
+            log_zs = torch.logsumexp(Z[:, kept], dim=1)
+            slot = int(po[u + 1]) - 1
+            zstar = torch.matmul(Q, bufs.k_packed[slot].double()) * scale
+            p = torch.sigmoid(lam_e - log_zs)
+            q = torch.sigmoid(zstar - log_zs)
+            l1 = (torch.softmax(Z[:, ev], dim=1) - r).abs().sum(dim=1)
+            vmax = torch.linalg.vector_norm(V, dim=1).max()
+            slack = q * torch.linalg.vector_norm(bufs.v_packed[slot].double() - r @ V[ev])
+            bound = vmax * (2 * (p - q).abs() + torch.minimum(p, q) * l1) + slack
+            ratios.append(err / bound)
+            errs.append(err)
+            bounds.append(bound)
+            ps.append(p)
+            qs.append(q)
+    cat = lambda xs: torch.cat(xs).cpu()
+    ratio, err, bound, p, q = cat(ratios), cat(errs), cat(bounds), cat(ps), cat(qs)
+    return {"sample": f"layers {list(layers)}, {H} KV heads, {tq * G} new query rows each; "
+                      "exact attention over the uncompressed cache in torch fp64",
+            "rows": int(ratio.numel()), "holds": float((ratio <= 1.0).double().mean()),
+            "ratio_median": float(ratio.median()), "ratio_max": float(ratio.max()),
+            "err_median": float(err.median()), "bound_median": float(bound.median()),
+            "p_median": float(p.median()), "q_median": float(q.median())}
+
+
 def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
     """Decode over the packed cache: one compression pass (untimed) builds it,
     then `steps` decodes of `tq` new queries per sequence are timed.  The
@@ -260,6 +316,16 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
     ms, kern, roof = time_tq(args.tq, args.steps, args.warmup)
     ms1, kern1, roof1 = time_tq(1, args.steps, args.warmup)
     log(f"decode tq={args.tq}: {ms:.3f} ms; tq=1: {ms1:.3f} ms")
+    lift = None
+    if cfg.batch == 1:
+        qn = synth.make_queries(cfg, args.tq, dev)
+        out = ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, args.tq,
+                        max_rows=max_rows)
+        torch.cuda.synchronize()
+        lift = lift_diagnostic(cfg, cache, bufs, qn, out, args.tq,
+                               sorted({0, cfg.layers - 1}))
+        log(f"lift bound: holds on {lift['holds']:.4f} of {lift['rows']} rows, "
+            f"median ratio {lift['ratio_median']:.3g}")
     tokens = cfg.batch * args.tq
     rec = {
         "metric": "decode over the packed cache: new tokens per second (all layers and heads)",
@@ -272,6 +338,7 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
                    "tq": args.tq, "packed_rows": rows, "max_segment_rows": max_rows},
         "roofline": roof, "kernels": kern,
         "tq1": {"ms_per_step": ms1, "roofline": roof1, "kernels": kern1},
+        "lift_bound": lift,
     }
     print(json.dumps(rec), flush=True)
 

@@ -97,6 +97,17 @@ def test_decode_head_dim_64_without_grouping(tq):
     _check_against_oracle(cfg, cache, spec, bufs, tq)
 
 
+@pytest.mark.parametrize("tq", [1, 16])
+def test_decode_cancelling_pairs(tq):
+    # the 70B-class shape (G = 8) with 256 cancelling value pairs per head:
+    # evicted pairs whose values cancel leave a slot value near zero while
+    # their keys keep mass; decode over that cache against the oracle
+    cfg = synth.config("C5", seqlens=[6000, 2500], layers=1)
+    cache = synth.make_cache(cfg, "cpu")
+    spec, bufs = _compress(cfg, cache)
+    _check_against_oracle(cfg, cache, spec, bufs, tq)
+
+
 def test_keep_all_decode_equals_full_attention():
     # n_keep = n: every head keeps n - 1 real rows and its slot is the one
     # evicted key itself, so decode over the packed cache is exact attention
@@ -122,11 +133,12 @@ def test_keep_all_decode_equals_full_attention():
             assert _row_err(got[r], ref[r]) <= OUT_RTOL, (h, r)
 
 
-def test_future_query_lift_bound_on_gpu_outputs():
+@pytest.mark.parametrize("name", ["C2", "C5"])
+def test_future_query_lift_bound_on_gpu_outputs(name):
     # The a-posteriori bound of the future-query lift theorem with the GPU's
     # compressed output: ||O - Ohat|| <= V_max (2 |p - q| + min(p, q) ||a - r||_1)
     # + q ||v*_stored - sum_T r_j v_j|| (the stored slot is rounded to bf16).
-    cfg = synth.config("C2", seqlens=[4000])
+    cfg = synth.config(name, seqlens=[4000], layers=1)
     cache = synth.make_cache(cfg, "cpu")
     spec, bufs = _compress(cfg, cache)
     tq = 4
