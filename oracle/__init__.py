@@ -65,6 +65,13 @@ def lib():
         L.ora_compress_block.argtypes = [
             _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _dbl, _i32, _i64, _dbl,
             _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
+        L.ora_curves_stat.argtypes = [_i64, _i32, _p, _p, _p, _i32, _p, _p]
+        L.ora_budget_params_slot.argtypes = [_i32, _i64, _i64, _dbl, _i32, _p, _p]
+        L.ora_allocate_variant.argtypes = [_i32, _i64, _p, _i64, _dbl, _i32, _i32, _i32, _p,
+                                           _p, _p]
+        L.ora_compress_block_variant.argtypes = [
+            _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _dbl, _i32, _i64, _dbl,
+            _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
         L.ora_num_threads.restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -128,22 +135,34 @@ def normalize(s32):
     return a
 
 
-def curves(s32, perm, v):
-    """Returns (c fp64, c32 fp32) over b = 0..n-1."""
+STATISTICS = {"centered": 0, "uncentered": 1, "tail_mass": 2}
+ALLOCATORS = ("lagrangian", "uniform", "greedy")
+
+
+def curves(s32, perm, v, statistic="centered"):
+    """Returns (c fp64, c32 fp32) over b = 0..n-1; statistic is the centered
+    dispersion (default), the uncentered one or the tail mass."""
     s32, perm, v = _f32(s32), _i32a(perm), _f64(v)
     n, d = v.shape
     c = np.zeros(n, np.float64)
     c32 = np.zeros(n, np.float32)
-    _check(lib().ora_curves(n, d, _ptr(s32), _ptr(perm), _ptr(v), _ptr(c), _ptr(c32)),
-           "curves")
+    if statistic == "centered":
+        st = lib().ora_curves(n, d, _ptr(s32), _ptr(perm), _ptr(v), _ptr(c), _ptr(c32))
+    else:
+        st = lib().ora_curves_stat(n, d, _ptr(s32), _ptr(perm), _ptr(v),
+                                   STATISTICS[statistic], _ptr(c), _ptr(c32))
+    _check(st, "curves")
     return c, c32
 
 
-def budget_params(H, n, n_keep, alpha=0.2):
+def budget_params(H, n, n_keep, alpha=0.2, slot=True):
     br = np.zeros(1, np.int64)
     bm = np.zeros(1, np.int64)
-    _check(lib().ora_budget_params(H, n, n_keep, float(alpha), _ptr(br), _ptr(bm)),
-           "budget_params")
+    if slot:
+        st = lib().ora_budget_params(H, n, n_keep, float(alpha), _ptr(br), _ptr(bm))
+    else:
+        st = lib().ora_budget_params_slot(H, n, n_keep, float(alpha), 0, _ptr(br), _ptr(bm))
+    _check(st, "budget_params")
     return int(br[0]), int(bm[0])
 
 
@@ -152,15 +171,27 @@ def argmin_penalized(c32, lo, hi, lam):
     return int(lib().ora_argmin_penalized(_ptr(c32), lo, hi, float(lam)))
 
 
-def allocate(c32, n_keep, alpha=0.2, steps=40, with_lambda=False):
-    """c32 [H][n] fp32 -> (budgets [H], repairs[, (lambda_lo, lambda_hi)])."""
+def allocate(c32, n_keep, alpha=0.2, steps=40, with_lambda=False, allocator="lagrangian",
+             slot=True):
+    """c32 [H][n] fp32 -> (budgets [H], repairs[, (lambda_lo, lambda_hi)]).
+    allocator: "lagrangian" (bisection + repair), "uniform" (B_real / H each)
+    or "greedy" (the repair from b_min, i.e. no bisection step); slot=False
+    is the no-slot budget algebra."""
     c32 = _f32(c32)
     H, n = c32.shape
     b = np.zeros(H, np.int32)
     rep = np.zeros(1, np.int64)
     lam = np.zeros(2, np.float64)
-    _check(lib().ora_allocate(H, n, _ptr(c32), n_keep, float(alpha), steps, _ptr(b),
-                              _ptr(rep), _ptr(lam)), "allocate")
+    assert allocator in ALLOCATORS
+    if allocator == "lagrangian" and slot:
+        st = lib().ora_allocate(H, n, _ptr(c32), n_keep, float(alpha), steps, _ptr(b),
+                                _ptr(rep), _ptr(lam))
+    else:
+        st = lib().ora_allocate_variant(H, n, _ptr(c32), n_keep, float(alpha),
+                                        0 if allocator == "greedy" else steps, int(slot),
+                                        int(allocator == "uniform"), _ptr(b), _ptr(rep),
+                                        _ptr(lam))
+    _check(st, "allocate")
     if with_lambda:
         return b, int(rep[0]), (float(lam[0]), float(lam[1]))
     return b, int(rep[0])
@@ -211,8 +242,16 @@ def row_error(A, V, kept_mask, u=None):
                                      _ptr(uu)))
 
 
+def variant_bits(statistic="centered", allocator="lagrangian", slot=True):
+    """The oracle's variant bit mask of a one-factor ablation."""
+    assert statistic in STATISTICS and allocator in ALLOCATORS
+    return ((1 if statistic == "uncentered" else 2 if statistic == "tail_mass" else 0)
+            | (4 if allocator == "uniform" else 8 if allocator == "greedy" else 0)
+            | (0 if slot else 16))
+
+
 def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32_in=None,
-                   keep_window=False):
+                   keep_window=False, statistic="centered", allocator="lagrangian", slot=True):
     """One (layer, sequence) block end to end.
 
     q [w][H*G][d], k/v [n][H][d] (any float dtype; converted to fp64 exactly).
@@ -237,12 +276,22 @@ def compress_block(q, k, v, n_keep, scale, causal=True, alpha=0.2, steps=40, s32
     m = np.zeros(H, np.float64)
     rep = np.zeros(1, np.int64)
     sin = _f32(s32_in) if s32_in is not None else None
-    _check(lib().ora_compress_block(
-        n, H, G, d, w, _ptr(q), _ptr(k), _ptr(v), float(scale), int(bool(causal)),
-        int(n_keep), float(alpha), int(steps), int(bool(keep_window)), _ptr(sin), _ptr(s),
-        _ptr(s32), _ptr(perm),
-        _ptr(c32), _ptr(b), _ptr(kept), _ptr(kept_off), _ptr(ks), _ptr(vs), _ptr(m),
-        _ptr(rep)), "compress_block")
+    var = variant_bits(statistic, allocator, slot)
+    if var == 0:
+        st = lib().ora_compress_block(
+            n, H, G, d, w, _ptr(q), _ptr(k), _ptr(v), float(scale), int(bool(causal)),
+            int(n_keep), float(alpha), int(steps), int(bool(keep_window)), _ptr(sin), _ptr(s),
+            _ptr(s32), _ptr(perm),
+            _ptr(c32), _ptr(b), _ptr(kept), _ptr(kept_off), _ptr(ks), _ptr(vs), _ptr(m),
+            _ptr(rep))
+    else:
+        st = lib().ora_compress_block_variant(
+            n, H, G, d, w, _ptr(q), _ptr(k), _ptr(v), float(scale), int(bool(causal)),
+            int(n_keep), float(alpha), int(steps), int(bool(keep_window)), var, _ptr(sin),
+            _ptr(s), _ptr(s32), _ptr(perm),
+            _ptr(c32), _ptr(b), _ptr(kept), _ptr(kept_off), _ptr(ks), _ptr(vs), _ptr(m),
+            _ptr(rep))
+    _check(st, "compress_block")
     return dict(s=s, s32=s32, perm=perm, c32=c32, budgets=b,
                 kept=[kept[kept_off[h]:kept_off[h + 1]].copy() for h in range(H)],
                 k_star=ks, v_star=vs, tail_mass=m, repairs=int(rep[0]))

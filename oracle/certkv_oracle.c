@@ -36,6 +36,23 @@
 #define ORA_ENONFINITE -4
 #define ORA_ENOMEM -7
 
+int ora_curves_stat(int64_t n, int32_t d, const float* s32, const int32_t* perm,
+                    const double* v, int32_t stat, double* c, float* c32);
+int ora_budget_params_slot(int32_t H, int64_t n, int64_t n_keep, double alpha,
+                           int32_t slot, int64_t* B_real, int64_t* b_min);
+int ora_allocate_variant(int32_t H, int64_t n, const float* c32, int64_t n_keep,
+                         double alpha, int32_t T, int32_t slot, int32_t uniform,
+                         int32_t* b, int64_t* repairs, double* lam);
+int ora_compress_block_variant(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
+                               const double* q, const double* k, const double* v,
+                               double scale, int32_t causal, int64_t n_keep,
+                               double alpha, int32_t T, int32_t keep_window,
+                               int32_t variant, const float* s32_in,
+                               double* s, float* s32, int32_t* perm, float* c32,
+                               int32_t* b, int32_t* kept, int64_t* kept_off,
+                               double* kstar, double* vstar, double* m,
+                               int64_t* repairs);
+
 /* ------------------------------------------------------------------------ */
 /* Scores.  Section 3, one-row setup: A_j = exp(l_j) / sum_t exp(l_t) with
  * l_j = <q, k_j> / sqrt(d).  The window scorer sums the softmax weights of
@@ -156,6 +173,16 @@ int ora_normalize(int64_t n, const float* s32, double* a) {
  *   may be NULL). */
 int ora_curves(int64_t n, int32_t d, const float* s32, const int32_t* perm,
                const double* v, double* c, float* c32) {
+  return ora_curves_stat(n, d, s32, perm, v, 0, c, c32);
+}
+
+/* The statistics of the one-factor ablations (appendix, one-factor ablations
+ * table): stat 0 is the centered dispersion above (the default), stat 1 the
+ * uncentered dispersion sqrt(m(b) Q(b)) and stat 2 the tail mass m(b), on the
+ * same suffix sums. */
+int ora_curves_stat(int64_t n, int32_t d, const float* s32, const int32_t* perm,
+                    const double* v, int32_t stat, double* c, float* c32) {
+  if (stat < 0 || stat > 2) return ORA_EINVAL;
   if (n <= 0 || d <= 0) return ORA_EINVAL;
   double* a = (double*)malloc(sizeof(double) * (size_t)n);
   double* W = (double*)calloc((size_t)d, sizeof(double));
@@ -181,8 +208,13 @@ int ora_curves(int64_t n, int32_t d, const float* s32, const int32_t* perm,
     for (int32_t t = 0; t < d; ++t) W[t] += a[j] * vj[t];
     double w2 = 0.0;
     for (int32_t t = 0; t < d; ++t) w2 += W[t] * W[t];
-    double c2 = m * Q - w2;
-    double cb = sqrt(c2 > 0.0 ? c2 : 0.0);
+    double cb;
+    if (stat == 2) {
+      cb = m;
+    } else {
+      double c2 = stat == 1 ? m * Q : m * Q - w2;
+      cb = sqrt(c2 > 0.0 ? c2 : 0.0);
+    }
     if (c) c[b] = cb;
     if (c32) c32[b] = (float)cb;
   }
@@ -197,9 +229,22 @@ int ora_curves(int64_t n, int32_t d, const float* s32, const int32_t* perm,
  * max{1, floor(alpha B_real / H)}; feasible iff 2 <= n_keep <= n. */
 int ora_budget_params(int32_t H, int64_t n, int64_t n_keep, double alpha,
                       int64_t* B_real, int64_t* b_min) {
+  return ora_budget_params_slot(H, n, n_keep, alpha, 1, B_real, b_min);
+}
+
+/* The same algebra with or without the slot.  Without it (the no-slot
+ * ablation: the slot's live row goes to one more real token per head) all
+ * H n_keep live rows are real: B_real = H n_keep, feasible iff
+ * 1 <= n_keep <= n - 1 (a head keeps at most n - 1 keys). */
+int ora_budget_params_slot(int32_t H, int64_t n, int64_t n_keep, double alpha,
+                           int32_t slot, int64_t* B_real, int64_t* b_min) {
   if (H <= 0 || n <= 0) return ORA_EINVAL;
-  if (n_keep < 2 || n_keep > n) return ORA_EINFEASIBLE;
-  int64_t br = (int64_t)H * n_keep - H;
+  if (slot) {
+    if (n_keep < 2 || n_keep > n) return ORA_EINFEASIBLE;
+  } else {
+    if (n_keep < 1 || n_keep > n - 1) return ORA_EINFEASIBLE;
+  }
+  int64_t br = (int64_t)H * n_keep - (slot ? H : 0);
   int64_t bm = (int64_t)floor(alpha * (double)br / (double)H);
   if (bm < 1) bm = 1;
   if (bm > n - 1 || (int64_t)H * bm > br) return ORA_EINFEASIBLE;
@@ -231,9 +276,26 @@ int64_t ora_argmin_penalized(const float* c32, int64_t lo, int64_t hi,
 int ora_allocate(int32_t H, int64_t n, const float* c32, int64_t n_keep,
                  double alpha, int32_t T, int32_t* b, int64_t* repairs,
                  double* lam) {
+  return ora_allocate_variant(H, n, c32, n_keep, alpha, T, 1, 0, b, repairs, lam);
+}
+
+/* The allocators of the one-factor ablations: uniform != 0 gives every head
+ * the same B_real / H (which the budget algebra makes whole: n_keep - 1 with
+ * the slot, n_keep without); otherwise the Lagrangian allocation with repair
+ * above, where T = 0 is the greedy-marginal allocator (every head at b_min,
+ * then one token at a time to the smallest marginal). */
+int ora_allocate_variant(int32_t H, int64_t n, const float* c32, int64_t n_keep,
+                         double alpha, int32_t T, int32_t slot, int32_t uniform,
+                         int32_t* b, int64_t* repairs, double* lam) {
   int64_t B_real, b_min;
-  int st = ora_budget_params(H, n, n_keep, alpha, &B_real, &b_min);
+  int st = ora_budget_params_slot(H, n, n_keep, alpha, slot, &B_real, &b_min);
   if (st != ORA_OK) return st;
+  if (uniform) {
+    for (int32_t h = 0; h < H; ++h) b[h] = (int32_t)(B_real / H);
+    if (repairs) *repairs = 0;
+    if (lam) lam[0] = lam[1] = 0.0;
+    return ORA_OK;
+  }
   double cmax = 0.0;
   for (int32_t h = 0; h < H; ++h)
     for (int64_t j = 0; j < n; ++j) {
@@ -455,11 +517,33 @@ int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
                        int32_t* b, int32_t* kept, int64_t* kept_off,
                        double* kstar, double* vstar, double* m,
                        int64_t* repairs) {
+  return ora_compress_block_variant(n, H, G, d, w, q, k, v, scale, causal, n_keep, alpha, T,
+                                    keep_window, 0, s32_in, s, s32, perm, c32, b, kept,
+                                    kept_off, kstar, vstar, m, repairs);
+}
+
+/* The whole block under a one-factor ablation.  variant bits: 1 uncentered
+ * statistic, 2 tail-mass statistic, 4 uniform allocator, 8 greedy-marginal
+ * allocator (T = 0), 16 no slot (B_real = H n_keep; the tail summary is still
+ * formed, the packed cache would hold no slot row). */
+int ora_compress_block_variant(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
+                               const double* q, const double* k, const double* v,
+                               double scale, int32_t causal, int64_t n_keep,
+                               double alpha, int32_t T, int32_t keep_window,
+                               int32_t variant, const float* s32_in,
+                               double* s, float* s32, int32_t* perm, float* c32,
+                               int32_t* b, int32_t* kept, int64_t* kept_off,
+                               double* kstar, double* vstar, double* m,
+                               int64_t* repairs) {
   if (w > n || w <= 0) return ORA_EINVAL;
+  if ((variant & 3) == 3 || (variant & 12) == 12 || (variant & ~31)) return ORA_EINVAL;
+  const int32_t stat = (variant & 1) ? 1 : (variant & 2) ? 2 : 0;
+  const int32_t slot = (variant & 16) ? 0 : 1;
+  if (variant & 8) T = 0;
   int32_t M = w * G;
   int err = ORA_OK;
   int64_t B_real, b_min;
-  int st = ora_budget_params(H, n, n_keep, alpha, &B_real, &b_min);
+  int st = ora_budget_params_slot(H, n, n_keep, alpha, slot, &B_real, &b_min);
   if (st != ORA_OK) return st;
   /* with the window kept, every head must be able to hold it */
   if (keep_window && b_min < w) return ORA_EINFEASIBLE;
@@ -501,8 +585,8 @@ int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
       lerr = ora_order_window(n, s32 + (size_t)h * n, keep_window ? w : 0,
                               perm + (size_t)h * n);
     if (lerr == ORA_OK)
-      lerr = ora_curves(n, d, s32 + (size_t)h * n, perm + (size_t)h * n, vh,
-                        NULL, c32 + (size_t)h * n);
+      lerr = ora_curves_stat(n, d, s32 + (size_t)h * n, perm + (size_t)h * n, vh,
+                             stat, NULL, c32 + (size_t)h * n);
     free(kh);
     free(vh);
     free(qh);
@@ -513,7 +597,8 @@ int ora_compress_block(int64_t n, int32_t H, int32_t G, int32_t d, int32_t w,
     }
   }
   if (err != ORA_OK) return err;
-  err = ora_allocate(H, n, c32, n_keep, alpha, T, b, repairs, NULL);
+  err = ora_allocate_variant(H, n, c32, n_keep, alpha, T, slot, (variant & 4) != 0, b,
+                             repairs, NULL);
   if (err != ORA_OK) return err;
   kept_off[0] = 0;
   for (int32_t h = 0; h < H; ++h) kept_off[h + 1] = kept_off[h] + b[h];
