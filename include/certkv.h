@@ -76,7 +76,7 @@ enum { CERTKV_F32 = 0, CERTKV_BF16 = 1 };
 enum {
   CERTKV_CAUSAL = 1u << 0,  /* window rows see only keys at or before them  */
   CERTKV_DRY_RUN = 1u << 1, /* validate arguments, launch nothing           */
-  CERTKV_KEEP_WINDOW = 1u << 2  /* the w window keys of each sequence take  */
+  CERTKV_KEEP_WINDOW = 1u << 2, /* the w window keys of each sequence take  */
                             /* ranks 0..w-1 (ascending position), as if     */
                             /* their scores were +infinity, so every head   */
                             /* keeps them; their masses a_j are unchanged.  */
@@ -86,6 +86,20 @@ enum {
                             /* coverage budgets are at least w.  The paper  */
                             /* ranks all n keys (the default); this is the  */
                             /* option of never evicting the window.         */
+  /* One-factor ablations of the appendix (one-factor ablations table),
+   * each changing one design choice of the default pass:                    */
+  CERTKV_STAT_UNCENTERED = 1u << 3, /* curves c(b) = sqrt(m Q), no centering */
+  CERTKV_STAT_TAIL_MASS = 1u << 4,  /* curves c(b) = m(b), the tail mass     */
+  CERTKV_ALLOC_UNIFORM = 1u << 5,   /* true uniform: b_h = B_real / H        */
+  CERTKV_ALLOC_GREEDY = 1u << 6,    /* greedy marginal: no bisection step,   */
+                                    /* the repair from b_min (steps ignored) */
+  CERTKV_NO_SLOT = 1u << 7          /* no tail-summary row: its live slot is */
+                                    /* one more real token per head, B_real  */
+                                    /* = H n_keep with 1 <= n_keep <= n - 1; */
+                                    /* k*, v* are still formed, the packed   */
+                                    /* segments hold the b_h kept rows only  */
+  /* The two statistic flags, or the two allocator flags, together are
+   * CERTKV_EINVAL. */
 };
 
 /* Selection modes of certkv_select. */

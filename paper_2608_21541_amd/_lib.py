@@ -24,6 +24,11 @@ CERTKV_BF16 = 1
 CERTKV_CAUSAL = 1
 CERTKV_DRY_RUN = 2
 CERTKV_KEEP_WINDOW = 4
+CERTKV_STAT_UNCENTERED = 1 << 3
+CERTKV_STAT_TAIL_MASS = 1 << 4
+CERTKV_ALLOC_UNIFORM = 1 << 5
+CERTKV_ALLOC_GREEDY = 1 << 6
+CERTKV_NO_SLOT = 1 << 7
 CERTKV_SELECT_BUDGET = 0
 CERTKV_SELECT_COVERAGE = 1
 

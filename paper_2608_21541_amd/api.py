@@ -29,6 +29,12 @@ class ProblemSpec:
     causal: bool = True
     dry_run: bool = False
     keep_window: bool = False   # window keys ranked first, never evicted
+    # one-factor ablations: "centered" | "uncentered" | "tail_mass";
+    # "lagrangian" | "uniform" | "greedy"; slot=False gives the slot's row to
+    # one more real token per head
+    statistic: str = "centered"
+    allocator: str = "lagrangian"
+    slot: bool = True
     status: Optional[torch.Tensor] = None  # device int32 [1]: CERTKV_ENONFINITE on non-finite input
     _cu: object = field(default=None, repr=False)
 
@@ -56,7 +62,12 @@ class ProblemSpec:
         dt = _dtype_code(self.dtype)
         flags = (_lib.CERTKV_CAUSAL if self.causal else 0) | (
             _lib.CERTKV_DRY_RUN if self.dry_run else 0) | (
-            _lib.CERTKV_KEEP_WINDOW if self.keep_window else 0)
+            _lib.CERTKV_KEEP_WINDOW if self.keep_window else 0) | {
+            "centered": 0, "uncentered": _lib.CERTKV_STAT_UNCENTERED,
+            "tail_mass": _lib.CERTKV_STAT_TAIL_MASS}[self.statistic] | {
+            "lagrangian": 0, "uniform": _lib.CERTKV_ALLOC_UNIFORM,
+            "greedy": _lib.CERTKV_ALLOC_GREEDY}[self.allocator] | (
+            0 if self.slot else _lib.CERTKV_NO_SLOT)
         st = self.status.data_ptr() if self.status is not None else None
         return _lib.Problem(self.layers, self.batch, self.kv_heads, self.group, self.head_dim,
                             self.window, ctypes.cast(self._cu, ctypes.POINTER(ctypes.c_int64)),
@@ -218,7 +229,7 @@ def compact(spec: ProblemSpec, k, v, kept_offsets, kept_idx, k_star, v_star):
     """(k_packed, v_packed [rows][d], pos_packed [rows], packed_offsets [U+1])."""
     L = _lib.lib()
     dev = k.device
-    rows = int(kept_offsets[-1].item()) + spec.units
+    rows = int(kept_offsets[-1].item()) + (spec.units if spec.slot else 0)
     k_packed = torch.empty((rows, spec.head_dim), dtype=k.dtype, device=dev)
     v_packed = torch.empty_like(k_packed)
     pos_packed = torch.empty(rows, dtype=torch.int32, device=dev)
@@ -279,8 +290,9 @@ class CompressBuffers:
         self.n_keep = [int(x) for x in n_keep]
         H, D = spec.kv_heads, spec.head_dim
         U = spec.units
-        kept = spec.layers * sum(H * nk - H for nk in self.n_keep)
-        rows = kept + U
+        slot = 1 if spec.slot else 0
+        kept = spec.layers * sum(H * nk - slot * H for nk in self.n_keep)
+        rows = kept + slot * U
         shape = (spec.layers, H, spec.total_tokens)
         dt = spec.dtype
         self.scores = torch.empty(shape, dtype=torch.float32, device=device)

@@ -62,6 +62,7 @@ struct Plan {
   int nsub_max;      // 16-rank allocation sub-blocks per unit
   int bm_words;      // 64-bit bitmap words per unit
   int nsplit;        // tail gather workgroups per unit
+  int alloc;         // allocator: 0 Lagrangian + repair, 1 uniform, 2 greedy marginal
   const int64_t* cu;
 };
 
@@ -74,7 +75,13 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   if (!p->cu_seqlens_host) return CERTKV_EINVAL;
   if (p->q_dtype != p->kv_dtype) return CERTKV_EUNSUPPORTED;
   if (p->kv_dtype != CERTKV_F32 && p->kv_dtype != CERTKV_BF16) return CERTKV_EUNSUPPORTED;
-  if (p->flags & ~(uint32_t)(CERTKV_CAUSAL | CERTKV_DRY_RUN | CERTKV_KEEP_WINDOW))
+  if (p->flags & ~(uint32_t)(CERTKV_CAUSAL | CERTKV_DRY_RUN | CERTKV_KEEP_WINDOW |
+                             CERTKV_STAT_UNCENTERED | CERTKV_STAT_TAIL_MASS |
+                             CERTKV_ALLOC_UNIFORM | CERTKV_ALLOC_GREEDY | CERTKV_NO_SLOT))
+    return CERTKV_EINVAL;
+  if ((p->flags & CERTKV_STAT_UNCENTERED) && (p->flags & CERTKV_STAT_TAIL_MASS))
+    return CERTKV_EINVAL;
+  if ((p->flags & CERTKV_ALLOC_UNIFORM) && (p->flags & CERTKV_ALLOC_GREEDY))
     return CERTKV_EINVAL;
   if (!(p->softmax_scale >= 0.f) || isinf(p->softmax_scale)) return CERTKV_EINVAL;
   const int64_t* cu = p->cu_seqlens_host;
@@ -100,6 +107,9 @@ static certkv_status make_plan(const certkv_problem* p, Plan* pl) {
   P.g.causal = (p->flags & CERTKV_CAUSAL) ? 1 : 0;
   P.g.status = p->dev_status;
   P.g.keep_w = (p->flags & CERTKV_KEEP_WINDOW) ? p->window : 0;
+  P.g.stat = (p->flags & CERTKV_STAT_UNCENTERED) ? 1 : (p->flags & CERTKV_STAT_TAIL_MASS) ? 2 : 0;
+  P.g.slot = (p->flags & CERTKV_NO_SLOT) ? 0 : 1;
+  P.alloc = (p->flags & CERTKV_ALLOC_UNIFORM) ? 1 : (p->flags & CERTKV_ALLOC_GREEDY) ? 2 : 0;
   P.dtype = p->kv_dtype;
   P.U = (int64_t)P.g.L * P.g.B * P.g.H;
   P.max_len = max_len;
@@ -161,7 +171,7 @@ static std::vector<SeqTab> make_tabs(const Plan& P, const int32_t* n_keep, doubl
       t.len[i] = (int32_t)(P.cu[b + 1] - P.cu[b]);
       if (n_keep) {
         t.n_keep[i] = n_keep[b];
-        const int64_t br = (int64_t)P.g.H * n_keep[b] - P.g.H;
+        const int64_t br = (int64_t)P.g.H * n_keep[b] - (P.g.slot ? P.g.H : 0);
         int64_t bm = (int64_t)floor(alpha * (double)br / (double)P.g.H);
         if (bm < 1) bm = 1;
         t.b_real[i] = br;
@@ -179,8 +189,11 @@ static certkv_status check_budget(const Plan& P, const int32_t* n_keep, double a
   if (steps < 0 || steps > 200) return CERTKV_EINVAL;
   for (int b = 0; b < P.g.B; ++b) {
     const int64_t nb = P.cu[b + 1] - P.cu[b];
-    if (n_keep[b] < 2 || n_keep[b] > nb) return CERTKV_EINFEASIBLE;
-    const int64_t br = (int64_t)P.g.H * n_keep[b] - P.g.H;
+    // with the slot 2 <= n_keep <= n; without it every live row is a real
+    // key and a head keeps at most n - 1 of them
+    if (P.g.slot ? (n_keep[b] < 2 || n_keep[b] > nb) : (n_keep[b] < 1 || n_keep[b] > nb - 1))
+      return CERTKV_EINFEASIBLE;
+    const int64_t br = (int64_t)P.g.H * n_keep[b] - (P.g.slot ? P.g.H : 0);
     int64_t bm = (int64_t)floor(alpha * (double)br / (double)P.g.H);
     if (bm < 1) bm = 1;
     if (bm > nb - 1 || (int64_t)P.g.H * bm > br) return CERTKV_EINFEASIBLE;
@@ -392,11 +405,16 @@ static certkv_status do_allocate(const Plan& P, const float* curves, const int32
   a.cpos = w.cpos;
   a.dmax = w.dmax;
   a.nblk_max = P.nblk_max;
-  a.steps = steps;
+  a.steps = P.alloc == 2 ? 0 : steps;  // greedy marginal: the repair from b_min
   a.budgets = budgets;
   a.repairs = stats ? stats : w.repairs;
   (void)minmax;
-  for (const SeqTab& t : make_tabs(P, n_keep, alpha)) TRY(run_allocate(a, t, s));
+  for (const SeqTab& t : make_tabs(P, n_keep, alpha)) {
+    if (P.alloc == 1)
+      TRY(run_uniform_budgets(P.g, t, budgets, s));
+    else
+      TRY(run_allocate(a, t, s));
+  }
   return CERTKV_OK;
 }
 
@@ -411,7 +429,7 @@ static certkv_status do_select(const Plan& P, const float* scores, const uint32_
     else
       TRY(run_clamp(P.g, t, budgets, s));
   }
-  TRY(run_offsets(P.U, budgets, kept_offsets, packed_offsets, s));
+  TRY(run_offsets(P.U, P.g.slot, budgets, kept_offsets, packed_offsets, s));
   SelectArgs a;
   a.g = P.g;
   a.scores = scores;
@@ -621,7 +639,7 @@ certkv_status certkv_compact(const certkv_problem* p, certkv_tensor k, certkv_te
   hipStream_t s = (hipStream_t)stream;
   // packed_offsets[u] = kept_offsets[u] + u: recompute from the kept counts.
   Bufs w;
-  TRY(run_packed_from_kept(P.U, kept_offsets, packed_offsets, s));
+  TRY(run_packed_from_kept(P.U, P.g.slot, kept_offsets, packed_offsets, s));
   TRY(do_tail(P, nullptr, k, v, kept_offsets, kept_idx, nullptr, nullptr, const_cast<float*>(k_star),
               const_cast<float*>(v_star), nullptr, k_packed, v_packed, pos_packed, false, true,
               false, w, s));
@@ -722,7 +740,8 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, cert
   int32_t* pm = out->perm ? out->perm : w.perm;
   float* cv = out->curves ? out->curves : w.curves;
   int64_t cap = 0;
-  for (int b = 0; b < P.g.B; ++b) cap += (int64_t)P.g.H * n_keep_host[b] - P.g.H;
+  for (int b = 0; b < P.g.B; ++b)
+    cap += (int64_t)P.g.H * n_keep_host[b] - (P.g.slot ? P.g.H : 0);
   cap *= P.g.L;
   TRY(do_score(P, q_win, k, lse_in, out->scores, w.ksum, out->lse, w, s));
   TRY(do_sort(P, out->scores, pm, w, s));

@@ -46,6 +46,8 @@ struct Geo {
   int32_t causal;
   int32_t keep_w;            // window keys ranked first (w), or 0
   int32_t* status;           // optional: set to CERTKV_ENONFINITE on a non-finite value
+  int32_t stat;              // curve statistic: 0 centered, 1 uncentered, 2 tail mass
+  int32_t slot;              // slot rows per unit in the packed cache (1, or 0 without)
 };
 
 // Record a non-finite value in the caller's status word (racing stores all

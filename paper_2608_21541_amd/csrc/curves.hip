@@ -327,7 +327,10 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       }
       m += ar;
       q = fma(ar, vv, q);
-      double cur = fma(m, q, -w2);
+      // the lanes' parts sum to m Q - |W|^2 (centered), m Q (uncentered) or,
+      // for the tail mass, m^2 (32 equal parts of m^2 / 32, exact), whose
+      // square root is m
+      double cur = g.stat == 0 ? fma(m, q, -w2) : g.stat == 1 ? m * q : (m * m) * (1.0 / kLPR);
       bool placed = false;
 #pragma unroll
       for (int lev = 0; lev < kLev; ++lev) {

@@ -26,8 +26,10 @@ __global__ void clamp_budgets_kernel(Geo g, SeqTab st, int32_t* __restrict__ bud
 }
 
 // Exclusive prefix over all units of the budgets -> kept_offsets[U+1];
-// packed_offsets[u] = kept_offsets[u] + u (one slot row per unit).
-__global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, const int32_t* __restrict__ budgets,
+// packed_offsets[u] = kept_offsets[u] + slot * u (slot = 1: one slot row per
+// unit; 0 without the slot).
+__global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, int32_t slot,
+                                                       const int32_t* __restrict__ budgets,
                                                        int64_t* __restrict__ kept_offsets,
                                                        int64_t* __restrict__ packed_offsets) {
   __shared__ int64_t wsum[16];
@@ -50,7 +52,7 @@ __global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, const int32_t*
     for (int w = 0; w < wave; ++w) before += wsum[w];
     if (i < U) {
       kept_offsets[i] = before + incl - v;
-      if (packed_offsets) packed_offsets[i] = before + incl - v + i;
+      if (packed_offsets) packed_offsets[i] = before + incl - v + slot * i;
     }
     __syncthreads();
     if (threadIdx.x == 1023) carry = before + incl;
@@ -58,7 +60,7 @@ __global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, const int32_t*
   }
   if (threadIdx.x == 0) {
     kept_offsets[U] = carry;
-    if (packed_offsets) packed_offsets[U] = carry + U;
+    if (packed_offsets) packed_offsets[U] = carry + slot * U;
   }
 }
 
@@ -247,23 +249,43 @@ certkv_status run_clamp(const Geo& g, const SeqTab& st, int32_t* budgets, hipStr
   return CERTKV_OK;
 }
 
-certkv_status run_offsets(int64_t U, const int32_t* budgets, int64_t* kept_offsets,
+certkv_status run_offsets(int64_t U, int32_t slot, const int32_t* budgets, int64_t* kept_offsets,
                           int64_t* packed_offsets, hipStream_t s) {
-  CERTKV_LAUNCH("kept_offsets", offsets_kernel, dim3(1), dim3(1024), 0, s, U, budgets, kept_offsets,
-                packed_offsets);
+  CERTKV_LAUNCH("kept_offsets", offsets_kernel, dim3(1), dim3(1024), 0, s, U, slot, budgets,
+                kept_offsets, packed_offsets);
   return CERTKV_OK;
 }
 
-__global__ void packed_from_kept_kernel(int64_t U, const int64_t* __restrict__ kept_offsets,
+__global__ void packed_from_kept_kernel(int64_t U, int32_t slot,
+                                        const int64_t* __restrict__ kept_offsets,
                                         int64_t* __restrict__ packed_offsets) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i <= U) packed_offsets[i] = kept_offsets[i] + i;
+  if (i <= U) packed_offsets[i] = kept_offsets[i] + slot * i;
 }
 
-certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64_t* packed_offsets,
-                                   hipStream_t s) {
+certkv_status run_packed_from_kept(int64_t U, int32_t slot, const int64_t* kept_offsets,
+                                   int64_t* packed_offsets, hipStream_t s) {
   CERTKV_LAUNCH("packed_offsets", packed_from_kept_kernel, dim3((unsigned)((U + 256) / 256)),
-                dim3(256), 0, s, U, kept_offsets, packed_offsets);
+                dim3(256), 0, s, U, slot, kept_offsets, packed_offsets);
+  return CERTKV_OK;
+}
+
+// True-uniform allocation (one-factor ablation): every head of a (layer,
+// sequence) gets B_real / H, which the budget algebra makes whole.
+__global__ void uniform_budgets_kernel(Geo g, SeqTab st, int32_t* __restrict__ budgets) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int total = st.count * g.H * g.L;
+  if (i >= total) return;
+  const int h = i % g.H;
+  const int bi = (i / g.H) % st.count;
+  const int l = i / (g.H * st.count);
+  budgets[unit_index(g, l, st.first + bi, h)] = (int32_t)(st.b_real[bi] / g.H);
+}
+
+certkv_status run_uniform_budgets(const Geo& g, const SeqTab& st, int32_t* budgets, hipStream_t s) {
+  const int total = st.count * g.H * g.L;
+  CERTKV_LAUNCH("uniform_budgets", uniform_budgets_kernel, dim3((total + 255) / 256), dim3(256), 0,
+                s, g, st, budgets);
   return CERTKV_OK;
 }
 

@@ -86,8 +86,9 @@ certkv_status run_coverage(const Geo& g, const SeqTab& st, const float* scores,
                            const uint32_t* sorted_keys, double retain, int32_t* budgets,
                            hipStream_t s);
 certkv_status run_clamp(const Geo& g, const SeqTab& st, int32_t* budgets, hipStream_t s);
-certkv_status run_offsets(int64_t U, const int32_t* budgets, int64_t* kept_offsets,
+certkv_status run_offsets(int64_t U, int32_t slot, const int32_t* budgets, int64_t* kept_offsets,
                           int64_t* packed_offsets, hipStream_t s);
+certkv_status run_uniform_budgets(const Geo& g, const SeqTab& st, int32_t* budgets, hipStream_t s);
 certkv_status run_select(const SelectArgs& a, const SeqTab& st, hipStream_t s);
 certkv_status run_mask(const Geo& g, const std::vector<SeqTab>& tabs, const int64_t* kept_offsets,
                        const int32_t* kept_idx, uint8_t* mask, hipStream_t s);
@@ -147,6 +148,6 @@ certkv_status run_decode(const DecodeArgs& a, hipStream_t s);
 size_t decode_partial_rows(int64_t U, int nsplit, int tq, int G);
 int decode_nsplit(int max_len);
 
-certkv_status run_packed_from_kept(int64_t U, const int64_t* kept_offsets, int64_t* packed_offsets,
-                                   hipStream_t s);
+certkv_status run_packed_from_kept(int64_t U, int32_t slot, const int64_t* kept_offsets,
+                                   int64_t* packed_offsets, hipStream_t s);
 }  // namespace certkv

@@ -146,7 +146,7 @@ __global__ __launch_bounds__(kTailThreads) void tail_gather_kernel(
   const int nk = (int)(kept_offsets[u + 1] - off);
   const int per = (nk + nsplit - 1) / nsplit;
   const int i0 = split * per, i1 = min(nk, i0 + per);
-  const int64_t poff = off + u;  // packed segment start
+  const int64_t poff = off + g.slot * u;  // packed segment start
   const T* kb = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
   const T* vb = vc + (int64_t)l * v_sl + tok0 * v_st + (int64_t)h * v_sh;
 
@@ -323,7 +323,7 @@ __global__ __launch_bounds__(kTailThreads) void tail_finalize_kernel(
     }
     __syncthreads();
   }
-  if (DO_COMPACT) {
+  if (DO_COMPACT && g.slot) {
     const int64_t prow = off + u + nk;
     for (int d = tid; d < D; d += kTailThreads) {
       k_packed[prow * D + d] = from_f32<T>(slot_k[d]);

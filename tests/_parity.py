@@ -65,7 +65,8 @@ def vec_rel_err(x, ref, scale):
 
 
 def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=print,
-                       keep_window=False):
+                       keep_window=False, alpha=0.2, statistic="centered",
+                       allocator="lagrangian", slot=True):
     """Compare one (layer, sequence) block of the GPU output with the oracle.
 
     Integer stages are compared against the oracle fed the GPU's own upstream
@@ -88,17 +89,20 @@ def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=prin
     res = {}
 
     # Stage parity: the oracle's steps fed the GPU scores.
-    st = oracle.compress_block(q, k, v, n_keep, scale, s32_in=s_gpu, keep_window=keep_window)
+    var = dict(statistic=statistic, allocator=allocator, slot=slot)
+    st = oracle.compress_block(q, k, v, n_keep, scale, s32_in=s_gpu, keep_window=keep_window,
+                               alpha=alpha, **var)
     assert np.array_equal(st["perm"], perm_gpu), "order differs from the oracle's on the same scores"
     dc = np.abs(c_gpu.astype(np.float64) - st["c32"].astype(np.float64))
     cmax = float(st["c32"].max())
     tol_c = 4.0 * np.spacing(np.abs(st["c32"])).astype(np.float64) + 1e-6 * cmax
     assert (dc <= tol_c).all(), f"curves off by {dc.max()} (max c {cmax})"
     res["curve_bits_differ"] = int((c_gpu != st["c32"]).sum())
-    b_on_gpu_curves, _ = oracle.allocate(c_gpu, n_keep)
+    b_on_gpu_curves, _ = oracle.allocate(c_gpu, n_keep, alpha=alpha, allocator=allocator,
+                                         slot=slot)
     assert np.array_equal(b_on_gpu_curves, bud_gpu), (b_on_gpu_curves, bud_gpu)
     res["budgets_equal_oracle_curves"] = bool(np.array_equal(st["budgets"], bud_gpu))
-    br, bm = oracle.budget_params(H, n, n_keep)
+    br, bm = oracle.budget_params(H, n, n_keep, alpha, slot=slot)
     assert int(bud_gpu.sum()) == br and bud_gpu.min() >= bm and bud_gpu.max() <= n - 1
 
     ko = out["kept_offsets"].numpy()
@@ -134,21 +138,26 @@ def check_block_stages(spec, cfg, cache, out, li, b, check_scores=True, log=prin
         assert rec <= VEC_RTOL, (h, rec)
         worst_rec = max(worst_rec, rec)
         # packed segment: kept rows copied bit-exactly, then the rounded slot
+        # (no slot row without the slot)
         p0, p1 = po[u], po[u + 1]
-        assert p1 - p0 == len(kept) + 1
-        assert np.array_equal(pos[p0:p1 - 1], kept) and pos[p1 - 1] == -1
-        assert torch.equal(kp[p0:p1 - 1], k_src[kept, h].cpu()) and \
-            torch.equal(vp[p0:p1 - 1], v_src[kept, h].cpu())
-        slot_k = out["k_star"][u].to(kp.dtype)
-        slot_v = out["v_star"][u].to(vp.dtype)
-        assert torch.equal(kp[p1 - 1], slot_k) and torch.equal(vp[p1 - 1], slot_v)
+        pk = p1 - 1 if slot else p1
+        assert pk - p0 == len(kept)
+        assert np.array_equal(pos[p0:pk], kept)
+        assert torch.equal(kp[p0:pk], k_src[kept, h].cpu()) and \
+            torch.equal(vp[p0:pk], v_src[kept, h].cpu())
+        if slot:
+            assert pos[p1 - 1] == -1
+            slot_k = out["k_star"][u].to(kp.dtype)
+            slot_v = out["v_star"][u].to(vp.dtype)
+            assert torch.equal(kp[p1 - 1], slot_k) and torch.equal(vp[p1 - 1], slot_v)
     res["worst_slot_err"] = worst_vec
     res["worst_pooled_err"] = worst_rec
     blk = po[units[-1] + 1] - po[units[0]]
     assert blk == H * n_keep, "packed rows per (layer, sequence) must equal H * n_keep"
 
     if check_scores:
-        e2e = oracle.compress_block(q, k, v, n_keep, scale, keep_window=keep_window)
+        e2e = oracle.compress_block(q, k, v, n_keep, scale, keep_window=keep_window,
+                                    alpha=alpha, **var)
         worst = 0.0
         for h in range(H):
             r, sm = score_rel_err(s_gpu[h], e2e["s"][h])

@@ -77,7 +77,15 @@ def test_dry_run_score_validation():
     assert call(problem(w=701)) == _lib.CERTKV_EINVAL
     assert call(problem(H=65)) == _lib.CERTKV_EUNSUPPORTED
     assert call(problem(w=64, G=9)) == _lib.CERTKV_EUNSUPPORTED  # 576 window rows > 512
-    assert call(problem(flags=_lib.CERTKV_DRY_RUN | 64)) == _lib.CERTKV_EINVAL
+    assert call(problem(flags=_lib.CERTKV_DRY_RUN | 256)) == _lib.CERTKV_EINVAL
+    # one statistic and one allocator at a time
+    both_stats = _lib.CERTKV_STAT_UNCENTERED | _lib.CERTKV_STAT_TAIL_MASS
+    both_allocs = _lib.CERTKV_ALLOC_UNIFORM | _lib.CERTKV_ALLOC_GREEDY
+    assert call(problem(flags=_lib.CERTKV_DRY_RUN | both_stats)) == _lib.CERTKV_EINVAL
+    assert call(problem(flags=_lib.CERTKV_DRY_RUN | both_allocs)) == _lib.CERTKV_EINVAL
+    for f in (_lib.CERTKV_STAT_UNCENTERED, _lib.CERTKV_STAT_TAIL_MASS, _lib.CERTKV_ALLOC_UNIFORM,
+              _lib.CERTKV_ALLOC_GREEDY, _lib.CERTKV_NO_SLOT):
+        assert call(problem(flags=_lib.CERTKV_DRY_RUN | _lib.CERTKV_CAUSAL | f)) == _lib.CERTKV_OK
     # the caller's row log-sum-exp and the row log-sum-exp output are plain
     # optional device pointers
     assert call(p, lse_in=FAKE, lse_out=FAKE) == _lib.CERTKV_OK
