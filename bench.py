@@ -77,6 +77,20 @@ def algorithmic_model(cfg, n_keep):
     return {k: (b * ht, fl * ht, sl * ht) for k, (b, fl, sl) in per.items()}, ht
 
 
+# One-factor ablations of the pass (appendix, one-factor ablations table).
+VARIANTS = {
+    "default": {},
+    "tail_mass": {"statistic": "tail_mass"},
+    "uncentered": {"statistic": "uncentered"},
+    "uniform": {"allocator": "uniform"},
+    "greedy": {"allocator": "greedy"},
+    "no_slot": {"slot": False},
+    "alpha0": {"alpha": 0.0},
+    "alpha0.1": {"alpha": 0.1},
+    "alpha0.4": {"alpha": 0.4},
+}
+
+
 def source_digest(kernel):
     """sha256 over the source file of a kernel and the shared headers."""
     import hashlib
@@ -274,7 +288,8 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
     import paper_2608_21541_amd as ck
     import synth
 
-    ck.compress(spec, cache["q_win"], cache["k"], cache["v"], n_keep, bufs=bufs)
+    ck.compress(spec, cache["q_win"], cache["k"], cache["v"], n_keep,
+                alpha=VARIANTS[args.variant].get("alpha", 0.2), bufs=bufs)
     torch.cuda.synchronize()
     rows = int(bufs.packed_offsets[-1].item())
     # the budgets are known once compression has run: the longest segment
@@ -354,6 +369,8 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="time decode over the packed cache instead of the pass")
     ap.add_argument("--tq", type=int, default=32, help="new queries per sequence (--decode)")
+    ap.add_argument("--variant", default="default", choices=sorted(VARIANTS),
+                    help="a one-factor ablation of the pass (statistic, allocator, slot, alpha)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("CSV", "OUT", "COMMAND"),
@@ -393,6 +410,11 @@ def main():
     n_keep = cache["n_keep"]
     spec = ck.ProblemSpec(cfg.layers, cfg.kv_heads, cfg.group, cfg.head_dim, cfg.window,
                           cfg.seqlens, cfg.dtype)
+    var = VARIANTS[args.variant]
+    spec.statistic = var.get("statistic", "centered")
+    spec.allocator = var.get("allocator", "lagrangian")
+    spec.slot = var.get("slot", True)
+    alpha = var.get("alpha", 0.2)
     bufs = ck.CompressBuffers(spec, n_keep, dev)
     q, k, v = cache["q_win"], cache["k"], cache["v"]
     torch.cuda.synchronize()
@@ -411,7 +433,7 @@ def main():
         run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log)
         return
     for _ in range(args.warmup):
-        ck.compress(spec, q, k, v, n_keep, bufs=bufs)
+        ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs)
     torch.cuda.synchronize()
     # Timed region.  Every launch of the pass is bracketed by HIP events on
     # the stream it runs on, giving per-kernel durations of these same steps.
@@ -421,7 +443,7 @@ def main():
     torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
-        ck.compress(spec, q, k, v, n_keep, bufs=bufs)
+        ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs)
     end.record(stream)
     torch.cuda.synchronize()
     prof = ck.profile_read()
@@ -452,7 +474,7 @@ def main():
     log(json.dumps(kernels, indent=1))
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.variant == "default":
         cpu = cpu_baseline(cache, cfg, n_keep, log)
 
     rec = {
@@ -472,7 +494,8 @@ def main():
                                f"{cfg.kv_heads} KV heads (GQA {cfg.group}), d {cfg.head_dim}, "
                                f"{tokens} tokens, window {cfg.window}, n_keep {n_keep[0]}",
                    "layers": cfg.layers, "seq_len": tokens, "kv_heads": cfg.kv_heads,
-                   "head_dim": cfg.head_dim, "window": cfg.window, "n_keep": n_keep[0]},
+                   "head_dim": cfg.head_dim, "window": cfg.window, "n_keep": n_keep[0],
+                   "variant": args.variant},
         "pass_alg_GBps": pass_bytes / (ms / 1e3) / 1e9,
         "pass_alg_frac_hbm": pass_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
         "roofline": roof,
