@@ -88,6 +88,8 @@ VARIANTS = {
     "alpha0": {"alpha": 0.0},
     "alpha0.1": {"alpha": 0.1},
     "alpha0.4": {"alpha": 0.4},
+    # the SnapKV-uniform baseline: n_keep real tokens per head, no slot
+    "snapkv_uniform": {"allocator": "uniform", "slot": False},
 }
 
 

@@ -33,6 +33,7 @@ VARIANTS = [
     ("no_slot", dict(slot=False)),
     ("alpha_0", dict(alpha=0.0)),
     ("alpha_0.4", dict(alpha=0.4)),
+    ("snapkv_uniform", dict(allocator="uniform", slot=False)),
 ]
 
 
@@ -62,9 +63,11 @@ def test_variant_matches_oracle(name, var):
                            allocator=var.get("allocator", "lagrangian"),
                            slot=var.get("slot", True))
     if var.get("allocator") == "uniform":
+        slot = var.get("slot", True)
         for b in range(cfg.batch):
             units = [unit_id(spec, 0, b, h) for h in range(cfg.kv_heads)]
-            assert (out["budgets"].numpy()[units] == cache["n_keep"][b] - 1).all()
+            want = cache["n_keep"][b] - (1 if slot else 0)
+            assert (out["budgets"].numpy()[units] == want).all()
 
 
 def test_no_slot_stage_entry_points_and_decode():
