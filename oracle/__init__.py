@@ -72,6 +72,10 @@ def lib():
         L.ora_compress_block_variant.argtypes = [
             _i64, _i32, _i32, _i32, _i32, _p, _p, _p, _dbl, _i32, _i64, _dbl,
             _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p]
+        L.ora_cluster_summaries.argtypes = [_i64, _i32, _p, _i64, _p, _p, _i32, _i32, _p, _p,
+                                            _p, _p, _p, _p]
+        L.ora_cluster_estimate.argtypes = [_i64, _i32, _p, _p, _p, _i32, _p, _p, _p, _p, _p,
+                                           ctypes.c_float, _dbl, _p, _p]
         L.ora_num_threads.restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -324,3 +328,41 @@ def lift_terms(q, k, v, kept_mask, r, kslot, vslot, scale):
     _check(lib().ora_lift_terms(n, d, _ptr(q), _ptr(k), _ptr(v), _ptr(kept), _ptr(r),
                                 _ptr(kslot), _ptr(vslot), float(scale), _ptr(out)), "lift_terms")
     return dict(zip(["p", "q", "l1", "lam_T", "z_slot", "v_max", "err"], out.tolist()))
+
+
+def cluster_summaries(perm, b, k, v, m, bf16=True):
+    """Clustered tail summaries of one head: the evicted ranks b..n-1 in the
+    order perm cut into m contiguous groups.  Returns dict(kbar [m][d],
+    vbar [m][d] (as stored), count [m], R [m], rho [m] fp32, vmax_kept)."""
+    perm, k, v = _i32a(perm), _f64(k), _f64(v)
+    n, d = k.shape
+    kbar = np.zeros((m, d), np.float64)
+    vbar = np.zeros((m, d), np.float64)
+    cnt = np.zeros(m, np.int32)
+    R = np.zeros(m, np.float32)
+    rho = np.zeros(m, np.float32)
+    vk = np.zeros(1, np.float32)
+    _check(lib().ora_cluster_summaries(n, d, _ptr(perm), int(b), _ptr(k), _ptr(v), int(m),
+                                       int(bool(bf16)), _ptr(kbar), _ptr(vbar), _ptr(cnt),
+                                       _ptr(R), _ptr(rho), _ptr(vk)), "cluster_summaries")
+    return dict(kbar=kbar, vbar=vbar, count=cnt, R=R, rho=rho, vmax_kept=float(vk[0]))
+
+
+def cluster_estimate(q, kp, vp, cl, scale):
+    """The clustered-summary estimator and certificate for one query q [d]
+    over kept rows kp, vp [nk][d] and the summaries cl (cluster_summaries).
+    Returns (out [d], dict(lse, dz, dn, vmax, bound, structural))."""
+    q, kp, vp = _f64(q), _f64(kp), _f64(vp)
+    d = q.shape[0]
+    nk = kp.shape[0]
+    m = cl["count"].shape[0]
+    out = np.zeros(d, np.float64)
+    cert = np.zeros(6, np.float64)
+    kb, vb = _f64(cl["kbar"]), _f64(cl["vbar"])
+    cnt, R, rho = _i32a(cl["count"]), _f32(cl["R"]), _f32(cl["rho"])
+    _check(lib().ora_cluster_estimate(nk, d, _ptr(q), _ptr(kp), _ptr(vp), m, _ptr(kb),
+                                      _ptr(vb), _ptr(cnt), _ptr(R), _ptr(rho),
+                                      float(cl["vmax_kept"]), float(scale), _ptr(out),
+                                      _ptr(cert)), "cluster_estimate")
+    return out, dict(lse=cert[0], dz=cert[1], dn=cert[2], vmax=cert[3], bound=cert[4],
+                     structural=cert[5])

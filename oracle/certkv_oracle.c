@@ -751,3 +751,158 @@ int ora_lift_terms(int64_t n, int32_t d, const double* q, const double* k, const
   free(Oh);
   return ORA_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Clustered tail summaries (appendix, deterministic output-error bound for
+ * clustered tail summaries).  The evicted ranks b..n-1 of one head, in the
+ * pass's order, are cut into m contiguous groups of ceil((n - b) / m) ranks
+ * (later groups may be short or empty).  Per group g: the count n_g, the
+ * representative key and value (the unweighted means, rounded to fp32 and
+ * then to bf16 when bf16 != 0, as they would be stored), and the radii
+ * R_g = max |k_j - kbar_g|, rho_g = max |v_j - vbar_g| against the stored
+ * representatives, rounded up to fp32.  Also the largest kept value norm.
+ *   perm [n] the rank order; k, v [n][d] position-indexed
+ *   kbar, vbar [m][d] out; cnt [m] out; R, rho [m] out; vmax_kept out. */
+static double ora_store_rep(double x, int32_t bf16) {
+  float f = (float)x;
+  if (!bf16) return (double)f;
+  uint32_t b = (uint32_t)ora_f32_to_bf16(f) << 16;
+  float y;
+  memcpy(&y, &b, 4);
+  return (double)y;
+}
+
+static float ora_round_up_f32(double x) {
+  float f = (float)x;
+  if ((double)f < x) f = nextafterf(f, INFINITY);
+  return f;
+}
+
+int ora_cluster_summaries(int64_t n, int32_t d, const int32_t* perm, int64_t b,
+                          const double* k, const double* v, int32_t m, int32_t bf16,
+                          double* kbar, double* vbar, int32_t* cnt, float* R, float* rho,
+                          float* vmax_kept) {
+  if (n <= 0 || d <= 0 || m <= 0 || b < 0 || b > n) return ORA_EINVAL;
+  const int64_t E = n - b;
+  const int64_t cs = (E + m - 1) / m;
+  for (int32_t g = 0; g < m; ++g) {
+    int64_t r0 = b + (int64_t)g * cs, r1 = r0 + cs;
+    if (r0 > n) r0 = n;
+    if (r1 > n) r1 = n;
+    cnt[g] = (int32_t)(r1 - r0);
+    double* kb = kbar + (size_t)g * d;
+    double* vb = vbar + (size_t)g * d;
+    for (int32_t t = 0; t < d; ++t) kb[t] = vb[t] = 0.0;
+    R[g] = rho[g] = 0.f;
+    if (r1 <= r0) continue;
+    for (int64_t r = r0; r < r1; ++r) {
+      const int32_t j = perm[r];
+      for (int32_t t = 0; t < d; ++t) {
+        kb[t] += k[(size_t)j * d + t];
+        vb[t] += v[(size_t)j * d + t];
+      }
+    }
+    for (int32_t t = 0; t < d; ++t) {
+      kb[t] = ora_store_rep(kb[t] / (double)(r1 - r0), bf16);
+      vb[t] = ora_store_rep(vb[t] / (double)(r1 - r0), bf16);
+    }
+    double rk = 0.0, rv = 0.0;
+    for (int64_t r = r0; r < r1; ++r) {
+      const int32_t j = perm[r];
+      double sk = 0.0, sv = 0.0;
+      for (int32_t t = 0; t < d; ++t) {
+        const double dk = k[(size_t)j * d + t] - kb[t];
+        const double dv = v[(size_t)j * d + t] - vb[t];
+        sk += dk * dk;
+        sv += dv * dv;
+      }
+      if (sk > rk) rk = sk;
+      if (sv > rv) rv = sv;
+    }
+    R[g] = ora_round_up_f32(sqrt(rk));
+    rho[g] = ora_round_up_f32(sqrt(rv));
+  }
+  double vm = 0.0;
+  for (int64_t r = 0; r < b; ++r) {
+    const int32_t j = perm[r];
+    double s2 = 0.0;
+    for (int32_t t = 0; t < d; ++t) s2 += v[(size_t)j * d + t] * v[(size_t)j * d + t];
+    if (s2 > vm) vm = s2;
+  }
+  *vmax_kept = ora_round_up_f32(sqrt(vm));
+  return ORA_OK;
+}
+
+/* The ratio estimator of the clustered-summary theorem and its certificate,
+ * for one query q [d]: logits l_j = scale <q, k_j> over the nk kept rows
+ * kp, vp [nk][d]; cluster logits lbar_g = scale <q, kbar_g> with weight
+ * n_g e^{lbar_g}; r_g = scale |q| R_g (the Cauchy-Schwarz logit radius).
+ *   out [d]: Ohat = (sum_S e^l v + sum_g n_g e^lbar vbar) / Zhat
+ *   cert[6]: log Zhat, D_Z / Zhat, D_N / Zhat, V'_max, the bound
+ *            3 (D_N + V'_max D_Z) / Zhat (+inf unless D_Z <= Zhat / 3), and
+ *            the structural form 3 (1 - p_S) max_g e^{r_g} (2 V' (e^{r_g} - 1)
+ *            + rho_g). */
+int ora_cluster_estimate(int64_t nk, int32_t d, const double* q, const double* kp,
+                         const double* vp, int32_t m, const double* kbar, const double* vbar,
+                         const int32_t* cnt, const float* R, const float* rho,
+                         float vmax_kept, double scale, double* out, double* cert) {
+  if (d <= 0 || m < 0 || nk < 0) return ORA_EINVAL;
+  double* l = (double*)malloc(sizeof(double) * (size_t)(nk + m + 1));
+  if (!l) return ORA_ENOMEM;
+  double mx = -INFINITY;
+  for (int64_t i = 0; i < nk; ++i) {
+    double s = 0.0;
+    for (int32_t t = 0; t < d; ++t) s += q[t] * kp[(size_t)i * d + t];
+    l[i] = scale * s;
+    if (l[i] > mx) mx = l[i];
+  }
+  for (int32_t g = 0; g < m; ++g) {
+    double s = 0.0;
+    for (int32_t t = 0; t < d; ++t) s += q[t] * kbar[(size_t)g * d + t];
+    l[nk + g] = cnt[g] > 0 ? scale * s + log((double)cnt[g]) : -INFINITY;
+    if (l[nk + g] > mx) mx = l[nk + g];
+  }
+  double Zs = 0.0, Z = 0.0;
+  for (int32_t t = 0; t < d; ++t) out[t] = 0.0;
+  for (int64_t i = 0; i < nk + m; ++i) {
+    if (l[i] == -INFINITY) continue;
+    const double w = exp(l[i] - mx);
+    Z += w;
+    if (i < nk) Zs += w;
+    const double* vi = i < nk ? vp + (size_t)i * d : vbar + (size_t)(i - nk) * d;
+    for (int32_t t = 0; t < d; ++t) out[t] += w * vi[t];
+  }
+  for (int32_t t = 0; t < d; ++t) out[t] /= Z;
+  double qn = 0.0;
+  for (int32_t t = 0; t < d; ++t) qn += q[t] * q[t];
+  qn = sqrt(qn);
+  double dz = 0.0, dn = 0.0, vmax = (double)vmax_kept, smax = 0.0;
+  for (int32_t g = 0; g < m; ++g) {
+    if (cnt[g] <= 0) continue;
+    double vb = 0.0;
+    for (int32_t t = 0; t < d; ++t) vb += vbar[(size_t)g * d + t] * vbar[(size_t)g * d + t];
+    vb = sqrt(vb);
+    if (vb + (double)rho[g] > vmax) vmax = vb + (double)rho[g];
+  }
+  for (int32_t g = 0; g < m; ++g) {
+    if (cnt[g] <= 0) continue;
+    double vb = 0.0;
+    for (int32_t t = 0; t < d; ++t) vb += vbar[(size_t)g * d + t] * vbar[(size_t)g * d + t];
+    vb = sqrt(vb);
+    const double r = scale * qn * (double)R[g];
+    const double zg = exp(l[nk + g] - mx) / Z; /* Zhat_g / Zhat */
+    const double er = exp(r);
+    dz += (er - 1.0) * er * zg;
+    dn += er * zg * ((er - 1.0) * vb + (double)rho[g]);
+    const double sf = er * (2.0 * vmax * (er - 1.0) + (double)rho[g]);
+    if (sf > smax) smax = sf;
+  }
+  cert[0] = mx + log(Z);
+  cert[1] = dz;
+  cert[2] = dn;
+  cert[3] = vmax;
+  cert[4] = dz <= 1.0 / 3.0 ? 3.0 * (dn + vmax * dz) : INFINITY;
+  cert[5] = dz <= 1.0 / 3.0 ? 3.0 * (1.0 - Zs / Z) * smax : INFINITY;
+  free(l);
+  return ORA_OK;
+}
