@@ -345,6 +345,52 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
  * cache).  bf16 caches only (CERTKV_EUNSUPPORTED for fp32); tq * G <= 512.
  * The workspace is certkv_decode_workspace_size(p, tq, max_rows) bytes,
  * 256-byte aligned; a non-finite output sets the status word. */
+/* Clustered tail summaries (appendix, deterministic output-error bound for
+ * clustered tail summaries): per head, the evicted ranks b_h..n-1 in the
+ * pass's rank order are cut into m contiguous groups of ceil((n - b_h) / m)
+ * ranks (later groups may be short or empty).  Per group g of unit u:
+ *   cluster_count [U][m] int32 out   n_g
+ *   cluster_k, cluster_v [U][m][d] out in kv_dtype: the unweighted mean key
+ *                  and value (fp64 sums), as stored
+ *   cluster_rk, cluster_rv [U][m] fp32 out: max |k_j - kbar_g|, max |v_j -
+ *                  vbar_g| over the members against the stored means, rounded
+ *                  up (radii that hold for the stored rows)
+ *   kept_vmax [U] fp32 out: the largest norm of a kept value
+ * Inputs: k, v as for certkv_score; perm [L][H][T] the rank order of the
+ * pass (certkv_allocate or certkv_outputs.perm); budgets [U] (b_h).
+ * 1 <= m <= 64, else CERTKV_EINVAL.  Allocates nothing. */
+certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k,
+                                  certkv_tensor v, const int32_t* perm,
+                                  const int32_t* budgets, int32_t m,
+                                  void* cluster_k, void* cluster_v,
+                                  int32_t* cluster_count, float* cluster_rk,
+                                  float* cluster_rv, float* kept_vmax,
+                                  void* stream);
+
+/* Decode with clustered tail summaries: as certkv_decode over the kept rows
+ * (k_packed, v_packed, packed_offsets: segments of kept rows only, e.g. the
+ * packed cache of a CERTKV_NO_SLOT pass), plus per unit the m cluster terms of
+ * certkv_cluster_tail: the ratio estimator
+ *   out = (sum_S e^l v + sum_g n_g e^lbar_g vbar_g) / Zhat,
+ *   lbar_g = scale <q, kbar_g>,  Zhat = sum_S e^l + sum_g n_g e^lbar_g,
+ * lse = log Zhat.  bound (optional [L][B*tq][Hq] fp32 out): the runtime
+ * certificate with r_g = scale |q| R_g: 3 (D_N + V' D_Z) / Zhat when
+ * D_Z <= Zhat / 3, +infinity otherwise.  bf16 only; the workspace is
+ * certkv_decode_workspace_size(p, tq, max_rows). */
+certkv_status certkv_decode_clustered(const certkv_problem* p,
+                                      certkv_tensor q_new, int32_t tq,
+                                      int32_t max_rows, const void* k_packed,
+                                      const void* v_packed,
+                                      const int64_t* packed_offsets, int32_t m,
+                                      const void* cluster_k,
+                                      const void* cluster_v,
+                                      const int32_t* cluster_count,
+                                      const float* cluster_rk,
+                                      const float* cluster_rv,
+                                      const float* kept_vmax, float* out,
+                                      float* lse, float* bound, void* ws,
+                                      size_t ws_bytes, void* stream);
+
 size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq,
                                     int32_t max_rows);
 certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,

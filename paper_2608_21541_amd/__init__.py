@@ -6,5 +6,5 @@ binding with the same entry-point names.
 """
 from .api import (ProblemSpec, CompressBuffers, score, allocate, allocate_curves, select,  # noqa: F401
                   tail_summary, compact, compress, workspace_size, decode, DecodeBuffers,
-                  decode_workspace_size, profile_enable, profile_reset, profile_read)
+                  decode_workspace_size, cluster_tail, decode_clustered, profile_enable, profile_reset, profile_read)
 from ._lib import CertKVError, CERTKV_OK, CERTKV_ENONFINITE, CERTKV_ERANGE  # noqa: F401

@@ -42,7 +42,8 @@ STAGE_COMPRESS = 6
 EXPORTS = [
     "certkv_status_string", "certkv_workspace_size", "certkv_score", "certkv_allocate",
     "certkv_allocate_curves", "certkv_select", "certkv_tail_summary", "certkv_compact",
-    "certkv_compress", "certkv_decode_workspace_size", "certkv_decode", "certkv_profile_enable",
+    "certkv_compress", "certkv_decode_workspace_size", "certkv_decode", "certkv_cluster_tail",
+    "certkv_decode_clustered", "certkv_profile_enable",
     "certkv_profile_read", "certkv_profile_reset",
 ]
 
@@ -117,6 +118,9 @@ def lib():
     L.certkv_decode_workspace_size.argtypes = [P, i32, i32]
     L.certkv_decode_workspace_size.restype = sz
     L.certkv_decode.argtypes = [P, Tensor, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.certkv_cluster_tail.argtypes = [P, Tensor, Tensor, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.certkv_decode_clustered.argtypes = [P, Tensor, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp,
+                                          vp, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_profile_enable.argtypes = [i32]
     L.certkv_profile_read.argtypes = [vp, vp, vp, i32]
     L.certkv_profile_read.restype = i32

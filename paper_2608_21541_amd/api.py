@@ -281,6 +281,47 @@ def decode(spec: ProblemSpec, q_new, k_packed, v_packed, packed_offsets, tq, wit
     return (bufs.out, bufs.lse) if with_lse else bufs.out
 
 
+def cluster_tail(spec: ProblemSpec, k, v, perm, budgets, m):
+    """Clustered tail summaries: m contiguous groups of each head's evicted
+    ranks.  Returns dict(kbar, vbar [U][m][d] in the cache dtype, count [U][m]
+    int32, rk, rv [U][m] fp32 radii, vmax_kept [U] fp32)."""
+    L = _lib.lib()
+    dev = k.device
+    U, D = spec.units, spec.head_dim
+    out = dict(kbar=torch.empty((U, m, D), dtype=k.dtype, device=dev),
+               vbar=torch.empty((U, m, D), dtype=k.dtype, device=dev),
+               count=torch.empty((U, m), dtype=torch.int32, device=dev),
+               rk=torch.empty((U, m), dtype=torch.float32, device=dev),
+               rv=torch.empty((U, m), dtype=torch.float32, device=dev),
+               vmax_kept=torch.empty(U, dtype=torch.float32, device=dev))
+    p = spec.c_problem()
+    _check(L.certkv_cluster_tail(ctypes.byref(p), _tensor(k), _tensor(v), _ptr(perm),
+                                 _ptr(budgets), int(m), _ptr(out["kbar"]), _ptr(out["vbar"]),
+                                 _ptr(out["count"]), _ptr(out["rk"]), _ptr(out["rv"]),
+                                 _ptr(out["vmax_kept"]), _stream(dev)), "certkv_cluster_tail")
+    return out
+
+
+def decode_clustered(spec: ProblemSpec, q_new, k_packed, v_packed, packed_offsets, tq, clusters,
+                     max_rows=0):
+    """Decode over kept-row segments plus the clustered tail summaries of
+    cluster_tail: (out [L][B*tq][Hq][d], lse, bound [L][B*tq][Hq]) fp32, the
+    bound being the runtime certificate (inf where it does not hold)."""
+    L = _lib.lib()
+    dev = q_new.device
+    bufs = DecodeBuffers(spec, tq, dev, with_lse=True, max_rows=max_rows)
+    bound = torch.empty_like(bufs.lse)
+    m = clusters["count"].shape[1]
+    p = spec.c_problem()
+    _check(L.certkv_decode_clustered(
+        ctypes.byref(p), _tensor(q_new), int(tq), bufs.max_rows, _ptr(k_packed), _ptr(v_packed),
+        _ptr(packed_offsets), int(m), _ptr(clusters["kbar"]), _ptr(clusters["vbar"]),
+        _ptr(clusters["count"]), _ptr(clusters["rk"]), _ptr(clusters["rv"]),
+        _ptr(clusters["vmax_kept"]), _ptr(bufs.out), _ptr(bufs.lse), _ptr(bound), _ptr(bufs.ws),
+        bufs.ws_bytes, _stream(dev)), "certkv_decode_clustered")
+    return bufs.out, bufs.lse, bound
+
+
 class CompressBuffers:
     """Preallocated outputs and workspace of the fused pass (reusable)."""
 

@@ -677,10 +677,10 @@ size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq, int32_t
   return decode_ws_layout(P, tq, max_rows).total;
 }
 
-certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
-                            int32_t max_rows, const void* k_packed, const void* v_packed,
-                            const int64_t* packed_offsets, float* out, float* lse, void* ws,
-                            size_t ws_bytes, void* stream) {
+static certkv_status decode_impl(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
+                                 int32_t max_rows, const void* k_packed, const void* v_packed,
+                                 const int64_t* packed_offsets, const DecodeClusters& cl,
+                                 float* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
   Plan P;
   TRY(make_plan(p, &P));
   if (tq < 1 || max_rows < 0) return CERTKV_EINVAL;
@@ -711,9 +711,76 @@ certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_
   a.part_ml = reinterpret_cast<float2*>(static_cast<char*>(ws) + W.ml_off);
   a.items = reinterpret_cast<int2*>(static_cast<char*>(ws) + W.items_off);
   a.item_count = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + W.count_off);
+  a.cl = cl;
   a.out = out;
   a.lse = lse;
   return run_decode(a, (hipStream_t)stream);
+}
+
+certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
+                            int32_t max_rows, const void* k_packed, const void* v_packed,
+                            const int64_t* packed_offsets, float* out, float* lse, void* ws,
+                            size_t ws_bytes, void* stream) {
+  DecodeClusters cl;
+  memset(&cl, 0, sizeof(cl));
+  return decode_impl(p, q_new, tq, max_rows, k_packed, v_packed, packed_offsets, cl, out, lse, ws,
+                     ws_bytes, stream);
+}
+
+certkv_status certkv_decode_clustered(const certkv_problem* p, certkv_tensor q_new, int32_t tq,
+                                      int32_t max_rows, const void* k_packed,
+                                      const void* v_packed, const int64_t* packed_offsets,
+                                      int32_t m, const void* cluster_k, const void* cluster_v,
+                                      const int32_t* cluster_count, const float* cluster_rk,
+                                      const float* cluster_rv, const float* kept_vmax,
+                                      float* out, float* lse, float* bound, void* ws,
+                                      size_t ws_bytes, void* stream) {
+  if (m < 1 || m > 64) return CERTKV_EINVAL;
+  if (!cluster_k || !cluster_v || !cluster_count || !cluster_rk || !cluster_rv || !kept_vmax)
+    return CERTKV_EINVAL;
+  DecodeClusters cl;
+  cl.m = m;
+  cl.kbar = static_cast<const uint16_t*>(cluster_k);
+  cl.vbar = static_cast<const uint16_t*>(cluster_v);
+  cl.count = cluster_count;
+  cl.rk = cluster_rk;
+  cl.rv = cluster_rv;
+  cl.vmax_kept = kept_vmax;
+  cl.bound = bound;
+  return decode_impl(p, q_new, tq, max_rows, k_packed, v_packed, packed_offsets, cl, out, lse, ws,
+                     ws_bytes, stream);
+}
+
+certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k, certkv_tensor v,
+                                  const int32_t* perm, const int32_t* budgets, int32_t m,
+                                  void* cluster_k, void* cluster_v, int32_t* cluster_count,
+                                  float* cluster_rk, float* cluster_rv, float* kept_vmax,
+                                  void* stream) {
+  Plan P;
+  TRY(make_plan(p, &P));
+  TRY(check_tensor(k, P));
+  TRY(check_tensor(v, P));
+  if (m < 1 || m > 64) return CERTKV_EINVAL;
+  if (!perm || !budgets || !cluster_k || !cluster_v || !cluster_count || !cluster_rk ||
+      !cluster_rv || !kept_vmax)
+    return CERTKV_EINVAL;
+  if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
+  ClusterArgs a;
+  a.g = P.g;
+  a.dtype = P.dtype;
+  a.m = m;
+  a.perm = perm;
+  a.budgets = budgets;
+  a.k = k;
+  a.v = v;
+  a.kbar = cluster_k;
+  a.vbar = cluster_v;
+  a.count = cluster_count;
+  a.rk = cluster_rk;
+  a.rv = cluster_rv;
+  a.vmax_kept = kept_vmax;
+  for (const SeqTab& t : make_tabs(P, nullptr, 0.0)) TRY(run_clusters(a, t, (hipStream_t)stream));
+  return CERTKV_OK;
 }
 
 certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win, certkv_tensor k,

@@ -400,11 +400,25 @@ __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
 // the result does not depend on timing.
 constexpr int kCombThreads = 256;
 
-template <int D>
+// With clustered tail summaries (CL), the m cluster terms n_g e^{lbar_g}
+// (lbar_g = scale <q, kbar_g>) and n_g e^{lbar_g} vbar_g join the kept rows'
+// sums (the ratio estimator of the clustered-summary bound), and the row's
+// runtime certificate is evaluated from the stored summaries: with r_g =
+// scale |q| R_g and zeta_g = n_g e^{lbar_g} / Zhat,
+//   D_Z / Zhat = sum_g (e^r_g - 1) e^r_g zeta_g,
+//   D_N / Zhat = sum_g e^r_g zeta_g ((e^r_g - 1) |vbar_g| + rho_g),
+//   V' = max(max kept |v|, max_g |vbar_g| + rho_g),
+// and |Ohat - O| <= 3 (D_N + V' D_Z) / Zhat when D_Z <= Zhat / 3 (else the
+// bound is infinite).
+template <int D, bool CL>
 __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
     Geo g, int32_t tq, int32_t nsplit, int32_t mp, const int64_t* __restrict__ poff,
     const float* __restrict__ part_o, const float2* __restrict__ part_ml, float* __restrict__ out,
-    float* __restrict__ lse) {
+    float* __restrict__ lse, DecodeClusters cl, const uint16_t* __restrict__ qn, int64_t q_sl,
+    int64_t q_st, int64_t q_sh) {
+  constexpr int kMaxCl = 64;
+  __shared__ float zc_s[CL ? kMaxCl : 1], vn_s[CL ? kMaxCl : 1];
+  __shared__ float qn_s;
   constexpr int C4 = D / 4;                // threads per slot row
   constexpr int S = kCombThreads / C4;     // slot groups
   __shared__ float4 acc_s[S][C4];
@@ -450,6 +464,34 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
   }
   acc_s[sg][c4] = acc;
   if (c4 == 0) ml_s[sg] = make_float2(m, L);
+  const int Hq = g.H * g.G;
+  const int h = (int)(u % g.H);
+  const int64_t lb = u / g.H;
+  const int b = (int)(lb % g.B);
+  const int l = (int)(lb / g.B);
+  const int t = row / g.G, gq = row % g.G;
+  const int64_t orow = ((int64_t)l * g.B * tq + (int64_t)b * tq + t) * Hq + h * g.G + gq;
+  const float c2 = g.scale * kDecLog2e;
+  if (CL && threadIdx.x < cl.m) {
+    // cluster logits in log2 units (with log2 n_g) and value norms
+    const int gi = threadIdx.x;
+    const uint16_t* qr = qn + (int64_t)l * q_sl + (int64_t)(b * tq + t) * q_st +
+                         (int64_t)(h * g.G + gq) * q_sh;
+    const uint16_t* kr = cl.kbar + (u * cl.m + gi) * D;
+    const uint16_t* vr = cl.vbar + (u * cl.m + gi) * D;
+    float dot = 0.f, vv = 0.f, qq = 0.f;
+    for (int e = 0; e < D; ++e) {
+      const float qe = bf16_to_f32(qr[e]);
+      dot = fmaf(qe, bf16_to_f32(kr[e]), dot);
+      const float ve = bf16_to_f32(vr[e]);
+      vv = fmaf(ve, ve, vv);
+      qq = fmaf(qe, qe, qq);
+    }
+    const int cnt = cl.count[u * cl.m + gi];
+    zc_s[gi] = cnt > 0 ? dot * c2 + __builtin_amdgcn_logf((float)cnt) : -INFINITY;
+    vn_s[gi] = sqrtf(vv);
+    if (gi == 0) qn_s = sqrtf(qq);
+  }
   __syncthreads();
   if (threadIdx.x >= D) return;
   const int dd = threadIdx.x;
@@ -465,13 +507,35 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(
     Lt += mk.y * w;
     at += reinterpret_cast<const float*>(&acc_s[k][0])[dd] * w;
   }
-  const int Hq = g.H * g.G;
-  const int h = (int)(u % g.H);
-  const int64_t lb = u / g.H;
-  const int b = (int)(lb % g.B);
-  const int l = (int)(lb / g.B);
-  const int t = row / g.G, gq = row % g.G;
-  const int64_t orow = ((int64_t)l * g.B * tq + (int64_t)b * tq + t) * Hq + h * g.G + gq;
+  if (CL) {
+    float mc = mx;
+    for (int gi = 0; gi < cl.m; ++gi) mc = fmaxf(mc, zc_s[gi]);
+    const float a = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mx - mc);
+    const float Ls = Lt * a;  // the kept rows' share, relative to 2^mc
+    Lt = Ls;
+    at *= a;
+    for (int gi = 0; gi < cl.m; ++gi) {
+      if (zc_s[gi] == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(zc_s[gi] - mc);
+      Lt += w;
+      at = fmaf(w, bf16_to_f32(cl.vbar[(u * cl.m + gi) * D + dd]), at);
+    }
+    mx = mc;
+    if (dd == 0 && cl.bound) {
+      const double rq = (double)g.scale * (double)qn_s;
+      double dz = 0.0, dn = 0.0, vmax = (double)cl.vmax_kept[u];
+      for (int gi = 0; gi < cl.m; ++gi)
+        if (zc_s[gi] != -INFINITY) vmax = fmax(vmax, (double)vn_s[gi] + (double)cl.rv[u * cl.m + gi]);
+      for (int gi = 0; gi < cl.m; ++gi) {
+        if (zc_s[gi] == -INFINITY) continue;
+        const double zeta = exp2((double)zc_s[gi] - (double)mc) / (double)Lt;
+        const double er = exp(rq * (double)cl.rk[u * cl.m + gi]);
+        dz += (er - 1.0) * er * zeta;
+        dn += er * zeta * ((er - 1.0) * (double)vn_s[gi] + (double)cl.rv[u * cl.m + gi]);
+      }
+      cl.bound[orow] = dz <= 1.0 / 3.0 ? (float)(3.0 * (dn + vmax * dz)) : INFINITY;
+    }
+  }
   const float o = at / Lt;
   if (!isfinite(o)) report_nonfinite(g);
   out[orow * D + dd] = o;
@@ -510,10 +574,16 @@ static certkv_status launch_decode(const DecodeArgs& a, hipStream_t s) {
                 a.item_count, a.tq, a.nsplit, mp, q, a.q.s_layer, a.q.s_token, a.q.s_head, kp, vp,
                 a.packed_offsets, a.part_o, a.part_ml);
   const int M = a.tq * g.G;
-  CERTKV_LAUNCH("decode_combine", decode_combine_kernel<D>, dim3((unsigned)a.U, (unsigned)M),
-                dim3(kCombThreads), 0, s,
-                g, a.tq, a.nsplit, mp, a.packed_offsets, (const float*)a.part_o,
-                (const float2*)a.part_ml, a.out, a.lse);
+  if (a.cl.m > 0)
+    CERTKV_LAUNCH("decode_combine", (decode_combine_kernel<D, true>),
+                  dim3((unsigned)a.U, (unsigned)M), dim3(kCombThreads), 0, s, g, a.tq, a.nsplit, mp,
+                  a.packed_offsets, (const float*)a.part_o, (const float2*)a.part_ml, a.out, a.lse,
+                  a.cl, q, a.q.s_layer, a.q.s_token, a.q.s_head);
+  else
+    CERTKV_LAUNCH("decode_combine", (decode_combine_kernel<D, false>),
+                  dim3((unsigned)a.U, (unsigned)M), dim3(kCombThreads), 0, s, g, a.tq, a.nsplit, mp,
+                  a.packed_offsets, (const float*)a.part_o, (const float2*)a.part_ml, a.out, a.lse,
+                  a.cl, q, a.q.s_layer, a.q.s_token, a.q.s_head);
   return CERTKV_OK;
 }
 

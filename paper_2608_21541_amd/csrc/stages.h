@@ -122,6 +122,34 @@ certkv_status run_bitmap(const TailArgs& a, const SeqTab& st, int64_t words_tota
 certkv_status run_tail(const TailArgs& a, const SeqTab& st, hipStream_t s);
 size_t score_smem_bytes(const Geo& g, int32_t dtype);
 
+struct ClusterArgs {
+  Geo g;
+  int32_t dtype;
+  int32_t m;                    // groups per head
+  const int32_t* perm;          // [L][H][T] rank order of the pass
+  const int32_t* budgets;       // [U]
+  certkv_tensor k, v;
+  void* kbar;                   // [U][m][d] in the cache dtype
+  void* vbar;
+  int32_t* count;               // [U][m]
+  float* rk;                    // [U][m] key radii
+  float* rv;                    // [U][m] value radii
+  float* vmax_kept;             // [U]
+};
+certkv_status run_clusters(const ClusterArgs& a, const SeqTab& st, hipStream_t s);
+
+// Optional clustered-tail terms of a decode (added in the combine).
+struct DecodeClusters {
+  int32_t m;                    // 0: none
+  const uint16_t* kbar;         // [U][m][d] bf16
+  const uint16_t* vbar;
+  const int32_t* count;
+  const float* rk;
+  const float* rv;
+  const float* vmax_kept;
+  float* bound;                 // optional [L][B*tq][Hq] certificate (inf if it does not hold)
+};
+
 struct DecodeArgs {
   Geo g;
   int64_t U;
@@ -137,6 +165,7 @@ struct DecodeArgs {
   int32_t* item_count;          // their number
   float* out;                   // [L][B*tq][Hq][d]
   float* lse;                   // optional [L][B*tq][Hq]
+  DecodeClusters cl;
 };
 // Query tiles of 32 rows for M decode rows, rounded up to a power of two.
 inline int decode_nqt(int M) {

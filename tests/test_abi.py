@@ -223,3 +223,23 @@ def test_dry_run_decode_validation():
     pf = problem(dtype=_lib.CERTKV_F32)
     nf = L.certkv_decode_workspace_size(ctypes.byref(pf), 8, 0)
     assert call(pp=pf, nbytes=nf) == _lib.CERTKV_EUNSUPPORTED
+
+
+def test_dry_run_cluster_validation():
+    L = _lib.lib()
+    p = problem()
+    t = tensor()
+
+    def tail(m=8, perm=FAKE, bud=FAKE, out=FAKE):
+        return L.certkv_cluster_tail(ctypes.byref(p), t, t, perm, bud, m, out, out, out, out, out,
+                                     out, None)
+    assert tail() == _lib.CERTKV_OK
+    assert tail(m=0) == _lib.CERTKV_EINVAL and tail(m=65) == _lib.CERTKV_EINVAL
+    assert tail(perm=None) == _lib.CERTKV_EINVAL and tail(out=None) == _lib.CERTKV_EINVAL
+    n = L.certkv_decode_workspace_size(ctypes.byref(p), 8, 0)
+
+    def dec(m=8, cl=FAKE):
+        return L.certkv_decode_clustered(ctypes.byref(p), tensor(), 8, 0, FAKE, FAKE, FAKE, m, cl,
+                                         cl, cl, cl, cl, cl, FAKE, None, None, FAKE, n, None)
+    assert dec() == _lib.CERTKV_OK
+    assert dec(m=0) == _lib.CERTKV_EINVAL and dec(cl=None) == _lib.CERTKV_EINVAL

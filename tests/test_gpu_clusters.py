@@ -1,0 +1,204 @@
+"""GPU parity of the clustered tail summaries (certkv_cluster_tail) and of
+decode with them and their runtime certificate (certkv_decode_clustered)
+against the oracle, through the C ABI."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_21541_amd as ck
+import synth
+from _parity import spec_of, unit_id
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.init()
+
+
+def _pass(seqlens, m):
+    cfg = synth.config("C2", seqlens=list(seqlens), layers=1)
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg, layers=1)
+    spec.slot = False
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], with_perm=True)
+    cl = ck.cluster_tail(spec, k, v, bufs.perm, bufs.budgets, m)
+    torch.cuda.synchronize()
+    return cfg, cache, spec, bufs, cl
+
+
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_cluster_summaries_match_oracle(m):
+    cfg, cache, spec, bufs, cl = _pass([3000, 1100], m)
+    H = cfg.kv_heads
+    cu = cache["cu_seqlens"]
+    perm = bufs.perm.cpu().numpy()
+    bud = bufs.budgets.cpu().numpy()
+    got = {x: t.cpu() for x, t in cl.items()}
+    rep_diff = 0
+    for b in range(cfg.batch):
+        t0, t1 = cu[b], cu[b + 1]
+        k = cache["k"][0, t0:t1].double().numpy()
+        v = cache["v"][0, t0:t1].double().numpy()
+        for h in range(H):
+            u = unit_id(spec, 0, b, h)
+            ref = oracle.cluster_summaries(perm[0, h, t0:t1], bud[u], k[:, h], v[:, h], m)
+            assert np.array_equal(got["count"][u].numpy(), ref["count"])
+            kb = got["kbar"][u].double().numpy()
+            vb = got["vbar"][u].double().numpy()
+            # fp64 sums in another order: the stored bf16 mean may differ by one ulp
+            for x, y in ((kb, ref["kbar"]), (vb, ref["vbar"])):
+                d = np.abs(x - y)
+                assert (d <= np.spacing(np.abs(y).astype(np.float32)) * 2 ** 16 + 1e-30).all()
+                rep_diff += int((x != y).sum())
+            # radii against the GPU's own stored representatives
+            ranks = perm[0, h, t0:t1]
+            E = ranks[bud[u]:]
+            cs = -(-len(E) // m)
+            for g in range(m):
+                mem = E[g * cs:(g + 1) * cs]
+                if len(mem) == 0:
+                    continue
+                rk = np.linalg.norm(k[mem, h] - kb[g], axis=1).max()
+                rv = np.linalg.norm(v[mem, h] - vb[g], axis=1).max()
+                assert rk <= got["rk"][u, g] <= rk * (1 + 1e-6) + 1e-30
+                assert rv <= got["rv"][u, g] <= rv * (1 + 1e-6) + 1e-30
+            vk = np.linalg.norm(v[ranks[:bud[u]], h], axis=1).max()
+            assert vk <= got["vmax_kept"][u] <= vk * (1 + 1e-6)
+    log(f"m={m}: representative elements differing from the oracle's by one ulp: {rep_diff}")
+
+
+@pytest.mark.parametrize("tq", [1, 8])
+def test_clustered_decode_and_certificate_match_oracle(tq):
+    m = 16
+    cfg, cache, spec, bufs, cl = _pass([3000], m)
+    dev = torch.device("cuda:0")
+    qn = synth.make_queries(cfg, tq, "cpu")
+    out, lse, bound = ck.decode_clustered(spec, qn.to(dev), bufs.k_packed, bufs.v_packed,
+                                          bufs.packed_offsets, tq, cl)
+    torch.cuda.synchronize()
+    out, lse, bound = out.cpu().numpy(), lse.cpu().numpy(), bound.cpu().numpy()
+    H, G, D = cfg.kv_heads, cfg.group, cfg.head_dim
+    po = bufs.packed_offsets.cpu().numpy()
+    kp = bufs.k_packed.cpu().double().numpy()
+    vp = bufs.v_packed.cpu().double().numpy()
+    got = {x: t.cpu() for x, t in cl.items()}
+    finite = 0
+    for h in range(H):
+        u = unit_id(spec, 0, 0, h)
+        summ = dict(kbar=got["kbar"][u].double().numpy(), vbar=got["vbar"][u].double().numpy(),
+                    count=got["count"][u].numpy(), R=got["rk"][u].numpy(),
+                    rho=got["rv"][u].numpy(), vmax_kept=float(got["vmax_kept"][u]))
+        for row in range(tq * G):
+            t, g = divmod(row, G)
+            q = qn[0, t, h * G + g].double().numpy()
+            ref, c = oracle.cluster_estimate(q, kp[po[u]:po[u + 1]], vp[po[u]:po[u + 1]], summ,
+                                             1.0 / math.sqrt(D))
+            o = out[0, t, h * G + g]
+            assert np.linalg.norm(o - ref) <= 1e-4 * np.linalg.norm(ref), (h, row)
+            assert abs(lse[0, t, h * G + g] - c["lse"]) <= 1e-4
+            bg = bound[0, t, h * G + g]
+            if math.isfinite(c["bound"]) and c["dz"] < 0.33:
+                finite += 1
+                assert abs(bg - c["bound"]) <= 1e-3 * c["bound"] + 1e-6, (bg, c)
+            elif not math.isfinite(c["bound"]) and c["dz"] > 0.34:
+                assert math.isinf(bg)
+    log(f"clustered decode tq={tq}: finite certificates {finite}")
+
+
+def test_singleton_clusters_decode_equals_full_attention():
+    # m at least the evicted count of every head: each cluster is one key with
+    # zero radius, so the estimator is exact attention and the certificate 0
+    cfg = synth.config("C2", seqlens=[700], layers=1)
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg, layers=1)
+    spec.slot = False
+    spec.allocator = "uniform"             # every head keeps n_keep: 64 evicted keys each
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    n_keep = [700 - 64]
+    bufs = ck.compress(spec, q, k, v, n_keep, with_perm=True)
+    cl = ck.cluster_tail(spec, k, v, bufs.perm, bufs.budgets, 64)
+    tq = 2
+    qn = synth.make_queries(cfg, tq, "cpu")
+    out, _, bound = ck.decode_clustered(spec, qn.to(dev), bufs.k_packed, bufs.v_packed,
+                                        bufs.packed_offsets, tq, cl)
+    torch.cuda.synchronize()
+    assert (cl["count"].cpu().numpy() <= 1).all() and (cl["rk"].cpu() == 0).all()
+    out = out.cpu().numpy()
+    assert (bound.cpu().numpy() == 0).all()
+    H, G, D = cfg.kv_heads, cfg.group, cfg.head_dim
+    kc, vc = cache["k"][0].double().numpy(), cache["v"][0].double().numpy()
+    for h in range(H):
+        qh = qn[0, :, h * G:(h + 1) * G].double().numpy().reshape(-1, D)
+        ref, _ = oracle.decode(qh, kc[:, h], vc[:, h], 1.0 / math.sqrt(D))
+        got = out[0, :, h * G:(h + 1) * G].reshape(-1, D)
+        err = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+        assert err.max() <= 1e-4, (h, err.max())
+
+
+def test_certificate_on_tight_planted_clusters():
+    # a planted head: ranks = positions, 64 kept keys, the evicted 448 keys in
+    # 8 runs of 56 around their own centres, so the logit radii are small and
+    # the certificate is finite; the GPU's bound equals the oracle's and holds
+    # against exact attention over the whole cache
+    rng = np.random.default_rng(7)
+    cfg = synth.config("C2", seqlens=[512], layers=1)
+    H, G, D = cfg.kv_heads, cfg.group, cfg.head_dim
+    n, b, m = 512, 64, 8
+    spec = spec_of(cfg, layers=1)
+    spec.slot = False
+    k = rng.normal(size=(1, n, H, D))
+    cs = (n - b) // m
+    for g in range(m):
+        k[0, b + g * cs:b + (g + 1) * cs] = rng.normal(size=(1, H, D)) + \
+            0.01 * rng.normal(size=(cs, H, D))
+    v = rng.normal(size=(1, n, H, D))
+    dev = torch.device("cuda:0")
+    kt = torch.from_numpy(k).to(torch.bfloat16).to(dev)
+    vt = torch.from_numpy(v).to(torch.bfloat16).to(dev)
+    perm = torch.arange(n, dtype=torch.int32).repeat(H, 1).reshape(1, H, n).to(dev)
+    budgets = torch.full((H,), b, dtype=torch.int32, device=dev)
+    cl = ck.cluster_tail(spec, kt, vt, perm, budgets, m)
+    kp = kt[0, :b].permute(1, 0, 2).reshape(H * b, D).contiguous()
+    vp = vt[0, :b].permute(1, 0, 2).reshape(H * b, D).contiguous()
+    po = torch.arange(H + 1, dtype=torch.int64, device=dev) * b
+    tq = 4
+    qn = synth.make_queries(cfg, tq, "cpu")
+    out, _, bound = ck.decode_clustered(spec, qn.to(dev), kp, vp, po, tq, cl)
+    torch.cuda.synchronize()
+    out, bound = out.cpu().numpy(), bound.cpu().numpy()
+    got = {x: t.cpu() for x, t in cl.items()}
+    kd = kt.cpu().double().numpy()[0]
+    vd = vt.cpu().double().numpy()[0]
+    finite, worst = 0, 0.0
+    for h in range(H):
+        summ = dict(kbar=got["kbar"][h].double().numpy(), vbar=got["vbar"][h].double().numpy(),
+                    count=got["count"][h].numpy(), R=got["rk"][h].numpy(),
+                    rho=got["rv"][h].numpy(), vmax_kept=float(got["vmax_kept"][h]))
+        for row in range(tq * G):
+            t, g = divmod(row, G)
+            q = qn[0, t, h * G + g].double().numpy()
+            ref, c = oracle.cluster_estimate(q, kd[:b, h], vd[:b, h], summ, 1.0 / math.sqrt(D))
+            exact, _ = oracle.decode(q[None], kd[:, h], vd[:, h], 1.0 / math.sqrt(D))
+            o = out[0, t, h * G + g]
+            bg = float(bound[0, t, h * G + g])
+            assert math.isfinite(c["bound"]) and math.isfinite(bg), c
+            finite += 1
+            assert abs(bg - c["bound"]) <= 1e-3 * c["bound"], (bg, c)
+            err = float(np.linalg.norm(o - exact[0]))
+            assert err <= bg, (err, bg)
+            worst = max(worst, err / bg)
+    log(f"planted clusters: {finite} finite certificates, worst error / bound {worst:.3g}")
