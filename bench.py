@@ -333,6 +333,36 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
     ms, kern, roof = time_tq(args.tq, args.steps, args.warmup)
     ms1, kern1, roof1 = time_tq(1, args.steps, args.warmup)
     log(f"decode tq={args.tq}: {ms:.3f} ms; tq=1: {ms1:.3f} ms")
+    clusters = None
+    if args.clusters > 0:
+        assert not spec.slot, "clustered summaries replace the slot: use --variant no_slot"
+        m = args.clusters
+        cl = ck.cluster_tail(spec, cache["k"], cache["v"], bufs.perm, bufs.budgets, m)
+        torch.cuda.synchronize()
+        qn = synth.make_queries(cfg, args.tq, dev)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(args.steps):
+            ck.cluster_tail(spec, cache["k"], cache["v"], bufs.perm, bufs.budgets, m)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        tail_ms = t0.elapsed_time(t1) / args.steps
+        ck.decode_clustered(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, args.tq,
+                            cl, max_rows=max_rows)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(args.steps):
+            _, _, bound = ck.decode_clustered(spec, qn, bufs.k_packed, bufs.v_packed,
+                                              bufs.packed_offsets, args.tq, cl, max_rows=max_rows)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        dec_ms = t0.elapsed_time(t1) / args.steps
+        evicted = int(cfg.layers * cfg.kv_heads * sum(cfg.seqlens)) - rows
+        clusters = {"m": m, "cluster_tail_ms": tail_ms,
+                    "cluster_tail_GBps": 2 * evicted * cfg.head_dim * e * 2 / (tail_ms / 1e3) / 1e9,
+                    "decode_clustered_ms": dec_ms,
+                    "finite_certificates": float(torch.isfinite(bound).float().mean())}
+        log(f"clusters: {clusters}")
     lift = None
     if cfg.batch == 1:
         qn = synth.make_queries(cfg, args.tq, dev)
@@ -356,6 +386,7 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
         "roofline": roof, "kernels": kern,
         "tq1": {"ms_per_step": ms1, "roofline": roof1, "kernels": kern1},
         "lift_bound": lift,
+        "clusters": clusters,
     }
     print(json.dumps(rec), flush=True)
 
@@ -371,6 +402,9 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="time decode over the packed cache instead of the pass")
     ap.add_argument("--tq", type=int, default=32, help="new queries per sequence (--decode)")
+    ap.add_argument("--clusters", type=int, default=0,
+                    help="with --decode --variant no_slot: time M clustered tail summaries "
+                         "per head and the clustered decode")
     ap.add_argument("--variant", default="default", choices=sorted(VARIANTS),
                     help="a one-factor ablation of the pass (statistic, allocator, slot, alpha)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -417,7 +451,7 @@ def main():
     spec.allocator = var.get("allocator", "lagrangian")
     spec.slot = var.get("slot", True)
     alpha = var.get("alpha", 0.2)
-    bufs = ck.CompressBuffers(spec, n_keep, dev)
+    bufs = ck.CompressBuffers(spec, n_keep, dev, with_perm=args.clusters > 0)
     q, k, v = cache["q_win"], cache["k"], cache["v"]
     torch.cuda.synchronize()
 

@@ -12,9 +12,11 @@
 // decode reads.  The workgroup of group 0 also records the largest kept value
 // norm, one of the terms of the runtime certificate.
 //
-// One 256-thread workgroup per (unit, group): a pass over the members sums
-// keys and values (a thread per (tensor, dim), rows four at a time), then a
-// pass measures the distances (a wave per row, lanes over dims).
+// One 256-thread workgroup per (unit, group), D/8 lanes per row (16-byte
+// loads of 8 dims of K and V) and 256 / (D/8) rows in flight: a pass over
+// the members sums keys and values in fp64 (row-lane partials combined in a
+// fixed order through LDS), then a pass measures the distances (reduced over
+// the lanes of a row by shuffles).
 #include "stages.h"
 
 namespace certkv {
@@ -42,10 +44,26 @@ __device__ __forceinline__ float cl_round_up(double x) {
   return f;
 }
 
-__device__ __forceinline__ double cl_wave_sum(double x) {
+// Eight consecutive elements of a row as floats (16 bytes of bf16, or 32 of
+// fp32).
+template <typename T>
+__device__ __forceinline__ void cl_load8(const T* p, float* x);
+template <>
+__device__ __forceinline__ void cl_load8<uint16_t>(const uint16_t* p, float* x) {
+  const uint4 r = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
-  return x;
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = bf16_lo(w[i]);
+    x[2 * i + 1] = bf16_hi(w[i]);
+  }
+}
+template <>
+__device__ __forceinline__ void cl_load8<float>(const float* p, float* x) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 c = reinterpret_cast<const float4*>(p)[1];
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
 }
 
 template <int D, typename T>
@@ -55,7 +73,9 @@ __global__ __launch_bounds__(kClThreads) void cluster_tail_kernel(
     int64_t k_sh, const T* __restrict__ vc, int64_t v_sl, int64_t v_st, int64_t v_sh,
     T* __restrict__ kbar, T* __restrict__ vbar, int32_t* __restrict__ count,
     float* __restrict__ rk, float* __restrict__ rv, float* __restrict__ vmax_kept) {
-  __shared__ double rep[2][D];
+  constexpr int CL = D / 8;                 // lanes per row (8 dims each)
+  constexpr int RL = kClThreads / CL;       // rows in flight
+  __shared__ double part[RL][2][D];         // per row-lane sums, then the representatives
   __shared__ double wmax[3][kClThreads / 64];
   const int gi = blockIdx.x % m;
   const int hb = blockIdx.x / m;
@@ -70,59 +90,108 @@ __global__ __launch_bounds__(kClThreads) void cluster_tail_kernel(
   const int r0 = min(n, b + gi * cs), r1 = min(n, r0 + cs);
   const int cnt = r1 - r0;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const T* kh = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
-  const T* vh = vc + (int64_t)l * v_sl + tok0 * v_st + (int64_t)h * v_sh;
+  const int cl = t % CL, rl = t / CL;       // dims 8 cl .. 8 cl + 7 of rows rl, rl + RL, ...
+  const T* kh = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh + 8 * cl;
+  const T* vh = vc + (int64_t)l * v_sl + tok0 * v_st + (int64_t)h * v_sh + 8 * cl;
   const int64_t cu = u * m + gi;
-  // pass 1: sums over the members, thread t -> tensor t / D, dim t % D
-  if (t < 2 * D) {
-    const int kv = t / D, dd = t % D;
-    const T* x = kv ? vh : kh;
-    const int64_t xs = kv ? v_st : k_st;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    int r = r0;
-    for (; r + 3 < r1; r += 4) {
-      const int j0 = perm[base + r], j1 = perm[base + r + 1];
-      const int j2 = perm[base + r + 2], j3 = perm[base + r + 3];
-      s0 += (double)cl_load(x + (int64_t)j0 * xs + dd);
-      s1 += (double)cl_load(x + (int64_t)j1 * xs + dd);
-      s2 += (double)cl_load(x + (int64_t)j2 * xs + dd);
-      s3 += (double)cl_load(x + (int64_t)j3 * xs + dd);
+  // pass 1: sums over the members (fp64), each lane its 8 dims of K and V
+  double sk[8], sv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) sk[i] = sv[i] = 0.0;
+  // the next row's position is loaded one step ahead (clamped into the
+  // group, so the load is always in bounds)
+  int64_t jn = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
+  for (int r = r0 + rl; r < r1; r += RL) {
+    const int64_t j = jn;
+    jn = perm[base + min(r + RL, r1 - 1)];
+    float xk[8], xv[8];
+    cl_load8(kh + j * k_st, xk);
+    cl_load8(vh + j * v_st, xv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      sk[i] += (double)xk[i];
+      sv[i] += (double)xv[i];
     }
-    for (; r < r1; ++r) s0 += (double)cl_load(x + (int64_t)perm[base + r] * xs + dd);
-    const double mean = cnt > 0 ? ((s0 + s1) + (s2 + s3)) / (double)cnt : 0.0;
-    const T stored = cl_store<T>((float)mean);
-    (kv ? vbar : kbar)[cu * D + dd] = stored;
-    rep[kv][dd] = (double)cl_load(&stored);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    part[rl][0][8 * cl + i] = sk[i];
+    part[rl][1][8 * cl + i] = sv[i];
   }
   __syncthreads();
-  // pass 2: squared distances to the stored representatives, a wave per row
-  double mk = 0.0, mv = 0.0;
-  for (int r = r0 + wave; r < r1; r += kClThreads / 64) {
-    const int j = perm[base + r];
-    double sk = 0.0, sv = 0.0;
+  if (t < 2 * D) {  // one thread per (tensor, dim): the row-lanes' sums in order
+    const int kv = t / D, dd = t % D;
+    double s = 0.0;
+    for (int q = 0; q < RL; ++q) s += part[q][kv][dd];
+    const double mean = cnt > 0 ? s / (double)cnt : 0.0;
+    const T stored = cl_store<T>((float)mean);
+    (kv ? vbar : kbar)[cu * D + dd] = stored;
+    sk[0] = (double)cl_load(&stored);
+  }
+  __syncthreads();
+  if (t < 2 * D) part[0][t / D][t % D] = sk[0];
+  __syncthreads();
+  double rep_k[8], rep_v[8];
 #pragma unroll
-    for (int dd = lane; dd < D; dd += 64) {
-      const double dk = (double)cl_load(kh + (int64_t)j * k_st + dd) - rep[0][dd];
-      const double dv = (double)cl_load(vh + (int64_t)j * v_st + dd) - rep[1][dd];
-      sk = fma(dk, dk, sk);
-      sv = fma(dv, dv, sv);
+  for (int i = 0; i < 8; ++i) {
+    rep_k[i] = part[0][0][8 * cl + i];
+    rep_v[i] = part[0][1][8 * cl + i];
+  }
+  // pass 2: squared distances to the stored representatives; the CL lanes of
+  // a row are consecutive lanes of one wave, reduced by shuffles
+  // (every lane runs the same number of steps, so the shuffles stay
+  // within full row groups)
+  double mk = 0.0, mv = 0.0;
+  const int steps = (cnt + RL - 1) / RL;
+  jn = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
+  for (int k = 0; k < steps; ++k) {
+    const int r = r0 + rl + k * RL;
+    const int64_t j = jn;
+    jn = perm[base + min(r + RL, r1 - 1)];
+    double dk2 = 0.0, dv2 = 0.0;
+    if (r < r1) {
+      float xk[8], xv[8];
+      cl_load8(kh + j * k_st, xk);
+      cl_load8(vh + j * v_st, xv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const double a = (double)xk[i] - rep_k[i], c = (double)xv[i] - rep_v[i];
+        dk2 = fma(a, a, dk2);
+        dv2 = fma(c, c, dv2);
+      }
     }
-    mk = fmax(mk, cl_wave_sum(sk));
-    mv = fmax(mv, cl_wave_sum(sv));
+#pragma unroll
+    for (int o = CL / 2; o >= 1; o >>= 1) {
+      dk2 += __shfl_xor(dk2, o, 64);
+      dv2 += __shfl_xor(dv2, o, 64);
+    }
+    mk = fmax(mk, dk2);
+    mv = fmax(mv, dv2);
   }
   // group 0 also takes the largest kept value norm (ranks 0..b-1)
   double mkept = 0.0;
   if (gi == 0) {
-    for (int r = wave; r < b; r += kClThreads / 64) {
-      const int j = perm[base + r];
-      double sv = 0.0;
+    const int ksteps = (b + RL - 1) / RL;
+    for (int k = 0; k < ksteps; ++k) {
+      const int r = rl + k * RL;
+      double s2 = 0.0;
+      if (r < b) {
+        const int64_t j = perm[base + r];
+        float xv[8];
+        cl_load8(vh + j * v_st, xv);
 #pragma unroll
-      for (int dd = lane; dd < D; dd += 64) {
-        const double x = (double)cl_load(vh + (int64_t)j * v_st + dd);
-        sv = fma(x, x, sv);
+        for (int i = 0; i < 8; ++i) s2 = fma((double)xv[i], (double)xv[i], s2);
       }
-      mkept = fmax(mkept, cl_wave_sum(sv));
+#pragma unroll
+      for (int o = CL / 2; o >= 1; o >>= 1) s2 += __shfl_xor(s2, o, 64);
+      mkept = fmax(mkept, s2);
     }
+  }
+#pragma unroll
+  for (int o = 32; o >= CL; o >>= 1) {
+    mk = fmax(mk, __shfl_xor(mk, o, 64));
+    mv = fmax(mv, __shfl_xor(mv, o, 64));
+    mkept = fmax(mkept, __shfl_xor(mkept, o, 64));
   }
   if (lane == 0) {
     wmax[0][wave] = mk;
