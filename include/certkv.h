@@ -336,7 +336,7 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
  *   max_rows       bound on the rows of any head's segment (b_h + 1), or 0 for
  *                  n_b of the longest sequence; it sizes the workspace. A
  *                  longer segment stores CERTKV_ERANGE in *dev_status and its
- *                  rows past the next multiple of 1024 are left out
+ *                  rows past the next multiple of 4096 are left out
  *   k_packed, v_packed, packed_offsets  the packed cache of certkv_compact or
  *                  certkv_compress (device)
  *   out            [L][B*tq][Hq][d] fp32 out (contiguous)

@@ -7,7 +7,7 @@
 // over the unit's packed segment:
 //   z_i = scale <q, k_i>,  out = sum_i softmax(z)_i v_i,  lse = log sum e^z.
 //
-// Split over keys: the work items are (unit, 1024-key chunk) pairs, listed on
+// Split over keys: the work items are (unit, 4096-key chunk) pairs, listed on
 // the device and taken in a fixed stride by a persistent grid of as many
 // workgroups as stay resident.  A workgroup holds the unit's query tiles of
 // 32 rows, one wave each; with fewer than four tiles, two or four waves share
@@ -31,7 +31,7 @@
 
 namespace certkv {
 
-constexpr int kDecKeys = 1024;  // keys per workgroup (one split)
+constexpr int kDecKeys = 4096;  // keys per work item (one split)
 constexpr int kDecTile = 32;    // keys per tile
 
 typedef __bf16 dec_bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));

@@ -77,7 +77,7 @@ def _check_against_oracle(cfg, cache, spec, bufs, tq, seed_offset=7919):
 
 @pytest.mark.parametrize("tq", [1, 8, 33, 65])
 def test_decode_matches_oracle_ragged_batch(tq):
-    # ragged lengths (several 1024-key chunks and a ragged last tile), two
+    # ragged lengths (segments of varying length, ragged last tiles), two
     # layers; tq = 33 gives 132 query rows (a padded fifth 32-row tile), tq = 65
     # gives 260 rows (sixteen query tiles, the largest workgroup)
     cfg = synth.config("C4", seqlens=[3000, 8192 + 5, 1024], layers=2)
@@ -112,7 +112,8 @@ def test_keep_all_decode_equals_full_attention():
     # n_keep = n: every head keeps n - 1 real rows and its slot is the one
     # evicted key itself, so decode over the packed cache is exact attention
     # over the whole cache.
-    cfg = synth.config("C2", seqlens=[2500])
+    # 9037 keys: segments of three 4096-key chunks with a ragged last tile
+    cfg = synth.config("C2", seqlens=[9037])
     cache = synth.make_cache(cfg, "cpu")
     n = cfg.seqlens[0]
     spec, bufs = _compress(cfg, cache, n_keep=[n])
@@ -184,10 +185,10 @@ def test_future_query_lift_bound_on_gpu_outputs(name):
 
 
 def test_keep_all_segment_of_exactly_one_chunk():
-    # n = 1024 with n_keep = n: every head's segment (n - 1 kept rows and the
-    # slot) fills exactly one 1024-key chunk, which is also the default row
+    # n = 4096 with n_keep = n: every head's segment (n - 1 kept rows and the
+    # slot) fills exactly one 4096-key chunk, which is also the default row
     # bound of the workspace.
-    cfg = synth.config("C2", seqlens=[1024])
+    cfg = synth.config("C2", seqlens=[4096])
     cache = synth.make_cache(cfg, "cpu")
     n = cfg.seqlens[0]
     spec, bufs = _compress(cfg, cache, n_keep=[n])
@@ -197,9 +198,10 @@ def test_keep_all_segment_of_exactly_one_chunk():
 
 
 def test_decode_row_bound_gives_same_output_and_flags_overflow():
-    cfg = synth.config("C4", seqlens=[3000, 5000])
+    # keep-all segments of 9036 and 5999 rows: three and two 4096-key chunks
+    cfg = synth.config("C4", seqlens=[9037, 6000])
     cache = synth.make_cache(cfg, "cpu")
-    spec, bufs = _compress(cfg, cache)
+    spec, bufs = _compress(cfg, cache, n_keep=list(cfg.seqlens))
     dev = torch.device("cuda:0")
     tq = 8
     qn = synth.make_queries(cfg, tq, "cpu").to(dev)
@@ -212,11 +214,11 @@ def test_decode_row_bound_gives_same_output_and_flags_overflow():
                       max_rows=seg)
     torch.cuda.synchronize()
     assert int(status.item()) == ck.CERTKV_OK
-    # the same 1024-key chunks in the same order: the same bits
+    # the same 4096-key chunks in the same order: the same bits
     assert torch.equal(ref, tight)
-    assert ck.decode_workspace_size(spec, tq, seg) < ck.decode_workspace_size(spec, tq)
+    assert ck.decode_workspace_size(spec, tq, seg - 4096) < ck.decode_workspace_size(spec, tq)
     # a bound below the longest segment (by more than a chunk) is reported
     ck.decode(spec, qn, bufs.k_packed, bufs.v_packed, bufs.packed_offsets, tq,
-              max_rows=seg - 1024)
+              max_rows=seg - 4096)
     torch.cuda.synchronize()
     assert int(status.item()) == ck.CERTKV_ERANGE
