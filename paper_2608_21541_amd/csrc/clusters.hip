@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kClThreads) void cluster_tail_kernel(
   const int64_t tok0 = st.start[bi];
   const int64_t u = unit_index(g, l, st.first + bi, h);
   const int64_t base = lht_base(g, l, h, tok0);
-  const int b = budgets[u];
+  const int b = min(max(budgets[u], 0), n);  // caller budgets clamped into [0, n]
   const int E = n - b;
   const int cs = (E + m - 1) / m;
   const int r0 = min(n, b + gi * cs), r1 = min(n, r0 + cs);
