@@ -202,3 +202,66 @@ def test_certificate_on_tight_planted_clusters():
             assert err <= bg, (err, bg)
             worst = max(worst, err / bg)
     log(f"planted clusters: {finite} finite certificates, worst error / bound {worst:.3g}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cluster_summaries_head_dim_64(dtype):
+    # head_dim 64 without grouping, in fp32 (summaries stored in fp32) and
+    # bf16 (also decoded with the clusters)
+    cfg = synth.config("C1", seqlens=[2000, 1500])
+    if dtype == "bf16":
+        cfg.dtype = torch.bfloat16
+    cache = synth.make_cache(cfg, "cpu")
+    spec = spec_of(cfg, layers=1)
+    spec.slot = False
+    dev = torch.device("cuda:0")
+    q, k, v = (cache[x].to(dev) for x in ("q_win", "k", "v"))
+    bufs = ck.compress(spec, q, k, v, cache["n_keep"], with_perm=True)
+    m = 8
+    cl = ck.cluster_tail(spec, k, v, bufs.perm, bufs.budgets, m)
+    torch.cuda.synchronize()
+    cu = cache["cu_seqlens"]
+    perm = bufs.perm.cpu().numpy()
+    bud = bufs.budgets.cpu().numpy()
+    got = {x: t.cpu() for x, t in cl.items()}
+    for b in range(cfg.batch):
+        t0, t1 = cu[b], cu[b + 1]
+        kk = cache["k"][0, t0:t1].double().numpy()
+        vv = cache["v"][0, t0:t1].double().numpy()
+        for h in range(cfg.kv_heads):
+            u = unit_id(spec, 0, b, h)
+            ref = oracle.cluster_summaries(perm[0, h, t0:t1], bud[u], kk[:, h], vv[:, h], m,
+                                           bf16=(dtype == "bf16"))
+            assert np.array_equal(got["count"][u].numpy(), ref["count"])
+            for x, y in ((got["kbar"][u].double().numpy(), ref["kbar"]),
+                         (got["vbar"][u].double().numpy(), ref["vbar"])):
+                ulp = np.spacing(np.abs(y).astype(np.float32)).astype(np.float64)
+                assert (np.abs(x - y) <= ulp * (2 ** 16 if dtype == "bf16" else 2)).all()
+            np.testing.assert_allclose(got["rk"][u].numpy(), ref["R"], rtol=1e-5)
+            np.testing.assert_allclose(got["rv"][u].numpy(), ref["rho"], rtol=1e-5)
+    if dtype != "bf16":
+        return
+    tq = 5
+    qn = synth.make_queries(cfg, tq, "cpu")
+    out, lse, _ = ck.decode_clustered(spec, qn.to(dev), bufs.k_packed, bufs.v_packed,
+                                      bufs.packed_offsets, tq, cl)
+    torch.cuda.synchronize()
+    out, lse = out.cpu().numpy(), lse.cpu().numpy()
+    po = bufs.packed_offsets.cpu().numpy()
+    kp = bufs.k_packed.cpu().double().numpy()
+    vp = bufs.v_packed.cpu().double().numpy()
+    D = cfg.head_dim
+    for b in range(cfg.batch):
+        for h in range(cfg.kv_heads):
+            u = unit_id(spec, 0, b, h)
+            summ = dict(kbar=got["kbar"][u].double().numpy(),
+                        vbar=got["vbar"][u].double().numpy(), count=got["count"][u].numpy(),
+                        R=got["rk"][u].numpy(), rho=got["rv"][u].numpy(),
+                        vmax_kept=float(got["vmax_kept"][u]))
+            for t in range(tq):
+                qv = qn[0, b * tq + t, h].double().numpy()
+                ref, c = oracle.cluster_estimate(qv, kp[po[u]:po[u + 1]], vp[po[u]:po[u + 1]],
+                                                 summ, 1.0 / math.sqrt(D))
+                o = out[0, b * tq + t, h]
+                assert np.linalg.norm(o - ref) <= 1e-4 * np.linalg.norm(ref), (b, h, t)
+                assert abs(lse[0, b * tq + t, h] - c["lse"]) <= 1e-4
