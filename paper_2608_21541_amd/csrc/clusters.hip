@@ -98,19 +98,29 @@ __global__ __launch_bounds__(kClThreads) void cluster_tail_kernel(
   double sk[8], sv[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) sk[i] = sv[i] = 0.0;
-  // the next row's position is loaded one step ahead (clamped into the
-  // group, so the load is always in bounds)
-  int64_t jn = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
-  for (int r = r0 + rl; r < r1; r += RL) {
-    const int64_t j = jn;
-    jn = perm[base + min(r + RL, r1 - 1)];
-    float xk[8], xv[8];
-    cl_load8(kh + j * k_st, xk);
-    cl_load8(vh + j * v_st, xv);
+  // Two rows per lane and step (rows r and r + RL), their positions loaded
+  // one step ahead; positions past the group are clamped to its last row
+  // (always in bounds) and such a row is added with weight zero.
+  const int steps = (cnt + 2 * RL - 1) / (2 * RL);
+  int64_t ja = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
+  int64_t jb = cnt > 0 ? perm[base + min(r0 + rl + RL, r1 - 1)] : 0;
+  for (int k = 0; k < steps; ++k) {
+    const int r = r0 + rl + 2 * k * RL;
+    const int64_t j0 = ja, j1 = jb;
+    ja = perm[base + min(r + 2 * RL, r1 - 1)];
+    jb = perm[base + min(r + 3 * RL, r1 - 1)];
+    float xk0[8], xv0[8], xk1[8], xv1[8];
+    cl_load8(kh + j0 * k_st, xk0);
+    cl_load8(vh + j0 * v_st, xv0);
+    cl_load8(kh + j1 * k_st, xk1);
+    cl_load8(vh + j1 * v_st, xv1);
+    const double w0 = r < r1 ? 1.0 : 0.0, w1 = r + RL < r1 ? 1.0 : 0.0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      sk[i] += (double)xk[i];
-      sv[i] += (double)xv[i];
+      sk[i] = fma(w0, (double)xk0[i], sk[i]);
+      sv[i] = fma(w0, (double)xv0[i], sv[i]);
+      sk[i] = fma(w1, (double)xk1[i], sk[i]);
+      sv[i] = fma(w1, (double)xv1[i], sv[i]);
     }
   }
 #pragma unroll
@@ -141,32 +151,40 @@ __global__ __launch_bounds__(kClThreads) void cluster_tail_kernel(
   // a row are consecutive lanes of one wave, reduced by shuffles
   // (every lane runs the same number of steps, so the shuffles stay
   // within full row groups)
+  // (clamped rows repeat the group's last row, whose distance is counted
+  // anyway, so the maximum is unchanged)
   double mk = 0.0, mv = 0.0;
-  const int steps = (cnt + RL - 1) / RL;
-  jn = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
+  ja = cnt > 0 ? perm[base + min(r0 + rl, r1 - 1)] : 0;
+  jb = cnt > 0 ? perm[base + min(r0 + rl + RL, r1 - 1)] : 0;
   for (int k = 0; k < steps; ++k) {
-    const int r = r0 + rl + k * RL;
-    const int64_t j = jn;
-    jn = perm[base + min(r + RL, r1 - 1)];
-    double dk2 = 0.0, dv2 = 0.0;
-    if (r < r1) {
-      float xk[8], xv[8];
-      cl_load8(kh + j * k_st, xk);
-      cl_load8(vh + j * v_st, xv);
+    const int r = r0 + rl + 2 * k * RL;
+    const int64_t j0 = ja, j1 = jb;
+    ja = perm[base + min(r + 2 * RL, r1 - 1)];
+    jb = perm[base + min(r + 3 * RL, r1 - 1)];
+    float xk0[8], xv0[8], xk1[8], xv1[8];
+    cl_load8(kh + j0 * k_st, xk0);
+    cl_load8(vh + j0 * v_st, xv0);
+    cl_load8(kh + j1 * k_st, xk1);
+    cl_load8(vh + j1 * v_st, xv1);
+    double dk0 = 0.0, dv0 = 0.0, dk1 = 0.0, dv1 = 0.0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const double a = (double)xk[i] - rep_k[i], c = (double)xv[i] - rep_v[i];
-        dk2 = fma(a, a, dk2);
-        dv2 = fma(c, c, dv2);
-      }
+    for (int i = 0; i < 8; ++i) {
+      const double a0 = (double)xk0[i] - rep_k[i], c0 = (double)xv0[i] - rep_v[i];
+      const double a1 = (double)xk1[i] - rep_k[i], c1 = (double)xv1[i] - rep_v[i];
+      dk0 = fma(a0, a0, dk0);
+      dv0 = fma(c0, c0, dv0);
+      dk1 = fma(a1, a1, dk1);
+      dv1 = fma(c1, c1, dv1);
     }
 #pragma unroll
     for (int o = CL / 2; o >= 1; o >>= 1) {
-      dk2 += __shfl_xor(dk2, o, 64);
-      dv2 += __shfl_xor(dv2, o, 64);
+      dk0 += __shfl_xor(dk0, o, 64);
+      dv0 += __shfl_xor(dv0, o, 64);
+      dk1 += __shfl_xor(dk1, o, 64);
+      dv1 += __shfl_xor(dv1, o, 64);
     }
-    mk = fmax(mk, dk2);
-    mv = fmax(mv, dv2);
+    mk = fmax(mk, fmax(dk0, dk1));
+    mv = fmax(mv, fmax(dv0, dv1));
   }
   // group 0 also takes the largest kept value norm (ranks 0..b-1)
   double mkept = 0.0;
