@@ -39,7 +39,7 @@ KERNEL_SOURCES = {
 }
 
 
-def algorithmic_model(cfg, n_keep):
+def algorithmic_model(cfg, n_keep, lse_in=False):
     """Algorithmic HBM bytes, MFMA flops and VALU slots per launch of each kernel.
 
     Per (KV head, token) unit with d = head_dim, e = element bytes, keep
@@ -58,6 +58,8 @@ def algorithmic_model(cfg, n_keep):
     spend one multiply (or fma), one exp2 (half rate: 2 slots) and one add;
     the fp64 curves spend per (rank, dim) two conversions and two fma in the
     totals pass and two conversions and three fma in the walk.
+    With the caller's row log-sum-exp (lse_in) score pass 1 does not run, so
+    K is read once.
     """
     L, H, D = cfg.layers, cfg.kv_heads, cfg.head_dim
     e = 2 if cfg.dtype_name == "bf16" else 4
@@ -74,6 +76,8 @@ def algorithmic_model(cfg, n_keep):
         "select": (4 + 4 * f + 0.125, 0, 0),
         "tail_compact_gather": (f * (4 * D * e + 12), 0, 0),
     }
+    if lse_in:
+        del per["score_pass1_mfma"]
     return {k: (b * ht, fl * ht, sl * ht) for k, (b, fl, sl) in per.items()}, ht
 
 
@@ -138,6 +142,64 @@ def roofline_of(name, model, avg_ms, workload):
     return {"bound": bound, "achieved": ach, "peak": peak, "unit": unit, "frac": ach / peak,
             "traffic": recorded_traffic(name, workload), "kernel": name,
             "lower_bounds_ms": {c[0]: c[1] * 1e3 for c in cands}}
+
+
+def run_metadata(cfg, dev):
+    """Digest of every source the run executes, of the workload's
+    configuration, and the device's identity and peak clocks."""
+    import ctypes
+    import hashlib
+    import torch
+    h = hashlib.sha256()
+    for sub in ("paper_2608_21541_amd/csrc", "include", "synth", "paper_2608_21541_amd"):
+        d = os.path.join(ROOT, sub)
+        for name in sorted(os.listdir(d)):
+            if name.endswith((".hip", ".h", ".py")):
+                with open(os.path.join(d, name), "rb") as fh:
+                    h.update(name.encode() + b"\0" + fh.read())
+    with open(os.path.abspath(__file__), "rb") as fh:
+        h.update(fh.read())
+    conf = json.dumps({k: (str(v) if k == "dtype" else v) for k, v in vars(cfg).items()},
+                      sort_keys=True, default=str)
+    props = torch.cuda.get_device_properties(dev)
+    clocks = {}
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        for name, attr in (("sclk_peak_mhz", 5), ("mclk_peak_mhz", 60)):
+            val = ctypes.c_int(0)
+            if hip.hipDeviceGetAttribute(ctypes.byref(val), attr, dev.index or 0) == 0:
+                clocks[name] = val.value / 1000.0
+    except OSError:
+        pass
+    return {"source_sha256": h.hexdigest(), "config_sha256": hashlib.sha256(conf.encode()).hexdigest(),
+            "device": props.name, "arch": getattr(props, "gcnArchName", ""),
+            "cus": props.multi_processor_count, **clocks}
+
+
+def time_passes(run, steps, stream, profile):
+    """Average milliseconds of `steps` calls of run(), timed with events on the
+    launch stream; with profile the library brackets every launch with events
+    and the per-kernel averages are returned too."""
+    import torch
+    import paper_2608_21541_amd as ck
+    torch.cuda.synchronize()
+    if profile:
+        ck.profile_reset()
+        ck.profile_enable(True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        run()
+    end.record(stream)
+    torch.cuda.synchronize()
+    kernels = None
+    if profile:
+        prof = ck.profile_read()
+        ck.profile_enable(False)
+        ck.profile_reset()
+        kernels = {name: {"launches_per_step": cnt / steps, "avg_ms": tot / max(cnt, 1)}
+                   for name, (cnt, tot) in prof.items()}
+    return start.elapsed_time(end) / steps, kernels
 
 
 def cpu_baseline(cache, cfg, n_keep, log, layers=6):
@@ -398,6 +460,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="C3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-lse-line", action="store_true",
+                    help="skip the pass with the caller's row log-sum-exp")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--decode", action="store_true",
                     help="time decode over the packed cache instead of the pass")
@@ -468,27 +532,18 @@ def main():
     if args.decode:
         run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log)
         return
+    run = lambda: ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs)
     for _ in range(args.warmup):
-        ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs)
-    torch.cuda.synchronize()
-    # Timed region.  Every launch of the pass is bracketed by HIP events on
-    # the stream it runs on, giving per-kernel durations of these same steps.
-    ck.profile_reset()
-    ck.profile_enable(True)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs)
-    end.record(stream)
-    torch.cuda.synchronize()
-    prof = ck.profile_read()
-    ck.profile_enable(False)
-    ck.profile_reset()
-    ms = start.elapsed_time(end) / args.steps
+        run()
+    # Timed region: the plain pass, no profiling events.  A second run of the
+    # same steps with every launch bracketed by HIP events on its stream gives
+    # the per-kernel durations (and the events' overhead on the pass).
+    ms, _ = time_passes(run, args.steps, stream, profile=False)
+    ms_prof, kernels = time_passes(run, args.steps, stream, profile=True)
     tokens = sum(cfg.seqlens)
-    value = tokens * cfg.layers / (ms / 1e3) / cfg.layers  # tokens per second per layer
-    log(f"pass: {ms:.3f} ms")
+    # KV tokens compressed per second per layer: n / (T_pass / L)
+    value = tokens / (ms / 1e3 / cfg.layers)
+    log(f"pass: {ms:.3f} ms ({ms_prof:.3f} ms with per-kernel events)")
 
     st = bufs.alloc_stats.cpu()
     alloc_diag = {"repairs_mean": float(st[:, 0].float().mean()), "repairs_max": int(st[:, 0].max()),
@@ -496,18 +551,44 @@ def main():
                   "repair_us_mean": float(st[:, 2].float().mean()) / 100.0}
     log(f"allocation: {alloc_diag}")
     model, ht = algorithmic_model(cfg, n_keep)
-    kernels = {}
-    for name, (cnt, tot) in prof.items():
-        avg = tot / max(cnt, 1)
-        kernels[name] = {"launches_per_step": cnt / args.steps, "avg_ms": avg}
-    dom = max(kernels, key=lambda n_: kernels[n_]["avg_ms"] * kernels[n_]["launches_per_step"])
-    roof = roofline_of(dom, model, kernels[dom]["avg_ms"], args.config)
+
+    def summarize(kernels, model):
+        for name, kk in kernels.items():
+            if name in model:
+                r = roofline_of(name, model, kk["avg_ms"], args.config)
+                kk.update({"bound": r["bound"], "frac": r["frac"]})
+        dom = max(kernels, key=lambda n_: kernels[n_]["avg_ms"] * kernels[n_]["launches_per_step"])
+        return roofline_of(dom, model, kernels[dom]["avg_ms"], args.config)
+
+    roof = summarize(kernels, model)
     pass_bytes = sum(b for b, _, _ in model.values())
-    for name, kk in kernels.items():
-        if name in model:
-            r = roofline_of(name, model, kk["avg_ms"], args.config)
-            kk.update({"bound": r["bound"], "frac": r["frac"]})
     log(json.dumps(kernels, indent=1))
+
+    # The same pass with the caller's row log-sum-exp (as an attention prefill
+    # already has it): pass 1 is skipped and K is read once.  The log-sum-exp
+    # comes from an untimed pass that exports it.
+    lse_line = None
+    if args.variant == "default" and not args.no_lse_line:
+        lbufs = ck.CompressBuffers(spec, n_keep, dev, with_lse=True)
+        ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=lbufs)
+        lse = lbufs.lse.clone()
+        del lbufs
+        run_l = lambda: ck.compress(spec, q, k, v, n_keep, alpha=alpha, bufs=bufs, lse_in=lse)
+        for _ in range(args.warmup):
+            run_l()
+        ms_l, _ = time_passes(run_l, args.steps, stream, profile=False)
+        _, kern_l = time_passes(run_l, args.steps, stream, profile=True)
+        model_l, _ = algorithmic_model(cfg, n_keep, lse_in=True)
+        roof_l = summarize(kern_l, model_l)
+        bytes_l = sum(b for b, _, _ in model_l.values())
+        lse_line = {"value": tokens / (ms_l / 1e3 / cfg.layers), "unit": "KV tokens/s per layer",
+                    "ms_per_step": ms_l, "pass_alg_bytes": bytes_l,
+                    "pass_alg_GBps": bytes_l / (ms_l / 1e3) / 1e9,
+                    "pass_alg_frac_hbm": bytes_l / (ms_l / 1e3) / 1e9 / HBM_PEAK_GBS,
+                    "roofline": roof_l, "kernels": kern_l,
+                    "note": "caller-supplied row log-sum-exp (from an untimed pass): score pass 1 "
+                            "skipped, K read once"}
+        log(f"pass with caller log-sum-exp: {ms_l:.3f} ms")
 
     cpu = None
     if not args.no_cpu_baseline and args.variant == "default":
@@ -532,12 +613,16 @@ def main():
                    "layers": cfg.layers, "seq_len": tokens, "kv_heads": cfg.kv_heads,
                    "head_dim": cfg.head_dim, "window": cfg.window, "n_keep": n_keep[0],
                    "variant": args.variant},
+        "pass_alg_bytes": pass_bytes,
         "pass_alg_GBps": pass_bytes / (ms / 1e3) / 1e9,
         "pass_alg_frac_hbm": pass_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
         "roofline": roof,
         "kernels": kernels,
+        "ms_per_step_with_kernel_events": ms_prof,
         "cpu_baseline": cpu,
         "allocation": alloc_diag,
+        "lse_in": lse_line,
+        "meta": run_metadata(cfg, dev),
     }
     print(json.dumps(rec), flush=True)
 

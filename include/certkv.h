@@ -345,6 +345,15 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
  * cache).  bf16 caches only (CERTKV_EUNSUPPORTED for fp32); tq * G <= 512.
  * The workspace is certkv_decode_workspace_size(p, tq, max_rows) bytes,
  * 256-byte aligned; a non-finite output sets the status word. */
+size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq,
+                                    int32_t max_rows);
+certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,
+                            int32_t tq, int32_t max_rows, const void* k_packed,
+                            const void* v_packed,
+                            const int64_t* packed_offsets, float* out,
+                            float* lse, void* ws, size_t ws_bytes,
+                            void* stream);
+
 /* Clustered tail summaries (appendix, deterministic output-error bound for
  * clustered tail summaries): per head, the evicted ranks b_h..n-1 in the
  * pass's rank order are cut into m contiguous groups of ceil((n - b_h) / m)
@@ -358,7 +367,9 @@ certkv_status certkv_compress(const certkv_problem* p, certkv_tensor q_win,
  *   kept_vmax [U] fp32 out: the largest norm of a kept value
  * Inputs: k, v as for certkv_score; perm [L][H][T] the rank order of the
  * pass (certkv_allocate or certkv_outputs.perm); budgets [U] (b_h).
- * 1 <= m <= 64, else CERTKV_EINVAL.  Allocates nothing. */
+ * The summaries replace the single slot: the problem must carry
+ * CERTKV_NO_SLOT (else CERTKV_EINVAL), so that the evicted ranks are counted
+ * once.  1 <= m <= 64, else CERTKV_EINVAL.  Allocates nothing. */
 certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k,
                                   certkv_tensor v, const int32_t* perm,
                                   const int32_t* budgets, int32_t m,
@@ -375,8 +386,10 @@ certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k,
  *   lbar_g = scale <q, kbar_g>,  Zhat = sum_S e^l + sum_g n_g e^lbar_g,
  * lse = log Zhat.  bound (optional [L][B*tq][Hq] fp32 out): the runtime
  * certificate with r_g = scale |q| R_g: 3 (D_N + V' D_Z) / Zhat when
- * D_Z <= Zhat / 3, +infinity otherwise.  bf16 only; the workspace is
- * certkv_decode_workspace_size(p, tq, max_rows). */
+ * D_Z <= Zhat / 3, +infinity otherwise.  The segments must hold kept rows
+ * only: a problem without CERTKV_NO_SLOT returns CERTKV_EINVAL (a slot row
+ * would count the evicted mass a second time beside the cluster terms).
+ * bf16 only; the workspace is certkv_decode_workspace_size(p, tq, max_rows). */
 certkv_status certkv_decode_clustered(const certkv_problem* p,
                                       certkv_tensor q_new, int32_t tq,
                                       int32_t max_rows, const void* k_packed,
@@ -390,15 +403,6 @@ certkv_status certkv_decode_clustered(const certkv_problem* p,
                                       const float* kept_vmax, float* out,
                                       float* lse, float* bound, void* ws,
                                       size_t ws_bytes, void* stream);
-
-size_t certkv_decode_workspace_size(const certkv_problem* p, int32_t tq,
-                                    int32_t max_rows);
-certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,
-                            int32_t tq, int32_t max_rows, const void* k_packed,
-                            const void* v_packed,
-                            const int64_t* packed_offsets, float* out,
-                            float* lse, void* ws, size_t ws_bytes,
-                            void* stream);
 
 /* Per-kernel timing.  While enabled, every kernel the library launches is
  * bracketed by two hipEvents on its launch stream; certkv_profile_read

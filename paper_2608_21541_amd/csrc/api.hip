@@ -684,6 +684,10 @@ static certkv_status decode_impl(const certkv_problem* p, certkv_tensor q_new, i
   Plan P;
   TRY(make_plan(p, &P));
   if (tq < 1 || max_rows < 0) return CERTKV_EINVAL;
+  // Cluster terms stand for the evicted ranks; a packed segment that already
+  // ends in the slot row (which carries the whole evicted tail) would count
+  // that mass twice, so the clustered decode needs a no-slot problem.
+  if (cl.m > 0 && P.g.slot) return CERTKV_EINVAL;
   if (P.dtype != CERTKV_BF16) return CERTKV_EUNSUPPORTED;
   if ((int64_t)tq * P.g.G > 512) return CERTKV_EUNSUPPORTED;
   if (!q_new.ptr || ((uintptr_t)q_new.ptr & 15u)) return CERTKV_EINVAL;
@@ -761,6 +765,8 @@ certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k, cert
   TRY(check_tensor(k, P));
   TRY(check_tensor(v, P));
   if (m < 1 || m > 64) return CERTKV_EINVAL;
+  // the summaries replace the single slot: the problem must have none
+  if (P.g.slot) return CERTKV_EINVAL;
   if (!perm || !budgets || !cluster_k || !cluster_v || !cluster_count || !cluster_rk ||
       !cluster_rv || !kept_vmax)
     return CERTKV_EINVAL;

@@ -123,9 +123,11 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 
 // Descending-order radix key of a float: larger value -> smaller key, so an
 // ascending stable sort of keys orders scores descending with ties kept in
-// position order.
+// position order.  -0.0 takes the key of +0.0: the two compare equal, so
+// they tie and keep position order like any other pair of equal scores.
 __device__ __forceinline__ uint32_t desc_key(float f) {
   uint32_t u = __float_as_uint(f);
+  u = (u << 1) ? u : 0u;
   uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
   return ~asc;
 }

@@ -227,19 +227,28 @@ def test_dry_run_decode_validation():
 
 def test_dry_run_cluster_validation():
     L = _lib.lib()
-    p = problem()
+    no_slot = _lib.CERTKV_CAUSAL | _lib.CERTKV_DRY_RUN | _lib.CERTKV_NO_SLOT
+    p = problem(flags=no_slot)
+    p_slot = problem()
     t = tensor()
 
-    def tail(m=8, perm=FAKE, bud=FAKE, out=FAKE):
-        return L.certkv_cluster_tail(ctypes.byref(p), t, t, perm, bud, m, out, out, out, out, out,
-                                     out, None)
+    def tail(m=8, perm=FAKE, bud=FAKE, out=FAKE, pp=p):
+        return L.certkv_cluster_tail(ctypes.byref(pp), t, t, perm, bud, m, out, out, out, out,
+                                     out, out, None)
     assert tail() == _lib.CERTKV_OK
     assert tail(m=0) == _lib.CERTKV_EINVAL and tail(m=65) == _lib.CERTKV_EINVAL
     assert tail(perm=None) == _lib.CERTKV_EINVAL and tail(out=None) == _lib.CERTKV_EINVAL
+    # the summaries replace the slot: a problem with the slot is rejected
+    assert tail(pp=p_slot) == _lib.CERTKV_EINVAL
     n = L.certkv_decode_workspace_size(ctypes.byref(p), 8, 0)
 
-    def dec(m=8, cl=FAKE):
-        return L.certkv_decode_clustered(ctypes.byref(p), tensor(), 8, 0, FAKE, FAKE, FAKE, m, cl,
-                                         cl, cl, cl, cl, cl, FAKE, None, None, FAKE, n, None)
+    def dec(m=8, cl=FAKE, pp=p):
+        return L.certkv_decode_clustered(ctypes.byref(pp), tensor(), 8, 0, FAKE, FAKE, FAKE, m,
+                                         cl, cl, cl, cl, cl, cl, FAKE, None, None, FAKE, n, None)
     assert dec() == _lib.CERTKV_OK
     assert dec(m=0) == _lib.CERTKV_EINVAL and dec(cl=None) == _lib.CERTKV_EINVAL
+    # segments that end in a slot row would count the evicted mass twice
+    assert dec(pp=p_slot) == _lib.CERTKV_EINVAL
+    # the plain decode takes either kind of segment
+    assert L.certkv_decode(ctypes.byref(p_slot), tensor(), 8, 0, FAKE, FAKE, FAKE, FAKE, None,
+                           FAKE, n, None) == _lib.CERTKV_OK

@@ -115,7 +115,11 @@ def test_clustered_decode_and_certificate_match_oracle(tq):
                 assert abs(bg - c["bound"]) <= 1e-3 * c["bound"] + 1e-6, (bg, c)
             elif not math.isfinite(c["bound"]) and c["dz"] > 0.34:
                 assert math.isinf(bg)
-    log(f"clustered decode tq={tq}: finite certificates {finite}")
+    # Rank-contiguous groups of random keys have wide radii, so the condition
+    # D_Z <= Zhat / 3 rarely holds here and the infinite branch is what this
+    # case checks; the finite branch is checked on every row of the planted
+    # case below.
+    log(f"clustered decode tq={tq}: finite certificates {finite} of {H * tq * G} rows")
 
 
 def test_singleton_clusters_decode_equals_full_attention():

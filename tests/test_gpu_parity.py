@@ -66,6 +66,91 @@ def test_c4_ragged_batch_two_layers():
             check_block_stages(spec, cfg, cache, out, li, b, check_scores=(li == 1), log=log)
 
 
+def test_c4_stated_config_all_blocks():
+    # the ragged batch exactly as stated: 8 single-layer caches of
+    # U{8192..65536} tokens, window 32, 5 % budget plus the slot; pass-1 and
+    # pass-2 key blocks grow with the longest sequence as in the benchmark
+    import concurrent.futures
+    cfg = synth.config("C4")
+    assert cfg.batch == 8 and cfg.layers == 1 and cfg.window == 32
+    cache = synth.make_cache(cfg, "cpu")
+    log(f"C4 lengths {cfg.seqlens}, n_keep {cache['n_keep']}")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    with concurrent.futures.ThreadPoolExecutor(2) as ex:
+        res = list(ex.map(lambda b: check_block_stages(spec, cfg, cache, out, 0, b,
+                                                       log=lambda m: None),
+                          range(cfg.batch)))
+    for b, r in enumerate(res):
+        log(f"  sequence {b} ({cfg.seqlens[b]} tokens): {r}")
+
+
+def test_caller_scores_signed_zeros_negatives_and_empty_heads():
+    # Caller scores through certkv_allocate and certkv_select (the appendix's
+    # clip-and-normalize guard: a = (s)+ / sum (s)+, uniform when the sum is
+    # zero).  -0.0 and +0.0 are equal scores: they tie and keep position
+    # order, as the oracle's comparison does.
+    cfg = synth.config("C2", seqlens=[3001])
+    cache = synth.make_cache(cfg, "cpu")
+    H, n, D = cfg.kv_heads, 3001, cfg.head_dim
+    rng = np.random.default_rng(5)
+    s = rng.random((H, n)).astype(np.float32)
+    s[0, 0::3] = 0.0                          # +0 / -0 ties among positives
+    s[0, 1::3] = -0.0
+    s[1, ::2] = -rng.random(len(s[1, ::2])).astype(np.float32)   # negatives
+    s[1, 5::7] = -0.0
+    s[2] = 0.0                                # all zero, both signs: uniform a
+    s[2, ::2] = -0.0
+    s[3] = -rng.random(n).astype(np.float32)  # all negative: uniform a
+    s[4] = np.round(s[4] * 4) / 4             # many exact ties
+    s[4, ::5] = -0.0
+    s[5, :] = 0.25                            # flat row
+    s[5, 100:200] = -0.0
+    assert np.signbit(s[0, 1]) and not np.signbit(s[0, 0])
+    spec = spec_of(cfg)
+    dev = torch.device("cuda:0")
+    st = torch.from_numpy(s).reshape(1, H, n).to(dev)
+    k, v = cache["k"].to(dev), cache["v"].to(dev)
+    n_keep = cache["n_keep"]
+    al = ck.allocate(spec, st, v, n_keep, with_perm=True, with_curves=True)
+    torch.cuda.synchronize()
+    perm = al["perm"].cpu().numpy()[0]
+    c_gpu = al["curves"].cpu().numpy()[0]
+    bud = al["budgets"].cpu().numpy()
+    vh = cache["v"][0].double().numpy()
+    kh = cache["k"][0].double().numpy()
+    for h in range(H):
+        assert np.array_equal(perm[h], oracle.order(s[h])), f"order of head {h}"
+        _, c32 = oracle.curves(s[h], perm[h], vh[:, h])
+        tol = 4.0 * np.spacing(np.abs(c32)).astype(np.float64) + 1e-6 * float(c32.max())
+        assert (np.abs(c_gpu[h].astype(np.float64) - c32) <= tol).all(), f"curves of head {h}"
+    want, _ = oracle.allocate(c_gpu, n_keep[0])
+    assert np.array_equal(bud, want)
+    kb, ko, ki = ck.select(spec, st, al["budgets"])
+    ks, vs, m = ck.tail_summary(spec, st, k, v, ko, ki)
+    torch.cuda.synchronize()
+    ko, ki = ko.cpu().numpy(), ki.cpu().numpy()
+    for h in range(H):
+        kept = ki[ko[h]:ko[h + 1]]
+        assert np.array_equal(kept, oracle.select(perm[h], bud[h])), f"kept set of head {h}"
+        rk, rv, rm = oracle.tail(s[h], kept, kh[:, h], vh[:, h])
+        assert abs(m[h].item() - rm) <= 1e-9 * max(rm, 1e-30) + 1e-15, (h, m[h].item(), rm)
+        for got, ref, x in ((ks[h], rk, kh[:, h]), (vs[h], rv, vh[:, h])):
+            a = oracle.normalize(s[h])
+            mask = np.ones(n, bool)
+            mask[kept] = False
+            scale_e = float((a[mask] * np.linalg.norm(x[mask], axis=1)).sum()) / max(rm, 1e-300)
+            err = np.linalg.norm(got.cpu().numpy() - ref) / max(np.linalg.norm(ref), scale_e)
+            assert err <= 2e-3, (h, err)
+    for retain in (0.5, 0.9):
+        kb, ko, ki = ck.select(spec, st, mode="coverage", retain_mass=retain)
+        torch.cuda.synchronize()
+        ko, ki = ko.cpu().numpy(), ki.cpu().numpy()
+        for h in range(H):
+            k_eta = oracle.coverage(s[h], perm[h], retain)
+            assert kb[h].item() == k_eta, (retain, h, kb[h].item(), k_eta)
+            assert np.array_equal(ki[ko[h]:ko[h + 1]], oracle.select(perm[h], k_eta))
+
+
 def test_keep_all_and_minimal_budgets():
     # n_keep = n: every head keeps n-1 tokens and the slot is the last-ranked
     # key; n_keep = 2: B_real = H, every head keeps exactly b_min = 1.
@@ -177,46 +262,6 @@ def test_allocate_from_supplied_curves_matches_oracle():
             got = ck.allocate_curves(spec, t, [n_keep]).cpu().numpy()
             want, _ = oracle.allocate(c32, n_keep)
             assert np.array_equal(got, want), (n_keep, got, want)
-
-
-# --------------------------------------------------------------------------
-# Full-size workloads in the launch configuration the benchmark times:
-# sampled blocks against the oracle, invariants everywhere.
-
-def _global_invariants(spec, cfg, cache, out):
-    L, H = spec.layers, cfg.kv_heads
-    w, G = cfg.window, cfg.group
-    s = out["scores"].to(torch.float64)
-    cu = cache["cu_seqlens"]
-    for b in range(cfg.batch):
-        tot = s[:, :, cu[b]:cu[b + 1]].sum(-1)
-        assert torch.all((tot - w * G).abs() <= 1e-3 * w * G)
-    bud = out["budgets"].numpy().reshape(L, cfg.batch, H)
-    for b in range(cfg.batch):
-        br, bm = oracle.budget_params(H, cu[b + 1] - cu[b], cache["n_keep"][b])
-        assert (bud[:, b].sum(-1) == br).all() and bud[:, b].min() >= bm
-    po = out["packed_offsets"].numpy()
-    ko = out["kept_offsets"].numpy()
-    assert (po - ko == np.arange(len(po))).all()
-    assert (np.diff(ko) == out["budgets"].numpy()).all()
-    assert (out["tail_mass"].numpy() > 0).all()
-
-
-@pytest.mark.parametrize("name", ["C3", "C5"])
-def test_full_size_sampled(name):
-    cfg = synth.config(name)
-    log(f"{name}: generating {cfg.layers} layers on the GPU")
-    cache = synth.make_cache(cfg, "cuda:0")
-    spec = spec_of(cfg)
-    bufs = ck.compress(spec, cache["q_win"], cache["k"], cache["v"], cache["n_keep"],
-                       with_curves=True, with_perm=True)
-    torch.cuda.synchronize()
-    out = {k: (t.cpu() if t is not None else None) for k, t in bufs.as_dict().items()}
-    del bufs
-    _global_invariants(spec, cfg, cache, out)
-    log(f"{name}: invariants hold; oracle on sampled layers")
-    for li in [0, cfg.layers - 1]:
-        check_block_stages(spec, cfg, cache, out, li, 0, check_scores=(li == 0), log=log)
 
 
 # --------------------------------------------------------------------------
