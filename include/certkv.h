@@ -230,6 +230,23 @@ certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win,
                            double* ksum, float* lse_out, void* ws,
                            size_t ws_bytes, void* stream);
 
+/* certkv_score without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that forbid
+ * allocation).  Same arguments, kernels and results as certkv_score; the
+ * scoring partials live in a fixed device array of
+ * certkv_score_noalloc_max_bytes() bytes (64 MiB) that each device holds
+ * from its first call until the process ends.  A problem whose scoring
+ * workspace (certkv_workspace_size(p, CERTKV_STAGE_SCORE)) exceeds that
+ * returns CERTKV_EWORKSPACE before any launch.  Nothing in the array needs
+ * to start at zero, and no call allocates or frees memory; every call on one
+ * device shares the array, so calls that overlap on one device (on different
+ * streams, or from several threads) race: the caller serializes them. */
+size_t certkv_score_noalloc_max_bytes(void);
+certkv_status certkv_score_noalloc(const certkv_problem* p,
+                                   certkv_tensor q_win, certkv_tensor k,
+                                   const float* lse_in, float* scores,
+                                   double* ksum, float* lse_out, void* stream);
+
 /* Dispersion curves and budget allocation (paper Section 4.1, Eq.
  * certkv-curve; appendix Algorithm 1, the sort, suffix-scan, bisection and
  * repair steps).

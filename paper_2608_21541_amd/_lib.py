@@ -45,6 +45,7 @@ EXPORTS = [
     "certkv_compress", "certkv_decode_workspace_size", "certkv_decode", "certkv_cluster_tail",
     "certkv_decode_clustered", "certkv_profile_enable",
     "certkv_profile_read", "certkv_profile_reset",
+    "certkv_score_noalloc", "certkv_score_noalloc_max_bytes",
 ]
 
 
@@ -108,6 +109,9 @@ def lib():
     L.certkv_workspace_size.argtypes = [P, i32]
     L.certkv_workspace_size.restype = sz
     L.certkv_score.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp, sz, vp]
+    L.certkv_score_noalloc.argtypes = [P, Tensor, Tensor, vp, vp, vp, vp, vp]
+    L.certkv_score_noalloc_max_bytes.argtypes = []
+    L.certkv_score_noalloc_max_bytes.restype = sz
     L.certkv_allocate.argtypes = [P, vp, Tensor, vp, dbl, i32, vp, vp, vp, vp, vp, sz, vp]
     L.certkv_allocate_curves.argtypes = [P, vp, vp, dbl, i32, vp, vp, sz, vp]
     L.certkv_select.argtypes = [P, vp, vp, i32, dbl, vp, vp, i64, vp, vp, sz, vp]
@@ -129,7 +133,7 @@ def lib():
     for name in EXPORTS:
         if name not in ("certkv_status_string", "certkv_workspace_size",
                         "certkv_decode_workspace_size", "certkv_profile_read",
-                        "certkv_profile_reset"):
+                        "certkv_profile_reset", "certkv_score_noalloc_max_bytes"):
             getattr(L, name).restype = i32
     _LIB = L
     return L

@@ -141,6 +141,27 @@ def score(spec: ProblemSpec, q_win, k, with_ksum=False, lse_in=None, with_lse=Fa
     return out[0] if len(out) == 1 else tuple(out)
 
 
+def score_noalloc(spec: ProblemSpec, q_win, k, scores, ksum=None, lse_out=None, lse_in=None):
+    """certkv_score with the library's fixed device workspace: the caller
+    passes every output (scores [L][H][T] fp32; optional ksum [U][d] fp64 and
+    lse_out [L][B*w][Hq] fp32) and nothing is allocated."""
+    L = _lib.lib()
+    dev = k.device
+    assert scores.dtype == torch.float32 and scores.is_contiguous()
+    assert tuple(scores.shape) == (spec.layers, spec.kv_heads, spec.total_tokens)
+    if ksum is not None:
+        assert ksum.dtype == torch.float64 and tuple(ksum.shape) == (spec.units, spec.head_dim)
+    for t in (lse_in, lse_out):
+        if t is not None:
+            assert t.dtype == torch.float32 and t.is_contiguous()
+            assert tuple(t.shape) == _lse_shape(spec)
+    p = spec.c_problem()
+    _check(L.certkv_score_noalloc(ctypes.byref(p), _tensor(q_win), _tensor(k), _ptr(lse_in),
+                                  _ptr(scores), _ptr(ksum), _ptr(lse_out), _stream(dev)),
+           "certkv_score_noalloc")
+    return scores
+
+
 def allocate(spec: ProblemSpec, scores, v, n_keep, alpha=0.2, steps=40, with_perm=False,
              with_curves=False, with_vsum=False):
     """Budgets [U] int32 (+ perm, curves [L][H][T], vsum [U][d])."""

@@ -543,6 +543,57 @@ certkv_status certkv_score(const certkv_problem* p, certkv_tensor q_win, certkv_
   return do_score(P, q_win, k, lse_in, scores, ksum, lse_out, w, (hipStream_t)stream);
 }
 
+}  // extern "C"
+
+// ---- scoring without a caller workspace ---------------------------------------
+// The workspace of certkv_score_noalloc: a fixed device array (every device
+// the library runs on holds its own copy until the process ends).  Host code
+// never uses the symbol itself as an address: the device address is looked
+// up once per device with hipGetSymbolAddress, with that device current.
+namespace certkv {
+namespace {
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+static certkv_status scratch_base(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CERTKV_EHIP;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return CERTKV_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CERTKV_OK;
+}
+}  // namespace certkv
+
+extern "C" {
+
+size_t certkv_score_noalloc_max_bytes(void) { return kScratchBytes; }
+
+certkv_status certkv_score_noalloc(const certkv_problem* p, certkv_tensor q_win,
+                                   certkv_tensor k, const float* lse_in, float* scores,
+                                   double* ksum, float* lse_out, void* stream) {
+  Plan P;
+  TRY(make_plan(p, &P));
+  TRY(check_tensor(q_win, P));
+  TRY(check_tensor(k, P));
+  if (!scores) return CERTKV_EINVAL;
+  Bufs w;
+  const size_t need = layout(P, stage_needs(CERTKV_STAGE_SCORE), nullptr, &w);
+  if (need > kScratchBytes) return CERTKV_EWORKSPACE;
+  if (p->flags & CERTKV_DRY_RUN) return CERTKV_OK;
+  void* ws = nullptr;
+  TRY(scratch_base(&ws));
+  TRY(check_ws(P, stage_needs(CERTKV_STAGE_SCORE), ws, kScratchBytes, &w));
+  return do_score(P, q_win, k, lse_in, scores, ksum, lse_out, w, (hipStream_t)stream);
+}
+
 certkv_status certkv_allocate(const certkv_problem* p, const float* scores, certkv_tensor v,
                               const int32_t* n_keep_host, double alpha, int32_t steps,
                               int32_t* budgets, int32_t* perm, float* curves, double* vsum,
