@@ -528,6 +528,278 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu((
 }
 
 // ---------------------------------------------------------------------------
+// Pass 2 for windows of at most 256 rows: sixteen waves per workgroup (four
+// per SIMD at one workgroup per CU) share one copy of the staged queries.
+// The layout is score_pass2_kernel's (query tile = A, key tile = B, one key
+// per lane), with two changes that free the registers a fourth wave needs:
+//  * the row log2-sums enter as the accumulators' starting value, -lse2 / c2,
+//    so the exponent of a weight is one multiply of the MFMA result;
+//  * the weighted key sums run on the matrix core.  After a tile's scores are
+//    known, each wave stages its key tile in LDS 64 dims at a time and adds
+//    s^T K with v_mfma_f32_4x4x4bf16_1k: block b of the instruction covers
+//    dims 4b..4b+3 of the stage and 4 keys, the rows of A are the scores
+//    split into three bf16 parts (hi + lo + lo2 = s exactly) and a zero row,
+//    and the B fragments (4 keys x 4 dims per block) come from transposing
+//    LDS reads (ds_read_b64_tr_b16: in each 16-lane group, lane i receives
+//    element i % 4 of the 8-byte rows addressed by lanes 4j + i / 4).
+// Per lane the key sums then take two 4-register accumulators instead of
+// half a key row of fp32 sums.
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+constexpr int kP2Threads = 1024;
+constexpr int kP2Waves = kP2Threads / 64;
+constexpr int kStageRow = 160;  // bytes per staged key row: 64 dims + 32 B (an 8-bank shift)
+
+template <int D, int NQT>
+struct P2Smem {
+  static constexpr int Mp = NQT * 32;
+  static constexpr size_t lse = (size_t)Mp * ScoreSmem<D>::kRowElems * 2;  // [Mp] -lse2 / c2
+  static constexpr size_t lim = lse + (size_t)Mp * 4;                      // [Mp] causal limits
+  static constexpr size_t stage = lim + (size_t)Mp * 4;                    // [waves][32 keys][kStageRow]
+  static constexpr size_t sparts = stage + (size_t)kP2Waves * 32 * kStageRow;  // [waves][4][32] bf16
+  static constexpr size_t total = sparts + (size_t)kP2Waves * 4 * 32 * 2;
+};
+
+__device__ __forceinline__ s16x4_t lds_tr_b16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4_t*)(__attribute__((address_space(3))) unsigned char*)p);
+}
+
+template <int D, int NQT, bool KSUM>
+__global__ __launch_bounds__(kP2Threads) __attribute__((amdgpu_waves_per_eu(4, 8))) void score_pass2_w16_kernel(
+    Geo g, SeqTab st, const uint16_t* __restrict__ qw, int64_t q_sl, int64_t q_st,
+    int64_t q_sh, const uint16_t* __restrict__ kc, int64_t k_sl, int64_t k_st,
+    int64_t k_sh, int32_t keys_per_block, int32_t nkb_max, const float* __restrict__ lse2,
+    float* __restrict__ scores, float* __restrict__ kpart) {
+  using SM = P2Smem<D, NQT>;
+  constexpr int KS = D / 16;   // MFMA k-steps
+  constexpr int HD = D / 2;    // dims per lane half
+  constexpr int RE = ScoreSmem<D>::kRowElems;
+  constexpr int NSTG = D / 64; // key-sum stages of 64 dims
+  static_assert(NQT <= 8, "sixteen-wave pass 2 holds at most 256 window rows");
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  uint16_t* q_lds = reinterpret_cast<uint16_t*>(smem_raw);
+  float* nl_lds = reinterpret_cast<float*>(smem_raw + SM::lse);
+  int* lim_lds = reinterpret_cast<int*>(smem_raw + SM::lim);
+  float* red_lds = reinterpret_cast<float*>(smem_raw);
+
+  const int kb = blockIdx.x;
+  const int h = blockIdx.y % g.H;
+  const int bl = blockIdx.y / g.H;
+  const int l = blockIdx.z;
+  if (bl >= st.count) return;
+  const int b = st.first + bl;
+  const int n = st.len[bl];
+  const int64_t tok0 = st.start[bl];
+  const int key_begin = kb * keys_per_block;
+  if (key_begin >= n) return;
+  const int key_end = min(n, key_begin + keys_per_block);
+  const int M = g.w * g.G;
+  const int Mp = NQT * 32;
+  const int64_t u = unit_index(g, l, b, h);
+  const float c2 = g.scale * kLog2e;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int hh = lane >> 5;
+  const int c32 = lane & 31;
+  unsigned char* stage = smem_raw + SM::stage + (size_t)wave * 32 * kStageRow;
+  uint16_t* sparts = reinterpret_cast<uint16_t*>(smem_raw + SM::sparts) + wave * 4 * 32;
+
+  // Stage the window queries (row rho = q*G + gq, zero padding rows), the
+  // accumulator starting values -lse2 / c2 (-infinity for padding rows,
+  // whose weights are then zero) and the causal limits; zero the fourth row
+  // of every wave's score parts.
+  {
+    const int chunks = D / 8;
+    for (int c = threadIdx.x; c < Mp * chunks; c += kP2Threads) {
+      int rho = c / chunks, part8 = c % chunks;
+      uint4 val = make_uint4(0u, 0u, 0u, 0u);
+      if (rho < M) {
+        int qq = rho / g.G, gq = rho % g.G;
+        const uint16_t* src = qw + (int64_t)l * q_sl + (int64_t)(b * g.w + qq) * q_st +
+                              (int64_t)(h * g.G + gq) * q_sh + part8 * 8;
+        val = *reinterpret_cast<const uint4*>(src);
+      }
+      *reinterpret_cast<uint4*>(q_lds + rho * RE + part8 * 8) = val;
+    }
+    for (int i = threadIdx.x; i < Mp; i += kP2Threads) {
+      int lim = -1;
+      if (i < M) lim = g.causal ? min(n - g.w + i / g.G, n - 1) : n - 1;
+      lim_lds[i] = lim;
+      nl_lds[i] = i < M ? -lse2[u * M + i] / c2 : -INFINITY;
+    }
+    if (KSUM && lane < 32) sparts[3 * 32 + lane] = 0;
+  }
+  __syncthreads();
+
+  const int first_masked = g.causal ? (n - g.w + 1) : n;  // keys >= this may be masked
+  const uint16_t* kbase = kc + (int64_t)l * k_sl + tok0 * k_st + (int64_t)h * k_sh;
+  constexpr int KPW = 32;                    // keys per wave iteration
+  constexpr int KPI = KPW * kP2Waves;        // keys per workgroup iteration
+  f32x4_t kacc[NSTG];
+#pragma unroll
+  for (int i = 0; i < NSTG; ++i) kacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // transposing-read address of this lane in a stage: key row 4t + (lane % 16) / 4,
+  // 8-byte column chunk 4 (lane / 16) + lane % 4
+  const int tr_row = (lane & 15) >> 2;
+  const int tr_col = 8 * (4 * (lane >> 4) + (lane & 3));
+
+  for (int it = key_begin + wave * KPW; it < key_end; it += KPI) {
+    Frag kf[KS];
+    {
+      const int key = it + c32;
+      const int keyc = key < n ? key : n - 1;
+      const uint4* src = reinterpret_cast<const uint4*>(kbase + (int64_t)keyc * k_st + hh * HD);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kf[s].u = src[s];
+    }
+    const bool need_mask = it + KPW - 1 >= first_masked;
+    float sp[16 / KS];
+#pragma unroll
+    for (int j = 0; j < 16 / KS; ++j) sp[j] = 0.f;
+
+    auto tiles = [&](auto masked_tag) {
+      constexpr bool MASKED = decltype(masked_tag)::value;
+      constexpr int SL = 16 / KS;
+      const int key = it + c32;
+      // accumulator starting values of query tile qt: rows qt*32 + 4*hh +
+      // 8*(v/4) + v%4 of -lse2 / c2
+      auto init_acc = [&](int qt, f32x16_t& a) {
+        const int rb = qt * 32 + 4 * hh;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 x = *reinterpret_cast<const float4*>(nl_lds + rb + 8 * i);
+          a[4 * i] = x.x;
+          a[4 * i + 1] = x.y;
+          a[4 * i + 2] = x.z;
+          a[4 * i + 3] = x.w;
+        }
+      };
+      f32x16_t acc;
+      init_acc(0, acc);
+      {
+        const uint16_t* qrow = q_lds + c32 * RE + hh * HD;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          Frag qf;
+          qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.v, kf[s].v, acc, 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int qt = 0; qt < NQT; ++qt) {
+        const bool more = qt + 1 < NQT;
+        const int rb = qt * 32 + 4 * hh;
+        int4 lim[4];
+        if (MASKED) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) lim[i] = *reinterpret_cast<const int4*>(lim_lds + rb + 8 * i);
+        }
+        f32x16_t nacc;
+        if (more) init_acc(qt + 1, nacc);
+        const uint16_t* qrow = q_lds + ((qt + 1) * 32 + c32) * RE + hh * HD;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          if (more) {
+            Frag qf;
+            qf.u = *reinterpret_cast<const uint4*>(qrow + s * 8);
+            nacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf.v, kf[s].v, nacc, 0, 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < SL; ++j) {
+            const int v = s * SL + j;
+            float x = acc[v] * c2;
+            if (MASKED) {
+              const int4 mv = lim[v >> 2];
+              const int limv = (v & 3) == 0 ? mv.x : (v & 3) == 1 ? mv.y : (v & 3) == 2 ? mv.z : mv.w;
+              if (key > limv) x = -INFINITY;
+            }
+            sp[j] += __builtin_amdgcn_exp2f(x);
+          }
+        }
+        if (more) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 + 4 + (MASKED ? 4 : 0), 0);
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x402, (MASKED ? 5 : 3) * SL, 0);
+            if (s + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+        }
+        acc = nacc;
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    if (need_mask)
+      tiles(std::integral_constant<bool, true>());
+    else
+      tiles(std::integral_constant<bool, false>());
+
+    float sp_all = sp[0];
+#pragma unroll
+    for (int j = 1; j < 16 / KS; ++j) sp_all += sp[j];
+    const float s_key = sp_all + __shfl_xor(sp_all, 32, 64);
+    const int key = it + c32;
+    if (hh == 0 && key < n) scores[lht_base(g, l, h, tok0) + key] = s_key;
+    if constexpr (KSUM) {
+      // s = hi + lo + lo2 exactly (three bf16 parts of the fp32 value)
+      const float s_t = (key < n && s_key > 0.f) ? s_key : 0.f;
+      const uint16_t p0 = f32_to_bf16_rne(s_t);
+      const float r1 = s_t - bf16_to_f32(p0);
+      const uint16_t p1 = f32_to_bf16_rne(r1);
+      const float r2 = r1 - bf16_to_f32(p1);
+      const uint16_t p2 = f32_to_bf16_rne(r2);
+      if (hh == 0) {
+        sparts[c32] = p0;
+        sparts[32 + c32] = p1;
+        sparts[64 + c32] = p2;
+      }
+#pragma unroll
+      for (int sg = 0; sg < NSTG; ++sg) {
+        // stage 64 dims of the 32 keys: for d = 128 the lane half hh == sg
+        // holds them (dims 64 sg ..), for d = 64 both halves write theirs
+        if (NSTG == 1 || hh == sg) {
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+            *reinterpret_cast<uint4*>(stage + c32 * kStageRow + (NSTG == 1 ? hh * 64 : 0) + 16 * s) =
+                kf[s].u;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const s16x4_t a = *reinterpret_cast<const s16x4_t*>(sparts + (lane & 3) * 32 + 4 * t);
+          const s16x4_t bfr = lds_tr_b16(stage + (4 * t + tr_row) * kStageRow + tr_col);
+          kacc[sg] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a, bfr, kacc[sg], 0, 0, 0);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    }
+  }
+
+  if constexpr (KSUM) {
+    __syncthreads();  // every wave is done with the staged queries
+    // lane L holds dim 64 sg + L of stage sg: the sum of its three part rows
+#pragma unroll
+    for (int sg = 0; sg < NSTG; ++sg)
+      red_lds[wave * D + 64 * sg + lane] = kacc[sg][0] + kacc[sg][1] + kacc[sg][2];
+    __syncthreads();
+    for (int dd = threadIdx.x; dd < D; dd += kP2Threads) {
+      float s = 0.f;
+      for (int wv = 0; wv < kP2Waves; ++wv) s += red_lds[wv * D + dd];
+      kpart[(u * nkb_max + kb) * D + dd] = s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Per-row log2-sum-exp from the pass-1 partials.
 // Sum format (shift-free partial sums): writes lse2 and flags the unit when a
 // row's total leaves [2^-60, 2^120].  Max format ((max, sum) partials):
@@ -741,6 +1013,12 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     hipFuncSetAttribute((const void*)score_pass2_kernel<D, NQT, false>,
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if constexpr (NQT <= 8) {
+      hipFuncSetAttribute((const void*)score_pass2_w16_kernel<D, NQT, true>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      hipFuncSetAttribute((const void*)score_pass2_w16_kernel<D, NQT, false>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    }
     attr_set = true;
   }
   const uint16_t* q = static_cast<const uint16_t*>(a.q.ptr);
@@ -764,16 +1042,31 @@ static certkv_status launch_mfma(const ScoreArgs& a, const SeqTab& st, int max_l
                   dim3(256), 0, s, g, st, a.keys_per_block, a.nkb_max, (const float2*)a.part, a.lse2,
                   a.flag, 1);
   }
-  if (a.ksum)
-    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid2,
-                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
-                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
-                  (const float*)a.lse2, a.scores, a.kpart);
-  else
-    CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, false>), grid2,
-                  dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
-                  a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
-                  (const float*)a.lse2, a.scores, (float*)nullptr);
+  if constexpr (NQT <= 8) {
+    // windows of at most 256 rows: sixteen waves share the staged queries
+    const size_t smem2 = P2Smem<D, NQT>::total;
+    if (a.ksum)
+      CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_w16_kernel<D, NQT, true>), grid2,
+                    dim3(kP2Threads), smem2, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                    a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                    (const float*)a.lse2, a.scores, a.kpart);
+    else
+      CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_w16_kernel<D, NQT, false>), grid2,
+                    dim3(kP2Threads), smem2, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                    a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                    (const float*)a.lse2, a.scores, (float*)nullptr);
+  } else {
+    if (a.ksum)
+      CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, true>), grid2,
+                    dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                    a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                    (const float*)a.lse2, a.scores, a.kpart);
+    else
+      CERTKV_LAUNCH("score_pass2_mfma", (score_pass2_kernel<D, NQT, false>), grid2,
+                    dim3(kScoreThreads), smem, s, g, st, q, a.q.s_layer, a.q.s_token, a.q.s_head, k,
+                    a.k.s_layer, a.k.s_token, a.k.s_head, a.keys_per_block2, a.nkb2_max,
+                    (const float*)a.lse2, a.scores, (float*)nullptr);
+  }
   if (a.ksum)
     CERTKV_LAUNCH("score_ksum_reduce", ksum_reduce_kernel, dim3(g.H * st.count, g.L), dim3(128), 0,
                   s, g, st, a.keys_per_block2, a.nkb2_max, (const float*)a.kpart, a.ksum);
