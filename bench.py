@@ -287,6 +287,52 @@ def summarize_traffic(fetch_csv, write_csv, kernel_regex, kernel, workload, out,
         fh.write("\n".join(lines) + "\n")
 
 
+def summarize_counters(csvs, kernel_regex, out, commands):
+    """Markdown summary of SQ issue counters (rocprofv3 --pmc runs) of the
+    kernels matching kernel_regex: per counter the mean over dispatches of the
+    value summed over the device, and the derived busy fractions."""
+    import re
+    import statistics
+    per = {}
+    for path in csvs:
+        for r in _read_csv(path):
+            name = r["Kernel_Name"]
+            if not re.search(kernel_regex, name):
+                continue
+            short = re.sub(r"^void ", "", name).split("(")[0]
+            d = per.setdefault(short, {}).setdefault(r["Counter_Name"], {})
+            d[r["Dispatch_Id"]] = d.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    lines = ["# SQ issue counters (%s)" % kernel_regex, "",
+             "Per counter: the mean over dispatches of the device-wide sum.  Busy",
+             "fractions are per SIMD: MFMA-busy and VALU-active cycles over the",
+             "wave-resident cycles of one SIMD (SQ_BUSY_CYCLES counts per shader",
+             "engine, 32 of them; SQ_VALU_MFMA_BUSY_CYCLES per SIMD, 1024; SQ_ACTIVE_INST_*",
+             "and SQ_WAVE_CYCLES per wave in units of 4 cycles).", "",
+             "Commands:", "", "```"] + commands + ["```", ""]
+    for k, cs in per.items():
+        m = {c: statistics.mean(v.values()) for c, v in cs.items()}
+        lines += ["## " + k, "", "| counter | value |", "|---|---:|"]
+        lines += ["| %s | %.4g |" % (c, v) for c, v in sorted(m.items())]
+        if "SQ_BUSY_CYCLES" in m and "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+            span = m["SQ_BUSY_CYCLES"] / 32.0           # cycles of one shader engine
+            mfma = m["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024.0
+            lines += ["", "| derived (per SIMD) | value |", "|---|---:|",
+                      "| busy span, cycles | %.4g |" % span,
+                      "| MFMA busy, cycles | %.4g (%.0f %%) |" % (mfma, 100 * mfma / span)]
+            if "SQ_ACTIVE_INST_VALU" in m:
+                valu = 4.0 * m["SQ_ACTIVE_INST_VALU"] / 1024.0
+                lines.append("| VALU active, cycles | %.4g (%.0f %%) |" % (valu, 100 * valu / span))
+            if "SQ_VALU_MFMA_COEXEC_CYCLES" in m:
+                co = m["SQ_VALU_MFMA_COEXEC_CYCLES"] / 1024.0
+                lines.append("| MFMA and VALU together, cycles | %.4g |" % co)
+            if "SQ_WAIT_ANY" in m and "SQ_WAVE_CYCLES" in m:
+                lines.append("| waves waiting, share of wave cycles | %.0f %% |"
+                             % (100 * m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"]))
+        lines.append("")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
 def lift_diagnostic(cfg, cache, bufs, qn, out, tq, layers):
     """The future-query lift theorem's a-posteriori bound on a sample of the
     decode: for each sampled (layer, head) and new query row, the exact output
@@ -475,12 +521,19 @@ def main():
                     help="run a 1 GiB device copy first (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("CSV", "OUT", "COMMAND"),
                     help="write a markdown summary of a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--summarize-counters", nargs=6,
+                    metavar=("CSV_A", "CSV_B", "REGEX", "OUT", "CMD1", "CMD2"),
+                    help="write a markdown summary of SQ issue counters from two pmc runs")
     ap.add_argument("--summarize-traffic", nargs=7,
                     metavar=("FETCH_CSV", "WRITE_CSV", "REGEX", "KERNEL", "OUT", "CMD1", "CMD2"),
                     help="write the HBM traffic record of one kernel from two pmc runs")
     args = ap.parse_args()
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_counters:
+        a, b, rx, out, c1, c2 = args.summarize_counters
+        summarize_counters([a, b], rx, out, [c1, c2])
         return
     if args.summarize_traffic:
         fc, wc, rx, kn, out, c1, c2 = args.summarize_traffic
