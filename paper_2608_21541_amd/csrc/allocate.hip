@@ -35,6 +35,19 @@ constexpr int kCandCap = 1024;    // candidate blocks evaluated per round
 constexpr int kBlk = 256;          // ranks per pruning block
 constexpr int kLdsItems = 8192;    // H * blocks handled from LDS
 constexpr int kRepairWin = 64;     // cached curve values per head (fallback repair)
+// Bisection across several workgroups per (layer, sequence): up to kTreeLev
+// levels per pass, one workgroup per node of the level tree.
+constexpr int kTreeLev = 3;
+constexpr int kTreeMax = (1 << kTreeLev) - 1;
+constexpr int kSyncGroups = 256;   // (layer, sequence) groups of one such launch at most
+// sync words: ticket, pad, one arrival counter per group, then per group and
+// pass parity the nodes' budget sums (int64) and argmin vectors (64 heads)
+constexpr size_t kSyncCnt = 2 + kSyncGroups;
+constexpr size_t kSyncSum = kSyncCnt;
+constexpr size_t kSyncArg = kSyncSum + (size_t)kSyncGroups * 2 * kTreeMax * 2;
+constexpr size_t kSyncWords = kSyncArg + (size_t)kSyncGroups * 2 * kTreeMax * 64;
+
+size_t alloc_sync_words() { return kSyncWords; }
 
 // Lanes below this one among those set in `mask`.
 __device__ __forceinline__ uint32_t count_below64(uint64_t mask) {
@@ -167,11 +180,16 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
   }
 }
 
+__global__ void alloc_sync_clear_kernel(int32_t* sync, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) sync[i] = 0;
+}
+
 __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     Geo g, SeqTab st, const float* __restrict__ curves, const float* __restrict__ cmin,
     const float* __restrict__ cmaxb, const int32_t* __restrict__ cpos,
     const double* __restrict__ dmax, int32_t nblk_max, int32_t steps,
-    int32_t* __restrict__ budgets, int64_t* __restrict__ stats) {
+    int32_t* __restrict__ budgets, int64_t* __restrict__ stats, int32_t K, int32_t* sync) {
   // 64 KB of LDS: block minima + candidate lists during the bisection, the
   // block-level running maxima of the marginals during the repair.
   __shared__ __align__(16) unsigned char pool[kLdsItems * 8];
@@ -192,10 +210,27 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   __shared__ int64_t cnt_lt[64], cnt_le[64];
   __shared__ int64_t cnt_j[kHeadGroup];  // per (threshold, head) counts of the repair search
   __shared__ float win[64][kRepairWin + 1];
+  __shared__ double tlam[kTreeMax], tlo[kTreeMax], thi[kTreeMax];  // node multipliers
+  __shared__ int64_t tsum[kTreeMax];                                // node budget sums
+  __shared__ int32_t ticket;
 
-  const int bl = blockIdx.x;
-  const int l = blockIdx.y;
-  if (bl >= st.count) return;
+  // With K > 1 workgroups per (layer, sequence), groups are formed from an
+  // atomic ticket in arrival order: a workgroup waits only for the others of
+  // its group, and the lowest unfinished group either has every member
+  // started or holds every started workgroup, so groups always complete.
+  int bl, l, node = 0, grp = 0;
+  if (K > 1) {
+    if (threadIdx.x == 0) ticket = atomicAdd(&sync[0], 1);
+    __syncthreads();
+    grp = ticket / K;
+    node = ticket - grp * K;
+    bl = grp % st.count;
+    l = grp / st.count;
+  } else {
+    bl = blockIdx.x;
+    l = blockIdx.y;
+  }
+  if (bl >= st.count || l >= g.L) return;
   const int b = st.first + bl;
   const int n = st.len[bl];
   const int64_t tok0 = st.start[bl];
@@ -608,19 +643,108 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       evaluate_scan(lam, out);
   };
 
-  evaluate(hi, bhi);
-  for (int t = 0; t < steps; ++t) {
-    const double lam = (lo + hi) / 2.0;
-    evaluate(lam, bcur);
-    int64_t sum = 0;
-    for (int h = 0; h < H; ++h) sum += bcur[h];
-    if (sum > B_real) {
-      lo = lam;
-    } else {
-      hi = lam;
-      if (tid < H) bhi[tid] = bcur[tid];
+  // Bisection on lambda: lambda = (lo + hi) / 2, then lo = lambda if the
+  // budgets at lambda sum above B_real, else hi = lambda (and bhi = the
+  // budgets there).
+  if (K <= 1) {
+    evaluate(hi, bhi);
+    for (int t = 0; t < steps; ++t) {
+      const double lam = (lo + hi) / 2.0;
+      evaluate(lam, bcur);
+      int64_t sum = 0;
+      for (int h = 0; h < H; ++h) sum += bcur[h];
+      if (sum > B_real) {
+        lo = lam;
+      } else {
+        hi = lam;
+        if (tid < H) bhi[tid] = bcur[tid];
+      }
+      __syncthreads();
     }
-    __syncthreads();
+  } else {
+    // The same steps, lev at a time: the multipliers of the next lev steps
+    // form a binary tree (node i's children 2i+1 after hi = lambda_i and
+    // 2i+2 after lo = lambda_i), each computed from its interval exactly as
+    // the step-by-step bisection would.  The group's workgroup `node`
+    // evaluates node `node`, the sums are exchanged through global memory,
+    // and every workgroup then follows the same path down the tree.  Only
+    // node 0 keeps bhi and goes on to the repair.
+    const int lev_max = 31 - __clz(K + 1);
+    int64_t* xsum = reinterpret_cast<int64_t*>(sync + kSyncSum) + (size_t)grp * 2 * kTreeMax;
+    int32_t* xarg = sync + kSyncArg + (size_t)grp * 2 * kTreeMax * 64;
+    int32_t* cnt = sync + 2 + grp;
+    if (node == 0) evaluate(hi, bhi);
+    int t = 0, pass = 0;
+    while (t < steps) {
+      const int lv = min(lev_max, steps - t);
+      const int nl = (1 << lv) - 1;
+      const int par = pass & 1;
+      if (tid == 0) {
+        tlo[0] = lo;
+        thi[0] = hi;
+        for (int i = 0; i < nl; ++i) {
+          tlam[i] = (tlo[i] + thi[i]) / 2.0;
+          if (2 * i + 2 < nl) {
+            tlo[2 * i + 1] = tlo[i];
+            thi[2 * i + 1] = tlam[i];
+            tlo[2 * i + 2] = tlam[i];
+            thi[2 * i + 2] = thi[i];
+          }
+        }
+      }
+      __syncthreads();
+      if (node < nl) {
+        evaluate(tlam[node], bcur);
+        int64_t sum = 0;
+        for (int h = 0; h < H; ++h) sum += bcur[h];
+        if (tid == 0)
+          __hip_atomic_store(&xsum[par * kTreeMax + node], sum, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        if (tid < H)
+          __hip_atomic_store(&xarg[(par * kTreeMax + node) * 64 + tid], bcur[tid],
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      // group barrier: every member has published this pass.  The arrival
+      // releases the workgroup's stores (ordered before it by the barrier);
+      // the wait polls with coherent loads and acquires once at the end.
+      __syncthreads();
+      if (tid == 0) {
+        const int target = K * (pass + 1);
+        __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        int spins = 0;
+        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+          __builtin_amdgcn_s_sleep(1);
+          if (++spins > (1 << 22)) {  // a member never arrived: give up, report
+            if (g.status) *g.status = CERTKV_EHIP;
+            break;
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      }
+      __syncthreads();
+      if (tid < nl)
+        tsum[tid] = __hip_atomic_load(&xsum[par * kTreeMax + tid], __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      int nd = 0, last = -1;
+      for (int j = 0; j < lv; ++j) {
+        if (tsum[nd] > B_real) {
+          lo = tlam[nd];
+          nd = 2 * nd + 2;
+        } else {
+          hi = tlam[nd];
+          last = nd;
+          nd = 2 * nd + 1;
+        }
+      }
+      if (node == 0 && last >= 0 && tid < H)
+        bhi[tid] = __hip_atomic_load(&xarg[(par * kTreeMax + last) * 64 + tid], __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      t += lv;
+      ++pass;
+    }
+    if (node != 0) return;
   }
   const uint64_t t_bisect = wall_clock64();
 
@@ -818,9 +942,30 @@ certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) 
   const int per_unit = (a.nblk_max + 3) / 4;
   CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
                 dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.cpos, a.dmax);
-  CERTKV_LAUNCH("allocate", allocate_kernel, dim3(st.count, a.g.L), dim3(kAllocThreads), 0, s, a.g,
-                st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb, (const int32_t*)a.cpos,
-                (const double*)a.dmax, a.nblk_max, a.steps, a.budgets, a.repairs);
+  // Workgroups per (layer, sequence): a node tree of 3 or 7 when every group
+  // of the launch then still has a compute unit per workgroup (one
+  // allocation workgroup fills a compute unit's LDS), else 1.
+  const int groups = st.count * a.g.L;
+  int K = 1;
+  if (a.sync && a.steps > 1 && groups <= kSyncGroups) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return CERTKV_EHIP;
+    const int cus = device_cus(dev);
+    K = 7 * groups <= cus ? 7 : 3 * groups <= cus ? 3 : 1;
+  }
+  if (K > 1) {
+    CERTKV_LAUNCH("alloc_sync_clear", alloc_sync_clear_kernel, dim3((unsigned)((kSyncCnt + 255) / 256)),
+                  dim3(256), 0, s, a.sync, (int)kSyncCnt);
+    CERTKV_LAUNCH("allocate", allocate_kernel, dim3((unsigned)(K * groups)), dim3(kAllocThreads), 0,
+                  s, a.g, st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb,
+                  (const int32_t*)a.cpos, (const double*)a.dmax, a.nblk_max, a.steps, a.budgets,
+                  a.repairs, K, a.sync);
+  } else {
+    CERTKV_LAUNCH("allocate", allocate_kernel, dim3(st.count, a.g.L), dim3(kAllocThreads), 0, s,
+                  a.g, st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb,
+                  (const int32_t*)a.cpos, (const double*)a.dmax, a.nblk_max, a.steps, a.budgets,
+                  a.repairs, 1, (int32_t*)nullptr);
+  }
   return CERTKV_OK;
 }
 

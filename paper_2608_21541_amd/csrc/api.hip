@@ -234,6 +234,7 @@ struct Bufs {
   double* dmax = nullptr;
   double* vsum = nullptr;
   int64_t* repairs = nullptr;
+  int32_t* alloc_sync = nullptr;
   // select / tail
   uint64_t* bitmap = nullptr;
   int64_t* kept_offsets = nullptr;
@@ -284,6 +285,7 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
     b->cpos = w.take<int32_t>((size_t)P.U * P.nblk_max);
     b->dmax = w.take<double>((size_t)P.U * P.nblk_max);
     b->repairs = w.take<int64_t>((size_t)P.g.L * P.g.B * 3);
+    b->alloc_sync = w.take<int32_t>(alloc_sync_words());
   }
   if (need & NEED_BITMAP) {
     b->bitmap = w.take<uint64_t>((size_t)P.U * P.bm_words);
@@ -408,6 +410,7 @@ static certkv_status do_allocate(const Plan& P, const float* curves, const int32
   a.steps = P.alloc == 2 ? 0 : steps;  // greedy marginal: the repair from b_min
   a.budgets = budgets;
   a.repairs = stats ? stats : w.repairs;
+  a.sync = w.alloc_sync;
   (void)minmax;
   for (const SeqTab& t : make_tabs(P, n_keep, alpha)) {
     if (P.alloc == 1)

@@ -103,7 +103,9 @@ __device__ __forceinline__ double uniform_f64(double x) {
                   __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)));
 }
 
-template <int D, bool BF16>
+// STAT: the curve statistic (0 centered, 1 uncentered, 2 tail mass), a
+// template parameter so that the walk has no branch on it.
+template <int D, bool BF16, int STAT>
 __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     Geo g, SeqTab st, const uint32_t* __restrict__ sorted_keys, const int32_t* __restrict__ perm,
     const double* __restrict__ ssum, const void* __restrict__ vc, int64_t v_sl, int64_t v_st,
@@ -330,7 +332,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       // the lanes' parts sum to m Q - |W|^2 (centered), m Q (uncentered) or,
       // for the tail mass, m^2 (32 equal parts of m^2 / 32, exact), whose
       // square root is m
-      double cur = g.stat == 0 ? fma(m, q, -w2) : g.stat == 1 ? m * q : (m * m) * (1.0 / kLPR);
+      double cur = STAT == 0 ? fma(m, q, -w2) : STAT == 1 ? m * q : (m * m) * (1.0 / kLPR);
       bool placed = false;
 #pragma unroll
       for (int lev = 0; lev < kLev; ++lev) {
@@ -384,28 +386,33 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   }
 }
 
-certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
-  dim3 grid(a.g.H * st.count, a.g.L);
-  if (a.dtype == CERTKV_BF16) {
-    if (a.g.D == 128)
-      CERTKV_LAUNCH("curves", (curves_kernel<128, true>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+template <int D, bool BF16>
+static certkv_status launch_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
+  const dim3 grid(a.g.H * st.count, a.g.L);
+  switch (a.g.stat) {
+    case 0:
+      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 0>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
                     a.curves, a.vsum);
-    else
-      CERTKV_LAUNCH("curves", (curves_kernel<64, true>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+      break;
+    case 1:
+      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 1>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
                     a.curves, a.vsum);
-  } else {
-    if (a.g.D == 128)
-      CERTKV_LAUNCH("curves", (curves_kernel<128, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+      break;
+    default:
+      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 2>), grid, dim3(kCurveThreads), 0, s, a.g, st,
                     a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
                     a.curves, a.vsum);
-    else
-      CERTKV_LAUNCH("curves", (curves_kernel<64, false>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.vsum);
+      break;
   }
   return CERTKV_OK;
+}
+
+certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
+  if (a.dtype == CERTKV_BF16)
+    return a.g.D == 128 ? launch_curves<128, true>(a, st, s) : launch_curves<64, true>(a, st, s);
+  return a.g.D == 128 ? launch_curves<128, false>(a, st, s) : launch_curves<64, false>(a, st, s);
 }
 
 }  // namespace certkv

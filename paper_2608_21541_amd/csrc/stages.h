@@ -64,7 +64,9 @@ struct AllocArgs {
   int32_t steps;
   int32_t* budgets;
   int64_t* repairs;
+  int32_t* sync;    // alloc_sync_words() words: cross-workgroup bisection (optional)
 };
+size_t alloc_sync_words();
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s);
 
 struct SelectArgs {

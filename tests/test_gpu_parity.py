@@ -264,6 +264,37 @@ def test_allocate_from_supplied_curves_matches_oracle():
             assert np.array_equal(got, want), (n_keep, got, want)
 
 
+@pytest.mark.parametrize("layers", [2, 40, 100])
+def test_allocate_workgroup_tree_widths_and_step_counts(layers):
+    # The bisection runs on 7, 3 or 1 workgroups per (layer, sequence)
+    # depending on how many (layer, sequence) groups the launch has (2 -> 7,
+    # 40 -> 3, 100 -> 1 on a 256-CU device), resolving up to 3 steps per
+    # exchange; step counts that leave a partial last pass and a batch of
+    # two sequences are included.  Budgets must equal the oracle's for every
+    # layer, sequence and step count.
+    rng = np.random.default_rng(layers)
+    H, lens = 4, [700, 333]
+    T = sum(lens)
+    c = np.zeros((layers, H, T), np.float32)
+    for li in range(layers):
+        off = 0
+        for n in lens:
+            r = np.abs(np.cumsum(rng.standard_normal((H, n)), 1))[:, ::-1]
+            c[li, :, off:off + n] = r * rng.uniform(0.1, 10, (H, 1))
+            off += n
+    spec = ck.ProblemSpec(layers, H, 2, 64, 16, lens, torch.bfloat16)
+    t = torch.from_numpy(c).cuda()
+    n_keep = [71, 40]
+    for steps in [0, 1, 2, 3, 4, 5, 7, 40]:
+        got = ck.allocate_curves(spec, t, n_keep, steps=steps).cpu().numpy().reshape(layers, 2, H)
+        for li in range(layers):
+            off = 0
+            for bi, n in enumerate(lens):
+                want, _ = oracle.allocate(c[li, :, off:off + n], n_keep[bi], steps=steps)
+                assert np.array_equal(got[li, bi], want), (layers, steps, li, bi, got[li, bi], want)
+                off += n
+
+
 # --------------------------------------------------------------------------
 # Rows whose unshifted exponentials leave fp32 range take the max-shifted
 # fallback of the scoring pass.
