@@ -466,8 +466,13 @@ def run_decode_bench(args, cfg, cache, spec, bufs, n_keep, dev, log):
         torch.cuda.synchronize()
         dec_ms = t0.elapsed_time(t1) / args.steps
         evicted = int(cfg.layers * cfg.kv_heads * sum(cfg.seqlens)) - rows
-        clusters = {"m": m, "cluster_tail_ms": tail_ms,
-                    "cluster_tail_GBps": 2 * evicted * cfg.head_dim * e * 2 / (tail_ms / 1e3) / 1e9,
+        # algorithmic bytes: every evicted row's K and V slice and rank entry
+        # once, the provisional centres' sample (every 16th member at most)
+        # again, and every kept row's V slice and rank entry (the kept value
+        # norm)
+        cl_bytes = evicted * (2 * cfg.head_dim * e + 4) * (1 + 1 / 16) + rows * (cfg.head_dim * e + 4)
+        clusters = {"m": m, "cluster_tail_ms": tail_ms, "cluster_tail_alg_bytes": cl_bytes,
+                    "cluster_tail_GBps": cl_bytes / (tail_ms / 1e3) / 1e9,
                     "decode_clustered_ms": dec_ms,
                     "finite_certificates": float(torch.isfinite(bound).float().mean())}
         log(f"clusters: {clusters}")

@@ -378,9 +378,12 @@ certkv_status certkv_decode(const certkv_problem* p, certkv_tensor q_new,
  *   cluster_count [U][m] int32 out   n_g
  *   cluster_k, cluster_v [U][m][d] out in kv_dtype: the unweighted mean key
  *                  and value (fp64 sums), as stored
- *   cluster_rk, cluster_rv [U][m] fp32 out: max |k_j - kbar_g|, max |v_j -
- *                  vbar_g| over the members against the stored means, rounded
- *                  up (radii that hold for the stored rows)
+ *   cluster_rk, cluster_rv [U][m] fp32 out: radii in the sense of the
+ *                  cluster-radii equation, >= |k_j - kbar_g| and >= |v_j -
+ *                  vbar_g| for every member against the stored means: with
+ *                  c_g the mean of every S-th member (S = n_g / 64 clamped to
+ *                  [1, 16]), max |x_j - c_g| + |c_g - xbar_g| (triangle
+ *                  inequality; one pass over the members), fp64, rounded up
  *   kept_vmax [U] fp32 out: the largest norm of a kept value
  * Inputs: k, v as for certkv_score; perm [L][H][T] the rank order of the
  * pass (certkv_allocate or certkv_outputs.perm); budgets [U] (b_h).

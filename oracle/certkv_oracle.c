@@ -758,11 +758,16 @@ int ora_lift_terms(int64_t n, int32_t d, const double* q, const double* k, const
  * pass's order, are cut into m contiguous groups of ceil((n - b) / m) ranks
  * (later groups may be short or empty).  Per group g: the count n_g, the
  * representative key and value (the unweighted means, rounded to fp32 and
- * then to bf16 when bf16 != 0, as they would be stored), and the radii
- * R_g = max |k_j - kbar_g|, rho_g = max |v_j - vbar_g| against the stored
- * representatives, rounded up to fp32.  Also the largest kept value norm.
+ * then to bf16 when bf16 != 0, as they would be stored), and radii that the
+ * cluster-radii equation admits, i.e. upper bounds of |k_j - kbar_g| and
+ * |v_j - vbar_g| over the members: with c_g the mean of every S-th member
+ * (ranks r0, r0 + S, ...; S = n_g / 64 clamped to [1, ORA_CLUSTER_SAMPLE],
+ * so at least 64 members or all of them),
+ *   R_g = max_j |k_j - c_g| + |c_g - kbar_g|   (triangle inequality),
+ * likewise rho_g, rounded up to fp32.  Also the largest kept value norm.
  *   perm [n] the rank order; k, v [n][d] position-indexed
  *   kbar, vbar [m][d] out; cnt [m] out; R, rho [m] out; vmax_kept out. */
+#define ORA_CLUSTER_SAMPLE 16
 static double ora_store_rep(double x, int32_t bf16) {
   float f = (float)x;
   if (!bf16) return (double)f;
@@ -806,21 +811,46 @@ int ora_cluster_summaries(int64_t n, int32_t d, const int32_t* perm, int64_t b,
       kb[t] = ora_store_rep(kb[t] / (double)(r1 - r0), bf16);
       vb[t] = ora_store_rep(vb[t] / (double)(r1 - r0), bf16);
     }
+    /* provisional centres: the mean of the sampled members */
+    double* ck = (double*)calloc((size_t)2 * d, sizeof(double));
+    if (!ck) return ORA_ENOMEM;
+    double* cv = ck + d;
+    int64_t stride = (r1 - r0) / 64;
+    if (stride < 1) stride = 1;
+    if (stride > ORA_CLUSTER_SAMPLE) stride = ORA_CLUSTER_SAMPLE;
+    int64_t ns = 0;
+    for (int64_t r = r0; r < r1; r += stride, ++ns) {
+      const int32_t j = perm[r];
+      for (int32_t t = 0; t < d; ++t) {
+        ck[t] += k[(size_t)j * d + t];
+        cv[t] += v[(size_t)j * d + t];
+      }
+    }
+    for (int32_t t = 0; t < d; ++t) {
+      ck[t] /= (double)ns;
+      cv[t] /= (double)ns;
+    }
     double rk = 0.0, rv = 0.0;
     for (int64_t r = r0; r < r1; ++r) {
       const int32_t j = perm[r];
       double sk = 0.0, sv = 0.0;
       for (int32_t t = 0; t < d; ++t) {
-        const double dk = k[(size_t)j * d + t] - kb[t];
-        const double dv = v[(size_t)j * d + t] - vb[t];
+        const double dk = k[(size_t)j * d + t] - ck[t];
+        const double dv = v[(size_t)j * d + t] - cv[t];
         sk += dk * dk;
         sv += dv * dv;
       }
       if (sk > rk) rk = sk;
       if (sv > rv) rv = sv;
     }
-    R[g] = ora_round_up_f32(sqrt(rk));
-    rho[g] = ora_round_up_f32(sqrt(rv));
+    double ek = 0.0, ev = 0.0;
+    for (int32_t t = 0; t < d; ++t) {
+      ek += (ck[t] - kb[t]) * (ck[t] - kb[t]);
+      ev += (cv[t] - vb[t]) * (cv[t] - vb[t]);
+    }
+    free(ck);
+    R[g] = ora_round_up_f32(sqrt(rk) + sqrt(ek));
+    rho[g] = ora_round_up_f32(sqrt(rv) + sqrt(ev));
   }
   double vm = 0.0;
   for (int64_t r = 0; r < b; ++r) {

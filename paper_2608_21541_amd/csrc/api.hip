@@ -839,6 +839,7 @@ certkv_status certkv_cluster_tail(const certkv_problem* p, certkv_tensor k, cert
   a.rk = cluster_rk;
   a.rv = cluster_rv;
   a.vmax_kept = kept_vmax;
+  TRY(run_clusters_clear(kept_vmax, P.U, (hipStream_t)stream));
   for (const SeqTab& t : make_tabs(P, nullptr, 0.0)) TRY(run_clusters(a, t, (hipStream_t)stream));
   return CERTKV_OK;
 }

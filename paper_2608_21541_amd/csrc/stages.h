@@ -139,6 +139,7 @@ struct ClusterArgs {
   float* vmax_kept;             // [U]
 };
 certkv_status run_clusters(const ClusterArgs& a, const SeqTab& st, hipStream_t s);
+certkv_status run_clusters_clear(float* vmax_kept, int64_t U, hipStream_t s);  // before run_clusters
 
 // Optional clustered-tail terms of a decode (added in the combine).
 struct DecodeClusters {

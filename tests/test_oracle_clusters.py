@@ -92,3 +92,58 @@ def test_certificate_bounds_the_true_error(seed):
         else:
             assert c["dz"] > 1 / 3
     assert finite >= 4   # the certificate is not vacuous here
+
+
+def test_radii_hand_computed_sampled_centre():
+    # One group of 192 members in rank order: member stride S = 192 / 64 = 3,
+    # so the sample is ranks 0, 3, 6, ...  The keys of sampled ranks are
+    # (0, 0), the others (6, 0); the values of sampled ranks are (0, 3), the
+    # others (0, -3).  With fp32 storage: c_k = (0, 0), kbar = (4, 0);
+    # c_v = (0, 3), vbar = (0, -1).  Then
+    #   R   = max |k - c_k| + |c_k - kbar| = 6 + 4 = 10   (exact max: 4)
+    #   rho = max |v - c_v| + |c_v - vbar| = 6 + 4 = 10   (exact max: 4)
+    n = 192
+    samp = np.arange(n) % 3 == 0
+    k = np.where(samp[:, None], [[0.0, 0.0]], [[6.0, 0.0]])
+    v = np.where(samp[:, None], [[0.0, 3.0]], [[0.0, -3.0]])
+    perm = np.arange(n, dtype=np.int32)
+    cl = oracle.cluster_summaries(perm, 0, k, v, 1, bf16=False)
+    np.testing.assert_array_equal(cl["kbar"][0], [4.0, 0.0])
+    np.testing.assert_array_equal(cl["vbar"][0], [0.0, -1.0])
+    assert cl["R"][0] == 10.0 and cl["rho"][0] == 10.0
+    # groups of at most 64 members use them all (S = 1): c is the exact mean
+    # and the radii are the exact maxima up to the storage rounding
+    k = np.array([[0.0, 0.0], [2.0, 0.0], [4.0, 0.0]])
+    cl = oracle.cluster_summaries(np.arange(3, dtype=np.int32), 0, k, k, 1, bf16=False)
+    assert cl["R"][0] == 2.0
+    # 2000 members: S = 2000 / 64 = 31 clamped to 16, sample ranks 0, 16, ...
+    rng = np.random.default_rng(5)
+    k = rng.integers(-8, 9, size=(2000, 4)).astype(np.float64)
+    v = rng.integers(-8, 9, size=(2000, 4)).astype(np.float64)
+    perm = rng.permutation(2000).astype(np.int32)
+    cl = oracle.cluster_summaries(perm, 0, k, v, 1, bf16=False)
+    for x, bar, r in ((k, cl["kbar"][0], cl["R"][0]), (v, cl["vbar"][0], cl["rho"][0])):
+        c = x[perm[::16]].mean(0)
+        want = np.linalg.norm(x - c, axis=1).max() + np.linalg.norm(c - bar)
+        assert want <= r <= want * (1 + 2 ** -22)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_radii_bound_every_member_and_stay_tight(bf16):
+    # the cluster-radii equation: every member within R of the stored key
+    # representative and within rho of the stored value one; on Gaussian
+    # groups of ~1000 members the sampled centre is close to the mean, so the
+    # radii exceed the exact maxima by a few percent only
+    rng = np.random.default_rng(6)
+    n, d, b = 4200, 32, 200
+    k, v, perm = _head(rng, n, d, b)
+    m = 4
+    cl = oracle.cluster_summaries(perm, b, k, v, m, bf16=bf16)
+    E = perm[b:]
+    cs = -(-len(E) // m)
+    for g in range(m):
+        mem = E[g * cs:(g + 1) * cs]
+        ek = np.linalg.norm(k[mem] - cl["kbar"][g], axis=1).max()
+        ev = np.linalg.norm(v[mem] - cl["vbar"][g], axis=1).max()
+        assert ek <= cl["R"][g] <= 1.15 * ek
+        assert ev <= cl["rho"][g] <= 1.15 * ev
