@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
     float sv[kSortRounds], sn[kSortRounds];
     load_scores(0, sv);
     for (int t0 = 0; t0 < n; t0 += kSortTile) {
-      if (t0 + kSortTile < n) load_scores(t0 + kSortTile, sn);
+      load_scores(t0 + kSortTile, sn);  // unconditional: clamped reads, no branch
 #pragma unroll
       for (int r = 0; r < kSortRounds; ++r) {
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
@@ -176,8 +176,10 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
       wave_scan256(bucket, lane);
     }
     // Loads through range-checked buffers: elements at or beyond n read as
-    // zero, so no clamp or branch sits around them (the asm keeps the score
-    // loads from being sunk into the window test).
+    // zero, so no clamp or branch sits around them.  The first pass loads
+    // the raw score bits and forms their radix keys (and the kept window's
+    // zero keys) only when the tile is ranked, so that the next tile's loads
+    // stay in flight meanwhile.
     const BufRsrc kin_r = make_rsrc(p == 0 ? (const void*)(scores + base) : (const void*)(kin + base),
                                     (uint32_t)n * 4u);
     const BufRsrc vin_r = make_rsrc(vin + base, (uint32_t)n * 4u);
@@ -189,9 +191,7 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
         const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
         const uint32_t off = (uint32_t)e * 4u;
         if (p == 0) {
-          uint32_t xb = buf_load_u32(kin_r, off);
-          __asm__ volatile("" : "+v"(xb));
-          key[r] = e >= wkeep ? 0u : desc_key(__uint_as_float(xb));
+          key[r] = buf_load_u32(kin_r, off);
           val[r] = e;
         } else {
           key[r] = buf_load_u32(kin_r, off);
@@ -206,7 +206,16 @@ __global__ __launch_bounds__(kSortThreads) void seg_sort_kernel(
       const int tp = (t0 / kSortTile) & 1;  // tile parity
 #pragma unroll
       for (int j = 0; j < 4; ++j) wave_cnt[wave][lane * 4 + j] = 0u;
-      if (t0 + kSortTile < n) load(t0 + kSortTile, nkey, nval);  // prefetch
+      // prefetch, unconditionally (past the end the range check reads zeros),
+      // so that no branch makes the compiler wait for it before the ranking
+      load(t0 + kSortTile, nkey, nval);
+      if (p == 0) {
+#pragma unroll
+        for (int r = 0; r < kSortRounds; ++r) {
+          const int e = t0 + wave * 64 * kSortRounds + r * 64 + lane;
+          key[r] = e >= wkeep ? 0u : desc_key(__uint_as_float(key[r]));
+        }
+      }
       // rank within the wave
       uint32_t rank[kSortRounds];
 #pragma unroll
