@@ -157,24 +157,23 @@ __global__ __launch_bounds__(kTailThreads) void tail_gather_kernel(
   // scores, are loaded together so that each step waits for two round trips.
   constexpr int UR = 4;
   for (int i = i0 + ri; i < i1; i += RPS * UR) {
+    // The entries past the run read a clamped one and fetch its row again,
+    // unused: no load sits behind a branch, so none waits for itself.
     int j[UR];
 #pragma unroll
-    for (int q = 0; q < UR; ++q) {
-      const int ii = i + q * RPS;
-      j[q] = ii < i1 ? min(max(kept_idx[off + ii], 0), n - 1) : -1;  // caller indices clamped
-    }
+    for (int q = 0; q < UR; ++q)
+      j[q] = min(max(kept_idx[off + min(i + q * RPS, i1 - 1)], 0), n - 1);  // caller indices clamped
     uint4 kq[UR], vq[UR];
     float sv[UR];
 #pragma unroll
     for (int q = 0; q < UR; ++q) {
-      const int jj = j[q] < 0 ? 0 : j[q];
-      kq[q] = *reinterpret_cast<const uint4*>(kb + (int64_t)jj * k_st + ci * EPL);
-      vq[q] = *reinterpret_cast<const uint4*>(vb + (int64_t)jj * v_st + ci * EPL);
-      sv[q] = DO_TAIL ? scores[sbase + jj] : 0.f;
+      kq[q] = *reinterpret_cast<const uint4*>(kb + (int64_t)j[q] * k_st + ci * EPL);
+      vq[q] = *reinterpret_cast<const uint4*>(vb + (int64_t)j[q] * v_st + ci * EPL);
+      sv[q] = DO_TAIL ? scores[sbase + j[q]] : 0.f;
     }
 #pragma unroll
     for (int q = 0; q < UR; ++q) {
-      if (j[q] < 0) continue;
+      if (i + q * RPS >= i1) continue;
       const int ii = i + q * RPS;
       if (DO_COMPACT) {
         *reinterpret_cast<uint4*>(k_packed + (poff + ii) * D + ci * EPL) = kq[q];
