@@ -722,12 +722,14 @@ __global__ __launch_bounds__(kP2Threads) __attribute__((amdgpu_waves_per_eu(4, 8
           }
         }
         if (more) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 2 + 4 + (MASKED ? 4 : 0), 0);
+          // every query fragment of the next tile read up front (measured
+          // faster here than two steps ahead), then per k-step one MFMA and
+          // the current tile's terms of that slice
+          __builtin_amdgcn_sched_group_barrier(0x100, KS + 4 + (MASKED ? 4 : 0), 0);
 #pragma unroll
           for (int s = 0; s < KS; ++s) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x402, (MASKED ? 5 : 3) * SL, 0);
-            if (s + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
         }
         acc = nacc;
