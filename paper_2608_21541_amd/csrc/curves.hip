@@ -103,8 +103,10 @@ __device__ __forceinline__ double uniform_f64(double x) {
                   __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)));
 }
 
-// STAT: the curve statistic (0 centered, 1 uncentered, 2 tail mass), a
-// template parameter so that the walk has no branch on it.
+// STAT: the curve statistic (0 centered, 1 uncentered, 2 tail mass) fixed at
+// compile time, so that the walk has no branch on it, or -1: read from
+// g.stat at run time (the ablation statistics: compiled with the statistic
+// fixed, their walks need more registers than the kernel has and spill).
 template <int D, bool BF16, int STAT>
 __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     Geo g, SeqTab st, const uint32_t* __restrict__ sorted_keys, const int32_t* __restrict__ perm,
@@ -332,7 +334,8 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       // the lanes' parts sum to m Q - |W|^2 (centered), m Q (uncentered) or,
       // for the tail mass, m^2 (32 equal parts of m^2 / 32, exact), whose
       // square root is m
-      double cur = STAT == 0 ? fma(m, q, -w2) : STAT == 1 ? m * q : (m * m) * (1.0 / kLPR);
+      const int stat = STAT >= 0 ? STAT : g.stat;
+      double cur = stat == 0 ? fma(m, q, -w2) : stat == 1 ? m * q : (m * m) * (1.0 / kLPR);
       bool placed = false;
 #pragma unroll
       for (int lev = 0; lev < kLev; ++lev) {
@@ -389,23 +392,14 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
 template <int D, bool BF16>
 static certkv_status launch_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
   const dim3 grid(a.g.H * st.count, a.g.L);
-  switch (a.g.stat) {
-    case 0:
-      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 0>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.vsum);
-      break;
-    case 1:
-      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 1>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.vsum);
-      break;
-    default:
-      CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 2>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                    a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                    a.curves, a.vsum);
-      break;
-  }
+  if (a.g.stat == 0)
+    CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 0>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+                  a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
+                  a.curves, a.vsum);
+  else
+    CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, -1>), grid, dim3(kCurveThreads), 0, s, a.g, st,
+                  a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
+                  a.curves, a.vsum);
   return CERTKV_OK;
 }
 
