@@ -35,6 +35,7 @@ constexpr int kCandCap = 1024;    // candidate blocks evaluated per round
 constexpr int kBlk = 256;          // ranks per pruning block
 constexpr int kLdsItems = 8192;    // H * blocks handled from LDS
 constexpr int kRepairWin = 64;     // cached curve values per head (fallback repair)
+constexpr int kRcStride = kBlk + 4;  // a cached curve block of the repair search: kBlk + 1 values
 // Bisection across several workgroups per (layer, sequence): up to kTreeLev
 // levels per pass, one workgroup per node of the level tree.
 constexpr int kTreeLev = 3;
@@ -63,6 +64,21 @@ struct BestFB {
   double f;
   int b;
 };
+
+// Minimum over each half-wave (lanes 0-31 and 32-63), in every lane of the
+// half: DPP exchanges within rows of 16 lanes (lane ^ 1, lane ^ 2, then the
+// mirrored lane within 8 and within 16: after the first steps the values are
+// equal within the smaller groups, so a mirror pairs the groups as an xor
+// would), then v_permlane16_swap pairs the two rows of each half.  Every lane
+// of a half must be active.
+__device__ __forceinline__ int half_min_i32(int x) {
+  x = min(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));
+  x = min(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));
+  x = min(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));
+  x = min(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));
+  const auto r = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
+  return min((int)r[0], (int)r[1]);
+}
 
 // Lexicographic (f, b) minimum over the 32 lanes of a half-wave.
 __device__ __forceinline__ BestFB half_wave_min(double f, int b) {
@@ -200,7 +216,17 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   __shared__ int32_t bbest[64], kstar[64];
   __shared__ float cbest[64], cprev[64];  // curve values at bbest and bprev
   __shared__ int32_t bprev[64];           // previous argmin (-1: none)
-  __shared__ int32_t mpos[kLdsItems];     // smallest position of each block's minimum
+  // One region for three phases: the smallest position of each block's
+  // minimum (bisection), the repair search's cached curve blocks, one per
+  // (threshold, head) half-wave, and the sequential repair's curve windows.
+  constexpr size_t kAuxA = (size_t)kLdsItems * 4, kAuxB = (size_t)kHeadGroup * kRcStride * 4,
+                   kAuxC = (size_t)64 * (kRepairWin + 1) * 4;
+  constexpr size_t kAux = kAuxA > kAuxB ? (kAuxA > kAuxC ? kAuxA : kAuxC) : (kAuxB > kAuxC ? kAuxB : kAuxC);
+  __shared__ __align__(16) unsigned char aux[kAux];
+  int32_t* mpos = reinterpret_cast<int32_t*>(aux);
+  float* rcache = reinterpret_cast<float*>(aux);
+  float(*win)[kRepairWin + 1] = reinterpret_cast<float(*)[kRepairWin + 1]>(aux);
+  __shared__ int32_t rkey[kHeadGroup];  // (head << 16) | block of each cached block (-1: none)
   __shared__ float cres_c[kCandCap];
   __shared__ int32_t bcur[64], bhi[64];
   __shared__ double redf[kAllocWaves];
@@ -208,8 +234,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   __shared__ int32_t cres_b[kCandCap];
   __shared__ int32_t ncand, scan_pos;
   __shared__ int64_t cnt_lt[64], cnt_le[64];
-  __shared__ int64_t cnt_j[kHeadGroup];  // per (threshold, head) counts of the repair search
-  __shared__ float win[64][kRepairWin + 1];
+  __shared__ int64_t cnt_j[64];  // per (threshold, head) counts of the repair search
   __shared__ double tlam[kTreeMax], tlo[kTreeMax], thi[kTreeMax];  // node multipliers
   __shared__ int64_t tsum[kTreeMax];                                // node budget sums
   __shared__ int32_t ticket;
@@ -646,8 +671,10 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   // Bisection on lambda: lambda = (lo + hi) / 2, then lo = lambda if the
   // budgets at lambda sum above B_real, else hi = lambda (and bhi = the
   // budgets there).
+  // The budgets at the initial lambda_hi are needed only when no step lowers
+  // it; they are then evaluated after the steps.
+  bool have_bhi = false;
   if (K <= 1) {
-    evaluate(hi, bhi);
     for (int t = 0; t < steps; ++t) {
       const double lam = (lo + hi) / 2.0;
       evaluate(lam, bcur);
@@ -657,10 +684,12 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         lo = lam;
       } else {
         hi = lam;
+        have_bhi = true;
         if (tid < H) bhi[tid] = bcur[tid];
       }
       __syncthreads();
     }
+    if (!have_bhi) evaluate(hi, bhi);
   } else {
     // The same steps, lev at a time: the multipliers of the next lev steps
     // form a binary tree (node i's children 2i+1 after hi = lambda_i and
@@ -673,7 +702,6 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     int64_t* xsum = reinterpret_cast<int64_t*>(sync + kSyncSum) + (size_t)grp * 2 * kTreeMax;
     int32_t* xarg = sync + kSyncArg + (size_t)grp * 2 * kTreeMax * 64;
     int32_t* cnt = sync + 2 + grp;
-    if (node == 0) evaluate(hi, bhi);
     int t = 0, pass = 0;
     while (t < steps) {
       const int lv = min(lev_max, steps - t);
@@ -740,11 +768,13 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       if (node == 0 && last >= 0 && tid < H)
         bhi[tid] = __hip_atomic_load(&xarg[(par * kTreeMax + last) * 64 + tid], __ATOMIC_RELAXED,
                                      __HIP_MEMORY_SCOPE_AGENT);
+      have_bhi = have_bhi || last >= 0;
       __syncthreads();
       t += lv;
       ++pass;
     }
     if (node != 0) return;
+    if (!have_bhi) evaluate(hi, bhi);
   }
   const uint64_t t_bisect = wall_clock64();
 
@@ -755,35 +785,68 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   const int kmax = (n - 2) / kBlk;  // last block holding an increment i <= n-2
 
   // Number of increments of head h whose key P is < p (le = false) or <= p
-  // (le = true); computed by the 32 threads of a half-wave.
-  auto count_head = [&](int h, double p, bool le) -> int64_t {
+  // (le = true); computed by the 32 threads of half-wave `slot` (< kHeadGroup),
+  // which keeps the last curve block it scanned in LDS: once the search has
+  // narrowed, successive thresholds cross in the same block and the count
+  // reads no global memory.
+  auto count_head = [&](int h, double p, bool le, int slot) -> int64_t {
     const int s = bhi[h];
     if (s > n - 2) return 0;
     const int ks = s / kBlk;
-    int lo_k = ks, hi_k = kmax + 1;  // first block whose running max crosses p
-    while (lo_k < hi_k) {
-      const int mid = (lo_k + hi_k) >> 1;
-      const double v = pbm[h * nblk + mid];
-      if (le ? (v > p) : (v >= p)) hi_k = mid;
-      else lo_k = mid + 1;
+    auto crosses = [&](double v) { return le ? (v > p) : (v >= p); };
+    const double* ph = pbm + h * nblk;
+    int lo_k;  // first block whose running max crosses p
+    const int key = rkey[slot];
+    const int kc = (key >> 16) == h ? (key & 0xffff) : -1;
+    if (kc >= ks && kc <= kmax && crosses(ph[kc]) && (kc == ks || !crosses(ph[kc - 1]))) {
+      lo_k = kc;
+    } else {
+      lo_k = ks;
+      int hi_k = kmax + 1;
+      while (lo_k < hi_k) {
+        const int mid = (lo_k + hi_k) >> 1;
+        if (crosses(ph[mid])) hi_k = mid;
+        else lo_k = mid + 1;
+      }
     }
     if (lo_k > kmax) return (int64_t)(n - 1 - s);
-    const float* ch = curves + lht_base(g, l, h, tok0);
+    float* rc = rcache + slot * kRcStride;  // c(lo_k kBlk + i), i = 0..kBlk
+    if (lo_k != kc) {
+      const float* ch = curves + lht_base(g, l, h, tok0);
+      float v[(kBlk + 32) / 32];
+#pragma unroll
+      for (int m = 0; m < (kBlk + 32) / 32; ++m) {
+        const int i = sub + 32 * m;
+        v[m] = i <= kBlk ? ch[min(lo_k * kBlk + i, n - 1)] : 0.f;
+      }
+#pragma unroll
+      for (int m = 0; m < (kBlk + 32) / 32; ++m) {
+        const int i = sub + 32 * m;
+        if (i <= kBlk) rc[i] = v[m];
+      }
+      // every thread of the half-wave has read rkey above; the block is read
+      // back by other threads of the same wave
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if (sub == 0) rkey[slot] = (h << 16) | lo_k;
+    }
     const int i0 = max(lo_k * kBlk, s), i1 = min(lo_k * kBlk + kBlk - 1, n - 2);
     int first = 0x7fffffff;
-    for (int i = i0 + sub; i <= i1; i += 32) {
-      const double d = (double)ch[i + 1] - (double)ch[i];
-      if ((le ? (d > p) : (d >= p)) && i < first) first = i;
-    }
 #pragma unroll
-    for (int m = 16; m >= 1; m >>= 1) first = min(first, __shfl_xor(first, m, 64));
+    for (int m = kBlk / 32 - 1; m >= 0; --m) {
+      const int r = sub + 32 * m, i = lo_k * kBlk + r;
+      const double d = (double)rc[r + 1] - (double)rc[r];
+      if (i >= i0 && i <= i1 && crosses(d)) first = i;
+    }
+    first = half_min_i32(first);
     return (int64_t)(first - s);
   };
   auto total_count = [&](double p, bool le, int64_t* per_head) -> int64_t {
     for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
       const int h = h0 + hg;
       if (h < H) {
-        const int64_t c = count_head(h, p, le);
+        const int64_t c = count_head(h, p, le, hg);
         if (sub == 0) per_head[h] = c;
       }
     }
@@ -804,6 +867,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       const int h = i / nblk, k = i - h * nblk;
       pbm[i] = dmax[unit_index(g, l, b, h) * nblk_max + k];
     }
+    if (tid < kHeadGroup) rkey[tid] = -1;
     __syncthreads();
     for (int h0 = 0; h0 < H; h0 += kHeadGroup) {
       const int h = h0 + hg;
@@ -854,18 +918,23 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     // increment): each step counts at J interior points of [klo, khi) at once,
     // one half-wave per (point, head).
     uint64_t klo = dkey(-INFINITY), khi = dkey(INFINITY);
-    const int J = kHeadGroup / H < 1 ? 1 : (kHeadGroup / H > 7 ? 7 : kHeadGroup / H);
-    // interior point j: klo + floor(span (j+1) / (J+1)), < khi, without overflow
+    // A = 2^la <= kHeadGroup / H (at least 2) parts per step, so that the
+    // points need no division; (point, head) pairs beyond the half-waves
+    // (more than 32 heads) are taken in further rounds
+    int la = 1;
+    while ((2 << la) <= kHeadGroup / H) ++la;
+    const int J = (1 << la) - 1;
+    // interior point j: klo + floor(span (j+1) / 2^la), < khi, without overflow
     auto point = [&](uint64_t lo_k, uint64_t span, int j) -> uint64_t {
-      const uint64_t q = span / (uint64_t)(J + 1), r = span % (uint64_t)(J + 1);
-      return lo_k + q * (uint64_t)(j + 1) + (r * (uint64_t)(j + 1)) / (uint64_t)(J + 1);
+      return lo_k + (span >> la) * (uint64_t)(j + 1) +
+             (((span & (uint64_t)J) * (uint64_t)(j + 1)) >> la);
     };
     while (klo < khi) {
       const uint64_t span = khi - klo;
-      if (hg < J * H) {
-        const int j = hg / H, h = hg % H;
-        const int64_t c = count_head(h, dval(point(klo, span, j)), true);
-        if (sub == 0) cnt_j[hg] = c;
+      for (int gi = hg; gi < J * H; gi += kHeadGroup) {
+        const int j = gi / H, h = gi - j * H;
+        const int64_t c = count_head(h, dval(point(klo, span, j)), true, hg);
+        if (sub == 0) cnt_j[gi] = c;
       }
       __syncthreads();
       int first = J;  // first point whose count reaches R

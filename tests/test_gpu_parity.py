@@ -264,6 +264,25 @@ def test_allocate_from_supplied_curves_matches_oracle():
             assert np.array_equal(got, want), (n_keep, got, want)
 
 
+@pytest.mark.parametrize("H", [5, 16, 40, 64])
+def test_allocate_many_heads_matches_oracle(H):
+    # The repair's threshold search takes 2^k - 1 points per step over the
+    # (point, head) pairs; with more than 32 heads the pairs exceed the
+    # half-waves and are counted in further rounds.  n = 3000 keeps the block
+    # minima of every head in LDS (the fast paths); n = 40000 with 64 heads
+    # does not (the pruned scans and the sequential repair).
+    rng = np.random.default_rng(H)
+    for n in ([3000, 40000] if H == 64 else [3000]):
+        c = np.abs(np.cumsum(rng.standard_normal((H, n)), 1))[:, ::-1]
+        c = np.ascontiguousarray(c * rng.uniform(0.1, 10, (H, 1)), np.float32)
+        spec = ck.ProblemSpec(1, H, 2, 64, 16, [n], torch.bfloat16)
+        t = torch.from_numpy(c).reshape(1, H, n).cuda()
+        for n_keep in [2, 97, n // 3]:
+            got = ck.allocate_curves(spec, t, [n_keep]).cpu().numpy()
+            want, _ = oracle.allocate(c, n_keep)
+            assert np.array_equal(got.reshape(-1), want), (H, n, n_keep, got, want)
+
+
 @pytest.mark.parametrize("layers", [2, 40, 100])
 def test_allocate_workgroup_tree_widths_and_step_counts(layers):
     # The bisection runs on 7, 3 or 1 workgroups per (layer, sequence)
