@@ -80,47 +80,71 @@ __device__ __forceinline__ int half_min_i32(int x) {
   return min((int)r[0], (int)r[1]);
 }
 
-// Lexicographic (f, b) minimum over the 32 lanes of a half-wave.
-__device__ __forceinline__ BestFB half_wave_min(double f, int b) {
-#pragma unroll
-  for (int m = 16; m >= 1; m >>= 1) {
-    const double fo = __shfl_xor(f, m, 64);
-    const int bo = __shfl_xor(b, m, 64);
-    if (lex_less(fo, bo, f, b)) {
-      f = fo;
-      b = bo;
-    }
+// Lexicographic (f, b) minimum reductions, carrying a float c of the winning
+// lane (the order is total on (f, b), so the result does not depend on the
+// pairing).  The exchanges are those of half_min_i32, plus v_permlane32_swap
+// for the whole wave; every lane of the reduced group must be active.
+__device__ __forceinline__ void lex_take(double& f, int& b, float& c, double fo, int bo, float co) {
+  if (lex_less(fo, bo, f, b)) {
+    f = fo;
+    b = bo;
+    c = co;
   }
+}
+
+template <int CTL>
+__device__ __forceinline__ void lex_dpp(double& f, int& b, float& c) {
+  const uint64_t u = (uint64_t)__double_as_longlong(f);
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)u, (int)(uint32_t)u, CTL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(u >> 32), (int)(uint32_t)(u >> 32), CTL,
+                                             0xF, 0xF, false);
+  const int bo = __builtin_amdgcn_update_dpp(b, b, CTL, 0xF, 0xF, false);
+  const int co = __builtin_amdgcn_update_dpp(__float_as_int(c), __float_as_int(c), CTL, 0xF, 0xF, false);
+  const double fo = __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+  lex_take(f, b, c, fo, bo, __int_as_float(co));
+}
+
+// One exchange between the pairs of 16-lane rows of each half (W = 16) or
+// between the halves (W = 32): both candidates arrive in every lane.
+template <int W>
+__device__ __forceinline__ void lex_swap(double& f, int& b, float& c) {
+  const uint64_t u = (uint64_t)__double_as_longlong(f);
+  const uint32_t lo = (uint32_t)u, hi = (uint32_t)(u >> 32);
+  const uint32_t bu = (uint32_t)b, cu = __float_as_uint(c);
+  auto sw = [](uint32_t x) {
+    if constexpr (W == 16)
+      return __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    else
+      return __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  };
+  const auto rl = sw(lo), rh = sw(hi), rb = sw(bu), rc = sw(cu);
+  f = __longlong_as_double((long long)(((uint64_t)rh[0] << 32) | rl[0]));
+  b = (int)rb[0];
+  c = __uint_as_float(rc[0]);
+  lex_take(f, b, c, __longlong_as_double((long long)(((uint64_t)rh[1] << 32) | rl[1])), (int)rb[1],
+           __uint_as_float(rc[1]));
+}
+
+// over `WIDTH` lanes: 32 (each half-wave) or 64 (the wave)
+template <int WIDTH>
+__device__ __forceinline__ void lexmin_fbc(double& f, int& b, float& c) {
+  lex_dpp<0xB1>(f, b, c);   // lane ^ 1
+  lex_dpp<0x4E>(f, b, c);   // lane ^ 2
+  lex_dpp<0x141>(f, b, c);  // mirrored within 8
+  lex_dpp<0x140>(f, b, c);  // mirrored within 16
+  lex_swap<16>(f, b, c);
+  if constexpr (WIDTH == 64) lex_swap<32>(f, b, c);
+}
+
+__device__ __forceinline__ BestFB half_wave_min(double f, int b) {
+  float c = 0.f;
+  lexmin_fbc<32>(f, b, c);
   return BestFB{f, b};
 }
 
-// Lexicographic (f, b) minimum over `width` lanes (32: a half-wave, 64: the
-// wave), carrying the curve value c of the winning position.
-template <int WIDTH>
-__device__ __forceinline__ void lexmin_fbc(double& f, int& b, float& c) {
-#pragma unroll
-  for (int m = WIDTH / 2; m >= 1; m >>= 1) {
-    const double fo = __shfl_xor(f, m, 64);
-    const int bo = __shfl_xor(b, m, 64);
-    const float co = __shfl_xor(c, m, 64);
-    if (lex_less(fo, bo, f, b)) {
-      f = fo;
-      b = bo;
-      c = co;
-    }
-  }
-}
-
 __device__ __forceinline__ BestFB wave_lexmin(double f, int b) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const double fo = __shfl_xor(f, m, 64);
-    const int bo = __shfl_xor(b, m, 64);
-    if (lex_less(fo, bo, f, b)) {
-      f = fo;
-      b = bo;
-    }
-  }
+  float c = 0.f;
+  lexmin_fbc<64>(f, b, c);
   return BestFB{f, b};
 }
 
@@ -421,7 +445,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         const uint64_t m = __ballot(take);
         int slot0 = 0;
         if (lane == 0 && m) slot0 = atomicAdd(&ncand, __popcll(m));
-        slot0 = __shfl(slot0, 0, 64);
+        slot0 = __builtin_amdgcn_readfirstlane(slot0);
         const int slot = slot0 + (int)count_below64(m);
         if (take && slot < kCandCap) cand[slot] = (h << 16) | k;
         __syncthreads();
@@ -521,6 +545,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         double f = INFINITY;
         int bb = 0x7fffffff;
         float cb = 0.f;
+#pragma unroll 4
         for (int k = kfirst + sub; k < nblk; k += 32) {
           const int p = mpos[h * nblk + k];
           if (p >= bmin) {
@@ -568,7 +593,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       const uint64_t m = __ballot(take);
       int slot0 = 0;
       if (lane == 0 && m) slot0 = atomicAdd(&ncand, __popcll(m));
-      slot0 = __shfl(slot0, 0, 64);
+      slot0 = __builtin_amdgcn_readfirstlane(slot0);
       const int slot = slot0 + (int)count_below64(m);
       if (take && slot < kCandCap) cand[slot] = (h << 16) | k;
     }
