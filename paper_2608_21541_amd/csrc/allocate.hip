@@ -759,7 +759,12 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       }
       // group barrier: every member has published this pass.  The arrival
       // releases the workgroup's stores (ordered before it by the barrier);
-      // the wait polls with coherent loads and acquires once at the end.
+      // the wait polls with coherent (agent-scope atomic) loads, and the
+      // published values are read the same way once the count is complete:
+      // the members' stores reached the coherence point before their
+      // arrivals, so no acquire fence is needed.  (An agent-scope acquire
+      // invalidates the compute die's L2, which also holds the curve blocks
+      // that the next evaluation reads again.)
       __syncthreads();
       if (tid == 0) {
         const int target = K * (pass + 1);
@@ -772,7 +777,6 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
             break;
           }
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       }
       __syncthreads();
       if (tid < nl)
