@@ -603,20 +603,21 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       evaluate_rounds(lam, out);
       return;
     }
-    // evaluate: each wave takes runs of 8 consecutive candidates (all loads
-    // of a run in flight); the sweep lists them in (head, block) order, so a
-    // run mostly belongs to one head: lanes keep a running best over the
-    // run's positions and the wave reduces once per head change, recording
-    // the result at that head's last candidate of the run (the others get
-    // +inf)
-    constexpr int QB = 8;
-    for (int c0 = wave * QB; c0 < C; c0 += QB * kAllocWaves) {
+    // evaluate: each wave takes a run of `per` consecutive candidates (up to
+    // 10, the most whose loads fit in flight in the registers), the
+    // candidates spread evenly over the waves; the sweep lists them in (head, block) order, so a run
+    // mostly belongs to one head: lanes keep a running best over the run's
+    // positions and the wave reduces once per head change, recording the
+    // result at that head's last candidate of the run (the others get +inf)
+    constexpr int QB = 10;
+    const int per = min(QB, (C + kAllocWaves - 1) / kAllocWaves);
+    for (int c0 = wave * per; c0 < C; c0 += per * kAllocWaves) {
       float cv[QB][kBlk / 64];
       int it[QB];
 #pragma unroll
       for (int q = 0; q < QB; ++q) {
         const int c = c0 + q;
-        it[q] = c < C ? cand[c] : -1;
+        it[q] = (q < per && c < C) ? cand[c] : -1;
         const int hq = it[q] < 0 ? 0 : (it[q] >> 16), kq = it[q] < 0 ? 0 : (it[q] & 0xffff);
         const float* ch = curves + lht_base(g, l, hq, tok0);
 #pragma unroll
