@@ -56,6 +56,17 @@ def test_c2_full_length():
     check_block_stages(spec, cfg, cache, out, 0, 0, log=log)
 
 
+@pytest.mark.parametrize("heads", [40, 64])
+def test_many_kv_heads_full_pass(heads):
+    # Multi-head attention shapes (no grouping) with more KV heads than the
+    # allocator's 32 half-waves: the repair search counts its (point, head)
+    # pairs in two rounds.  Every stage of the block against the oracle.
+    cfg = synth.CacheConfig("MHA", 1, heads, 1, 64, 16, [3001], 0.10, torch.bfloat16, 11)
+    cache = synth.make_cache(cfg, "cpu")
+    spec, out, _, _ = run_gpu(cfg, cache)
+    check_block_stages(spec, cfg, cache, out, 0, 0, log=log)
+
+
 def test_c4_ragged_batch_two_layers():
     # ragged batch with two layers: per-sequence offsets and budgets
     cfg = synth.config("C4", seqlens=[3000, 8192 + 5, 1024, 4500], layers=2)
