@@ -4,10 +4,10 @@
 //
 // Bisection.  Each step needs, per head, the smallest b in [b_min, n-1]
 // minimizing f(b) = fma(lambda, b, c(b)) in fp64 on the fp32 curve.  The scan
-// is pruned exactly: for a block of 256 ranks starting at b0 (clamped to
-// b_min) with block minimum cmin, every candidate has lambda*b + c(b) >=
-// lambda*b0 + cmin, and round-to-nearest is monotone, so LB = fma(lambda, b0,
-// cmin) <= f(b) on the block.  The block with the smallest bound is evaluated
+// is pruned exactly: for a run of ranks starting at b0 (clamped to b_min)
+// with minimum cmin, every candidate has lambda*b + c(b) >= lambda*b0 + cmin,
+// and round-to-nearest is monotone, so LB = fma(lambda, b0, cmin) <= f(b) on
+// the run (the runs are the two 128-rank halves of each 256-rank block).  The block with the smallest bound is evaluated
 // first (32 threads per head); every block whose (LB, b0) undercuts the best
 // (f*, b*) lexicographically is then put on a candidate list and evaluated
 // by the whole workgroup, one coalesced 256-wide row per block.  Blocks left
@@ -78,6 +78,16 @@ __device__ __forceinline__ int half_min_i32(int x) {
   x = min(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));
   const auto r = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
   return min((int)r[0], (int)r[1]);
+}
+
+// The same minimum for floats (no NaN among the values).
+__device__ __forceinline__ float half_min_f32(float x) {
+  x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+  x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0x4E, 0xF, 0xF, false)));
+  x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0x141, 0xF, 0xF, false)));
+  x = fminf(x, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0x140, 0xF, 0xF, false)));
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fminf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // Lexicographic (f, b) minimum reductions, carrying a float c of the winning
@@ -158,10 +168,11 @@ __device__ __forceinline__ double dval(uint64_t k) {
   return __longlong_as_double((long long)u);
 }
 
-// Per-block statistics of the curves: minimum and maximum of c over each
-// 256-rank block, the smallest position holding the minimum, and the maximum
-// marginal d(i) = c(i+1) - c(i) (fp64) over the i of the block with
-// i <= n-2.  One wave per block.
+// Per-block statistics of the curves: minimum of c over each 128-rank half of
+// each 256-rank block (+inf where a half is past the end), maximum of c over
+// the block, the smallest position holding the block minimum, and the
+// maximum marginal d(i) = c(i+1) - c(i) (fp64) over the i of the block with
+// i <= n-2.  One wave per block; lanes 0-31 hold the first half.
 __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st, int32_t nblk_max,
                                                                const float* __restrict__ curves,
                                                                float* __restrict__ cmin,
@@ -200,6 +211,7 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
     }
     if (i0 + e <= n - 2) dm = fmax(dm, (double)c[e + 1] - (double)c[e]);
   }
+  const float mhalf = half_min_f32(mn);
   // (min c, smallest position) over the wave
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -212,8 +224,8 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
   }
   mx = wave_max(mx);
   dm = wave_max(dm);
+  if ((lane & 31) == 0) cmin[(u * nblk_max + k) * 2 + (lane >> 5)] = mhalf;
   if (lane == 0) {
-    cmin[u * nblk_max + k] = mn;
     cmaxb[u * nblk_max + k] = mx;
     cpos[u * nblk_max + k] = pmn;
     dmax[u * nblk_max + k] = dm;
@@ -230,12 +242,12 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     const float* __restrict__ cmaxb, const int32_t* __restrict__ cpos,
     const double* __restrict__ dmax, int32_t nblk_max, int32_t steps,
     int32_t* __restrict__ budgets, int64_t* __restrict__ stats, int32_t K, int32_t* sync) {
-  // 64 KB of LDS: block minima + candidate lists during the bisection, the
+  // 64 KB of LDS: the half-block minima during the bisection, the
   // block-level running maxima of the marginals during the repair.
   __shared__ __align__(16) unsigned char pool[kLdsItems * 8];
-  float* mcache = reinterpret_cast<float*>(pool);
-  int32_t* cand = reinterpret_cast<int32_t*>(pool + kLdsItems * 4);
+  float2* mcache = reinterpret_cast<float2*>(pool);  // half-block minima
   double* pbm = reinterpret_cast<double*>(pool);
+  __shared__ int32_t cand[kCandCap];
   __shared__ double fbest[64];
   __shared__ int32_t bbest[64], kstar[64];
   __shared__ float cbest[64], cprev[64];  // curve values at bbest and bprev
@@ -306,7 +318,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   if (fast) {
     for (int i = tid; i < H * nblk; i += kAllocThreads) {
       const int h = i / nblk, k = i % nblk;
-      mcache[i] = cmin[unit_index(g, l, b, h) * nblk_max + k];
+      mcache[i] = reinterpret_cast<const float2*>(cmin)[unit_index(g, l, b, h) * nblk_max + k];
       mpos[i] = cpos[unit_index(g, l, b, h) * nblk_max + k];
     }
   }
@@ -315,8 +327,21 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   for (int w = 0; w < kAllocWaves; ++w) cm = fmax(cm, redf[w]);
   double lo = 0.0, hi = 2.0 * cm + 1.0;
 
+  // minimum of c over block k of head h
   auto mh_at = [&](int h, int k) -> float {
-    return fast ? mcache[h * nblk + k] : cmin[unit_index(g, l, b, h) * nblk_max + k];
+    const float2 m = fast ? mcache[h * nblk + k]
+                          : reinterpret_cast<const float2*>(cmin)[unit_index(g, l, b, h) * nblk_max + k];
+    return fminf(m.x, m.y);
+  };
+  // Whether block k of head h (LDS item i) may hold a point undercutting the
+  // head's best (f*, b*): per half, every point b of it has (f(b), b) >=
+  // (fma(lam, b0, min c), b0) lexicographically.
+  auto undercuts = [&](int i, int h, int k, double lam) -> bool {
+    const float2 m = mcache[i];
+    const int b0a = max(k * kBlk, bmin), b0b = max(k * kBlk + kBlk / 2, bmin);
+    const bool a = k * kBlk + kBlk / 2 - 1 >= bmin &&
+                   lex_less(fma(lam, (double)b0a, (double)m.x), b0a, fbest[h], bbest[h]);
+    return a || lex_less(fma(lam, (double)b0b, (double)m.y), b0b, fbest[h], bbest[h]);
   };
 
   // Per head, the block with the smallest bound fma(lambda, b0, min c) is
@@ -436,11 +461,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         if (i < nitems) {
           h = i / nblk;
           k = i - h * nblk;
-          if (k >= kfirst && k != kstar[h]) {
-            const int b0 = max(k * kBlk, bmin);
-            const double lb = fma(lam, (double)b0, (double)mcache[i]);
-            take = lex_less(lb, b0, fbest[h], bbest[h]);
-          }
+          if (k >= kfirst && k != kstar[h]) take = undercuts(i, h, k, lam);
         }
         const uint64_t m = __ballot(take);
         int slot0 = 0;
@@ -549,7 +570,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         for (int k = kfirst + sub; k < nblk; k += 32) {
           const int p = mpos[h * nblk + k];
           if (p >= bmin) {
-            const float cv = mcache[h * nblk + k];
+            const float cv = fminf(mcache[h * nblk + k].x, mcache[h * nblk + k].y);
             const double v = fma(lam, (double)p, (double)cv);
             if (lex_less(v, p, f, bb)) {
               f = v;
@@ -584,11 +605,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       if (i < nitems) {
         h = i / nblk;
         k = i - h * nblk;
-        if (k >= kfirst) {
-          const int b0 = max(k * kBlk, bmin);
-          const double lb = fma(lam, (double)b0, (double)mcache[i]);
-          take = lex_less(lb, b0, fbest[h], bbest[h]);
-        }
+        if (k >= kfirst) take = undercuts(i, h, k, lam);
       }
       const uint64_t m = __ballot(take);
       int slot0 = 0;
@@ -604,12 +621,12 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       return;
     }
     // evaluate: each wave takes a run of `per` consecutive candidates (up to
-    // 10, the most whose loads fit in flight in the registers), the
+    // 9, the most whose loads fit in flight in the registers), the
     // candidates spread evenly over the waves; the sweep lists them in (head, block) order, so a run
     // mostly belongs to one head: lanes keep a running best over the run's
     // positions and the wave reduces once per head change, recording the
     // result at that head's last candidate of the run (the others get +inf)
-    constexpr int QB = 10;
+    constexpr int QB = 9;
     const int per = min(QB, (C + kAllocWaves - 1) / kAllocWaves);
     for (int c0 = wave * per; c0 < C; c0 += per * kAllocWaves) {
       float cv[QB][kBlk / 64];

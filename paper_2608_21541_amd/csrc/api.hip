@@ -280,7 +280,7 @@ static size_t layout(const Plan& P, uint32_t need, void* ws, Bufs* b) {
   if (need & NEED_PERM) b->perm = w.take<int32_t>(LHT);
   if (need & NEED_CURVEBUF) b->curves = w.take<float>(LHT);
   if (need & (NEED_CURVES | NEED_MINMAX)) {
-    b->cmin = w.take<float>((size_t)P.U * P.nblk_max);
+    b->cmin = w.take<float>((size_t)P.U * P.nblk_max * 2);
     b->cmaxb = w.take<float>((size_t)P.U * P.nblk_max);
     b->cpos = w.take<int32_t>((size_t)P.U * P.nblk_max);
     b->dmax = w.take<double>((size_t)P.U * P.nblk_max);

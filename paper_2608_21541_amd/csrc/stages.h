@@ -56,7 +56,7 @@ certkv_status run_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s);
 struct AllocArgs {
   Geo g;
   const float* curves;
-  float* cmin;      // [U][nblk_max] block minima of c
+  float* cmin;      // [U][nblk_max][2] minima of c over the two halves of each block
   float* cmaxb;     // [U][nblk_max] block maxima of c
   int32_t* cpos;    // [U][nblk_max] smallest position of the block minimum
   double* dmax;     // [U][nblk_max] block maxima of c(i+1) - c(i)
