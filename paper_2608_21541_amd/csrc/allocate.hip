@@ -262,7 +262,8 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
   int32_t* mpos = reinterpret_cast<int32_t*>(aux);
   float* rcache = reinterpret_cast<float*>(aux);
   float(*win)[kRepairWin + 1] = reinterpret_cast<float(*)[kRepairWin + 1]>(aux);
-  __shared__ int32_t rkey[kHeadGroup];  // (head << 16) | block of each cached block (-1: none)
+  __shared__ int32_t rkey[kHeadGroup];
+  __shared__ int32_t sfirst;  // (head << 16) | block of each cached block (-1: none)
   __shared__ float cres_c[kCandCap];
   __shared__ int32_t bcur[64], bhi[64];
   __shared__ double redf[kAllocWaves];
@@ -984,13 +985,17 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         if (sub == 0) cnt_j[gi] = c;
       }
       __syncthreads();
-      int first = J;  // first point whose count reaches R
-      for (int j = J - 1; j >= 0; --j) {
+      // first point whose count reaches R (the counts grow with the point):
+      // lane j of wave 0 totals point j over the heads
+      if (wave == 0) {
         int64_t c = 0;
-        for (int h = 0; h < H; ++h) c += cnt_j[j * H + h];
-        if (c >= R) first = j;
+        if (lane < J)
+          for (int h = 0; h < H; ++h) c += cnt_j[lane * H + h];
+        const uint64_t reach = __ballot(lane < J && c >= R);
+        if (lane == 0) sfirst = reach ? (int)__builtin_ctzll(reach) : J;
       }
       __syncthreads();
+      const int first = sfirst;
       if (first < J) {
         const uint64_t nlo = first > 0 ? point(klo, span, first - 1) + 1 : klo;
         khi = point(klo, span, first);
