@@ -41,8 +41,9 @@ constexpr int kRcStride = kBlk + 4;  // a cached curve block of the repair searc
 constexpr int kTreeLev = 3;
 constexpr int kTreeMax = (1 << kTreeLev) - 1;
 constexpr int kSyncGroups = 256;   // (layer, sequence) groups of one such launch at most
-// sync words: ticket, pad, one arrival counter per group, then per group and
-// pass parity the nodes' budget sums (int64) and argmin vectors (64 heads)
+// sync words: ticket, pad, one word per group (unused), then per group and
+// pass parity the nodes' budget sums tagged with their pass ((pass + 1) << 48
+// | sum, int64) and argmin vectors (64 heads)
 constexpr size_t kSyncCnt = 2 + kSyncGroups;
 constexpr size_t kSyncSum = kSyncCnt;
 constexpr size_t kSyncArg = kSyncSum + (size_t)kSyncGroups * 2 * kTreeMax * 2;
@@ -745,7 +746,6 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     const int lev_max = 31 - __clz(K + 1);
     int64_t* xsum = reinterpret_cast<int64_t*>(sync + kSyncSum) + (size_t)grp * 2 * kTreeMax;
     int32_t* xarg = sync + kSyncArg + (size_t)grp * 2 * kTreeMax * 64;
-    int32_t* cnt = sync + 2 + grp;
     int t = 0, pass = 0;
     while (t < steps) {
       const int lv = min(lev_max, steps - t);
@@ -767,40 +767,43 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
       __syncthreads();
       if (node < nl) {
         evaluate(tlam[node], bcur);
-        int64_t sum = 0;
-        for (int h = 0; h < H; ++h) sum += bcur[h];
-        if (tid == 0)
-          __hip_atomic_store(&xsum[par * kTreeMax + node], sum, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
         if (tid < H)
           __hip_atomic_store(&xarg[(par * kTreeMax + node) * 64 + tid], bcur[tid],
                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      // group barrier: every member has published this pass.  The arrival
-      // releases the workgroup's stores (ordered before it by the barrier);
-      // the wait polls with coherent (agent-scope atomic) loads, and the
-      // published values are read the same way once the count is complete:
-      // the members' stores reached the coherence point before their
-      // arrivals, so no acquire fence is needed.  (An agent-scope acquire
-      // invalidates the compute die's L2, which also holds the curve blocks
-      // that the next evaluation reads again.)
+      // Exchange.  Each evaluating node publishes its budget sum tagged with
+      // the pass, released after its argmins (ordered before it by the
+      // barrier); lanes 0..nl-1 of wave 0 poll one node's slot each with
+      // coherent (agent-scope atomic) loads until every tag shows this pass,
+      // and so hold the sums when the wait ends.  No acquire fence is needed
+      // (the argmins are read with the same loads; an agent-scope acquire
+      // would also invalidate the compute die's L2, which holds the curve
+      // blocks the next evaluation rereads).  Slots alternate by pass parity:
+      // a node publishes pass p + 2 only after it has seen every node's pass
+      // p + 1, which each node publishes after reading pass p.
       __syncthreads();
-      if (tid == 0) {
-        const int target = K * (pass + 1);
-        __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      if (node < nl && tid == 0) {
+        int64_t sum = 0;
+        for (int h = 0; h < H; ++h) sum += bcur[h];
+        __hip_atomic_store(&xsum[par * kTreeMax + node], ((int64_t)(pass + 1) << 48) | sum,
+                           __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (wave == 0) {
+        int64_t v = 0;
         int spins = 0;
-        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        while (true) {
+          if (lane < nl)
+            v = __hip_atomic_load(&xsum[par * kTreeMax + lane], __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+          if (__ballot(lane < nl && (v >> 48) != (int64_t)(pass + 1)) == 0) break;
           __builtin_amdgcn_s_sleep(1);
-          if (++spins > (1 << 22)) {  // a member never arrived: give up, report
-            if (g.status) *g.status = CERTKV_EHIP;
+          if (++spins > (1 << 22)) {  // a member never published: give up, report
+            if (lane == 0 && g.status) *g.status = CERTKV_EHIP;
             break;
           }
         }
+        if (lane < nl) tsum[lane] = v & (((int64_t)1 << 48) - 1);
       }
-      __syncthreads();
-      if (tid < nl)
-        tsum[tid] = __hip_atomic_load(&xsum[par * kTreeMax + tid], __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
       __syncthreads();
       int nd = 0, last = -1;
       for (int j = 0; j < lv; ++j) {
@@ -1075,8 +1078,9 @@ certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) 
     K = 7 * groups <= cus ? 7 : 3 * groups <= cus ? 3 : 1;
   }
   if (K > 1) {
-    CERTKV_LAUNCH("alloc_sync_clear", alloc_sync_clear_kernel, dim3((unsigned)((kSyncCnt + 255) / 256)),
-                  dim3(256), 0, s, a.sync, (int)kSyncCnt);
+    // the ticket and the tagged sums start at zero
+    CERTKV_LAUNCH("alloc_sync_clear", alloc_sync_clear_kernel, dim3((unsigned)((kSyncArg + 255) / 256)),
+                  dim3(256), 0, s, a.sync, (int)kSyncArg);
     CERTKV_LAUNCH("allocate", allocate_kernel, dim3((unsigned)(K * groups)), dim3(kAllocThreads), 0,
                   s, a.g, st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb,
                   (const int32_t*)a.cpos, (const double*)a.dmax, a.nblk_max, a.steps, a.budgets,
