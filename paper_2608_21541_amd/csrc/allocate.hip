@@ -747,6 +747,10 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     int64_t* xsum = reinterpret_cast<int64_t*>(sync + kSyncSum) + (size_t)grp * 2 * kTreeMax;
     int32_t* xarg = sync + kSyncArg + (size_t)grp * 2 * kTreeMax * 64;
     int t = 0, pass = 0;
+    // node 0: the argmins of the last node whose sum lowered lambda_hi, kept
+    // in flight in registers while the next pass evaluates (the release of
+    // the next publication waits for them) and stored once after the loop
+    int32_t arg_hi = 0;
     while (t < steps) {
       const int lv = min(lev_max, steps - t);
       const int nl = (1 << lv) - 1;
@@ -817,14 +821,16 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         }
       }
       if (node == 0 && last >= 0 && tid < H)
-        bhi[tid] = __hip_atomic_load(&xarg[(par * kTreeMax + last) * 64 + tid], __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
+        arg_hi = __hip_atomic_load(&xarg[(par * kTreeMax + last) * 64 + tid], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
       have_bhi = have_bhi || last >= 0;
-      __syncthreads();
+      __syncthreads();  // every thread has walked the tree before tid 0 rebuilds it
       t += lv;
       ++pass;
     }
     if (node != 0) return;
+    if (have_bhi && tid < H) bhi[tid] = arg_hi;
+    __syncthreads();
     if (!have_bhi) evaluate(hi, bhi);
   }
   const uint64_t t_bisect = wall_clock64();
