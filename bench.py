@@ -14,6 +14,7 @@ workload.
 """
 import argparse
 import json
+import statistics
 import math
 import os
 import sys
@@ -176,22 +177,28 @@ def run_metadata(cfg, dev):
             "cus": props.multi_processor_count, **clocks}
 
 
-def time_passes(run, steps, stream, profile):
+def time_passes(run, steps, stream, profile, per_step=None):
     """Average milliseconds of `steps` calls of run(), timed with events on the
     launch stream; with profile the library brackets every launch with events
-    and the per-kernel averages are returned too."""
+    and the per-kernel averages are returned too.  With a list `per_step`,
+    an event at every step boundary (one per step, on the same stream) adds
+    each step's time to it."""
     import torch
     import paper_2608_21541_amd as ck
     torch.cuda.synchronize()
     if profile:
         ck.profile_reset()
         ck.profile_enable(True)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1 if per_step is not None else 2)]
+    ev[0].record(stream)
+    for i in range(steps):
         run()
-    end.record(stream)
+        if per_step is not None:
+            ev[i + 1].record(stream)
+    ev[-1].record(stream)
     torch.cuda.synchronize()
+    if per_step is not None:
+        per_step.extend(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
     kernels = None
     if profile:
         prof = ck.profile_read()
@@ -199,7 +206,26 @@ def time_passes(run, steps, stream, profile):
         ck.profile_reset()
         kernels = {name: {"launches_per_step": cnt / steps, "avg_ms": tot / max(cnt, 1)}
                    for name, (cnt, tot) in prof.items()}
-    return start.elapsed_time(end) / steps, kernels
+    return ev[0].elapsed_time(ev[-1]) / steps, kernels
+
+
+def copy_bandwidth(dev, nbytes=1 << 30, reps=5):
+    """GB/s of a plain device-to-device copy (bytes read + bytes written per
+    second), the practical ceiling a streaming kernel is compared with."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    gbps = 2.0 * nbytes * reps / (a.elapsed_time(b) / 1e3) / 1e9
+    del src, dst
+    return gbps
 
 
 def cpu_baseline(cache, cfg, n_keep, log, layers=6):
@@ -596,8 +622,10 @@ def main():
     # Timed region: the plain pass, no profiling events.  A second run of the
     # same steps with every launch bracketed by HIP events on its stream gives
     # the per-kernel durations (and the events' overhead on the pass).
-    ms, _ = time_passes(run, args.steps, stream, profile=False)
+    steps_ms = []
+    ms, _ = time_passes(run, args.steps, stream, profile=False, per_step=steps_ms)
     ms_prof, kernels = time_passes(run, args.steps, stream, profile=True)
+    copy_gbps = copy_bandwidth(dev)
     tokens = sum(cfg.seqlens)
     # KV tokens compressed per second per layer: n / (T_pass / L)
     value = tokens / (ms / 1e3 / cfg.layers)
@@ -674,6 +702,10 @@ def main():
         "pass_alg_bytes": pass_bytes,
         "pass_alg_GBps": pass_bytes / (ms / 1e3) / 1e9,
         "pass_alg_frac_hbm": pass_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "ms_median": statistics.median(steps_ms),
+        "ms_min": min(steps_ms),
+        "copy_GBps": copy_gbps,
+        "pass_alg_frac_copy": pass_bytes / (ms / 1e3) / 1e9 / copy_gbps,
         "roofline": roof,
         "kernels": kernels,
         "ms_per_step_with_kernel_events": ms_prof,
