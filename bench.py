@@ -243,8 +243,14 @@ def cpu_baseline(cache, cfg, n_keep, log, layers=6):
         t0 = time.perf_counter()
         oracle.compress_block(q, k, v, n_keep[0], 1.0 / math.sqrt(cfg.head_dim))
         dt += time.perf_counter() - t0
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": n / (dt / layers), "unit": "KV tokens/s per layer",
-            "cores": oracle.num_threads(), "kind": "oracle",
+            "cores": oracle.num_threads(), "cpu_model": cpu_model, "kind": "oracle",
             "sample": f"layers 0-{layers - 1} of the workload: {cfg.kv_heads} KV heads x {n} tokens "
                       f"each, full pass (score, order, curves, allocation, selection, tail), "
                       f"{dt:.1f} s of oracle time"}
