@@ -107,17 +107,20 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int64_t off = kept_offsets[u];
   int64_t run = 0;
   double se = 0.0, sa = 0.0;
+  // Positions past the end read the last score (clamped, so no branch sits
+  // around the loads and the next step's loads stay in flight while this
+  // step is tested); they are masked where used.
   auto load = [&](int j0, float (&sv)[kSelPer]) {
 #pragma unroll
     for (int r = 0; r < kSelPer; ++r) {
       const int j = j0 + kSelPer * threadIdx.x + r;
-      sv[r] = j < n ? scores[base + j] : 0.f;
+      sv[r] = scores[base + min(j, n - 1)];
     }
   };
   float cur[kSelPer], nxt[kSelPer];
-  load(0, cur);
+  if (n > 0) load(0, cur);  // (an empty segment reads nothing)
   for (int j0 = 0, it = 0; j0 < n; j0 += kSelTile, ++it) {
-    if (j0 + kSelTile < n) load(j0 + kSelTile, nxt);
+    load(j0 + kSelTile, nxt);
     const int jt = j0 + kSelPer * threadIdx.x;
     bool keep[kSelPer];
     uint64_t bal[kSelPer];
@@ -131,11 +134,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       // are kept up to the threshold pair at rank bb-1
       keep[r] = valid && (j >= wkeep ? (j - wkeep < bb)
                                      : (bb > g.keep_w && (key < kthr || (key == kthr && j <= ithr))));
-      if (valid) {
-        const double sp = cur[r] > 0.f ? (double)cur[r] : 0.0;
-        sa += sp;
-        if (!keep[r]) se += sp;
-      }
+      const double sp = (valid && cur[r] > 0.f) ? (double)cur[r] : 0.0;
+      sa += sp;
+      se += keep[r] ? 0.0 : sp;
       bal[r] = __ballot(keep[r]);
       below += __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[r] >> 32),
                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal[r], 0u));
