@@ -24,6 +24,8 @@
 // sum b_h: a bisection over the ordered bit patterns of fp64 keys finds it,
 // counting per head with block-level running maxima (LDS) and one scan of the
 // block where the running maximum crosses the threshold.
+#include <type_traits>
+
 #include "stages.h"
 
 namespace certkv {
@@ -173,14 +175,43 @@ __device__ __forceinline__ double dval(uint64_t k) {
 // each 256-rank block (+inf where a half is past the end), maximum of c over
 // the block, the smallest position holding the block minimum, and the
 // maximum marginal d(i) = c(i+1) - c(i) (fp64) over the i of the block with
-// i <= n-2.  One wave per block; lanes 0-31 hold the first half.
+// i <= n-2.  One wave per kBsBlocks consecutive blocks, the loads of all of
+// them in flight at once (positions clamped into the segment, masked where
+// used); lane L covers positions 4L..4L+3 of a block (lanes 0-31 the first
+// half), and the wave reductions are DPP and lane-row exchanges.
+constexpr int kBsBlocks = 8;
+
+template <typename T, typename F>
+__device__ __forceinline__ T wave_reduce_dpp(T x, F op) {
+  static_assert(sizeof(T) == 4, "32-bit values");
+  auto dpp = [&](auto ctl) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, x), __builtin_bit_cast(int, x),
+                                                             decltype(ctl)::value, 0xF, 0xF, false));
+  };
+  x = op(x, dpp(std::integral_constant<int, 0xB1>()));
+  x = op(x, dpp(std::integral_constant<int, 0x4E>()));
+  x = op(x, dpp(std::integral_constant<int, 0x141>()));
+  x = op(x, dpp(std::integral_constant<int, 0x140>()));
+  // (the swap results are read into scalars before the bit casts: a bit cast
+  // applied to a subscripted element of the result vector compiled to the
+  // first element for both subscripts)
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const uint32_t a0 = r16[0], a1 = r16[1];
+  x = op(__builtin_bit_cast(T, a0), __builtin_bit_cast(T, a1));
+  const uint32_t v = __builtin_bit_cast(uint32_t, x);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  const uint32_t b0 = r32[0], b1 = r32[1];
+  return op(__builtin_bit_cast(T, b0), __builtin_bit_cast(T, b1));
+}
+
 __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st, int32_t nblk_max,
                                                                const float* __restrict__ curves,
                                                                float* __restrict__ cmin,
                                                                float* __restrict__ cmaxb,
                                                                int32_t* __restrict__ cpos,
                                                                double* __restrict__ dmax) {
-  const int per_unit = (nblk_max + 3) / 4;
+  const int per_unit = (nblk_max + 4 * kBsBlocks - 1) / (4 * kBsBlocks);
   const int wb = blockIdx.x % per_unit;
   const int hb = blockIdx.x / per_unit;
   const int h = hb % g.H;
@@ -190,46 +221,49 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
   const int n = st.len[bl];
   const int nblk = (n + kBlk - 1) / kBlk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int k = wb * 4 + wave;
-  if (k >= nblk) return;
+  const int k0 = (wb * 4 + wave) * kBsBlocks;
+  if (k0 >= nblk) return;
   const int64_t u = unit_index(g, l, st.first + bl, h);
   const float* ch = curves + lht_base(g, l, h, st.start[bl]);
-  const int i0 = k * kBlk + lane * 4;
-  float c[5];
+  float c[kBsBlocks][5];
 #pragma unroll
-  for (int e = 0; e < 5; ++e) c[e] = (i0 + e < n) ? ch[i0 + e] : 0.f;
-  float mn = INFINITY, mx = -INFINITY;
-  int pmn = 0x7fffffff;
-  double dm = -INFINITY;
+  for (int j = 0; j < kBsBlocks; ++j) {
+    const int i0 = (k0 + j) * kBlk + lane * 4;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    if (i0 + e < n) {
-      if (c[e] < mn) {
-        mn = c[e];
-        pmn = i0 + e;
+    for (int e = 0; e < 5; ++e) c[j][e] = ch[min(i0 + e, n - 1)];
+  }
+#pragma unroll
+  for (int j = 0; j < kBsBlocks; ++j) {
+    const int k = k0 + j;
+    if (k >= nblk) break;
+    const int i0 = k * kBlk + lane * 4;
+    float mn = INFINITY, mx = -INFINITY;
+    int pmn = 0x7fffffff;
+    double dm = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (i0 + e < n) {
+        if (c[j][e] < mn) {
+          mn = c[j][e];
+          pmn = i0 + e;
+        }
+        mx = fmaxf(mx, c[j][e]);
       }
-      mx = fmaxf(mx, c[e]);
+      if (i0 + e <= n - 2) dm = fmax(dm, (double)c[j][e + 1] - (double)c[j][e]);
     }
-    if (i0 + e <= n - 2) dm = fmax(dm, (double)c[e + 1] - (double)c[e]);
-  }
-  const float mhalf = half_min_f32(mn);
-  // (min c, smallest position) over the wave
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const float mo = __shfl_xor(mn, m, 64);
-    const int po = __shfl_xor(pmn, m, 64);
-    if (mo < mn || (mo == mn && po < pmn)) {
-      mn = mo;
-      pmn = po;
+    const float mhalf = half_min_f32(mn);
+    // (min c, smallest position): the lexicographic minimum of (c, position)
+    // (min c, smallest position): the smallest position holding the minimum
+    const float mnw = wave_reduce_dpp(mn, [](float a, float b) { return fminf(a, b); });
+    const int pw = wave_reduce_dpp(mn == mnw ? pmn : 0x7fffffff, [](int a, int b) { return min(a, b); });
+    mx = wave_reduce_dpp(mx, [](float a, float b) { return fmaxf(a, b); });
+    dm = wave_max(dm);
+    if ((lane & 31) == 0) cmin[(u * nblk_max + k) * 2 + (lane >> 5)] = mhalf;
+    if (lane == 0) {
+      cmaxb[u * nblk_max + k] = mx;
+      cpos[u * nblk_max + k] = pw;
+      dmax[u * nblk_max + k] = dm;
     }
-  }
-  mx = wave_max(mx);
-  dm = wave_max(dm);
-  if ((lane & 31) == 0) cmin[(u * nblk_max + k) * 2 + (lane >> 5)] = mhalf;
-  if (lane == 0) {
-    cmaxb[u * nblk_max + k] = mx;
-    cpos[u * nblk_max + k] = pmn;
-    dmax[u * nblk_max + k] = dm;
   }
 }
 
@@ -1069,7 +1103,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
 }
 
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) {
-  const int per_unit = (a.nblk_max + 3) / 4;
+  const int per_unit = (a.nblk_max + 4 * kBsBlocks - 1) / (4 * kBsBlocks);
   CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
                 dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.cpos, a.dmax);
   // Workgroups per (layer, sequence): a node tree of 3 or 7 when every group
