@@ -210,7 +210,12 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
                                                                float* __restrict__ cmin,
                                                                float* __restrict__ cmaxb,
                                                                int32_t* __restrict__ cpos,
-                                                               double* __restrict__ dmax) {
+                                                               double* __restrict__ dmax,
+                                                               int32_t* __restrict__ sync, int32_t nsync) {
+  // the allocation's exchange words (ticket, tagged sums) start at zero: the
+  // first workgroup clears them for the allocation kernel launched next
+  if (sync && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < nsync; i += 256) sync[i] = 0;
   const int per_unit = (nblk_max + 4 * kBsBlocks - 1) / (4 * kBsBlocks);
   const int wb = blockIdx.x % per_unit;
   const int hb = blockIdx.x / per_unit;
@@ -265,11 +270,6 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
       dmax[u * nblk_max + k] = dm;
     }
   }
-}
-
-__global__ void alloc_sync_clear_kernel(int32_t* sync, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) sync[i] = 0;
 }
 
 __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
@@ -1103,9 +1103,6 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
 }
 
 certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) {
-  const int per_unit = (a.nblk_max + 4 * kBsBlocks - 1) / (4 * kBsBlocks);
-  CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
-                dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.cpos, a.dmax);
   // Workgroups per (layer, sequence): a node tree of 3 or 7 when every group
   // of the launch then still has a compute unit per workgroup (one
   // allocation workgroup fills a compute unit's LDS), else 1.
@@ -1117,10 +1114,11 @@ certkv_status run_allocate(const AllocArgs& a, const SeqTab& st, hipStream_t s) 
     const int cus = device_cus(dev);
     K = 7 * groups <= cus ? 7 : 3 * groups <= cus ? 3 : 1;
   }
+  const int per_unit = (a.nblk_max + 4 * kBsBlocks - 1) / (4 * kBsBlocks);
+  CERTKV_LAUNCH("curve_blockstats", curve_blockstats_kernel, dim3(a.g.H * st.count * per_unit, a.g.L),
+                dim3(256), 0, s, a.g, st, a.nblk_max, a.curves, a.cmin, a.cmaxb, a.cpos, a.dmax,
+                K > 1 ? a.sync : (int32_t*)nullptr, (int32_t)kSyncArg);
   if (K > 1) {
-    // the ticket and the tagged sums start at zero
-    CERTKV_LAUNCH("alloc_sync_clear", alloc_sync_clear_kernel, dim3((unsigned)((kSyncArg + 255) / 256)),
-                  dim3(256), 0, s, a.sync, (int)kSyncArg);
     CERTKV_LAUNCH("allocate", allocate_kernel, dim3((unsigned)(K * groups)), dim3(kAllocThreads), 0,
                   s, a.g, st, a.curves, (const float*)a.cmin, (const float*)a.cmaxb,
                   (const int32_t*)a.cpos, (const double*)a.dmax, a.nblk_max, a.steps, a.budgets,

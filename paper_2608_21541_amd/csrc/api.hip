@@ -429,7 +429,7 @@ static certkv_status do_select(const Plan& P, const float* scores, const uint32_
   for (const SeqTab& t : tabs) {
     if (mode == CERTKV_SELECT_COVERAGE)
       TRY(run_coverage(P.g, t, scores, sorted_keys, retain, budgets, s));
-    else
+    else if (!fused)  // the pass's own budgets lie in [b_min, n - 1] already
       TRY(run_clamp(P.g, t, budgets, s));
   }
   TRY(run_offsets(P.U, P.g.slot, budgets, kept_offsets, packed_offsets, s));
