@@ -249,6 +249,7 @@ __global__ __launch_bounds__(kTailThreads) void tail_finalize_kernel(
       nE = (double)(n - nk);
     } else {
       S_all = S_E = nE = 0.0;
+#pragma unroll 8
       for (int sp = 0; sp < nsplit; ++sp) {
         S_all += mpart[(u * nsplit + sp) * 3 + 0];
         S_E += mpart[(u * nsplit + sp) * 3 + 1];
@@ -264,6 +265,9 @@ __global__ __launch_bounds__(kTailThreads) void tail_finalize_kernel(
     if (!direct) {
       for (int d = tid; d < D; d += kTailThreads) {
         double sk = 0.0, sv = 0.0;
+        // partials added in split order; unrolled so that the loads of 16
+        // splits are in flight together
+#pragma unroll 16
         for (int sp = 0; sp < nsplit; ++sp) {
           sk += kpart[((u * nsplit + sp) * 2 + 0) * D + d];
           sv += kpart[((u * nsplit + sp) * 2 + 1) * D + d];
