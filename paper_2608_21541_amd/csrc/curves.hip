@@ -16,14 +16,17 @@
 //   phase 2  the half-wave walks its ranks top-down extending m, W and its
 //            lane parts q; per rank each lane forms m q - |W|^2 over its dims
 //            and a transpose-reduce over the 32 lanes, folded in as the ranks
-//            are produced, yields c^2 of all 16 ranks.  The last sub-range's
-//            final state is the carry of the next chunk.
+//            are produced, yields c^2 of all 16 ranks.
+// The carry pass also forms the chunk carry plus every total, the carry of the
+// next chunk, so a chunk needs two barriers (after phase 1 and after the carry
+// pass) and a wave that finishes its walk early goes on to the next phase 1.
 // The weights and row offsets of a wave's 32 ranks pass through a
 // wave-private LDS table, so that each half reads those of its own rank.  The
-// gathers are software-pipelined: while chunk k is computed, the value rows
-// of chunk k-1 are in flight and the order/score entries of chunk k-2 are
-// being fetched.  Also emitted: sum_j (s_j)_+ v_j (the value total of the
-// tail summary).
+// gathers are software-pipelined: once the walk has taken step r of chunk k,
+// the row of step r of chunk k-1 is fetched into the same registers (one set
+// of row registers, no copies), and the order/score entries of chunk k-2 are
+// fetched at the top of chunk k.  Also emitted: sum_j (s_j)_+ v_j (the value
+// total of the tail summary).
 #include "stages.h"
 
 namespace certkv {
@@ -118,12 +121,11 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   constexpr int NR = DP + 2;                   // per-lane record: W (its dims), q, m
   // Per lane of a half-wave: phase-1 totals of each wave (both halves), the
   // upper half's own totals, and the chunk carry (suffix sums above the
-  // chunk), double-buffered by chunk parity (the last sub-range writes the
-  // next carry while others may still read the current one).  One record
-  // layout for all three keeps a single per-lane LDS address.
+  // chunk; each column read and rewritten by one thread of the carry pass).
+  // One record layout for all three keeps a single per-lane LDS address.
   __shared__ __align__(16) double tR[kCurveWaves][kLPR][NR];
   __shared__ __align__(16) double uR[kCurveWaves][kLPR][NR];
-  __shared__ __align__(16) double cR[2][kLPR][NR];
+  __shared__ __align__(16) double cR[kLPR][NR];
   // per wave, by chunk parity: weights and row byte offsets (in 64-bit
   // slots) of its 32 ranks, entries 16 h + r: half h, step r
   __shared__ __align__(16) double wa[2][kCurveWaves][2 * kRPH];
@@ -186,16 +188,10 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       wo[k & 1][wave][lane] = (uint32_t)(valid ? min(max(pos, 0), n - 1) : 0) * vrow_bytes;
     }
   };
-  // Value rows of the half-wave's 16 ranks of the chunk in table slot `sl`;
-  // rows are clamped into the sequence, so every offset stays in the slice.
-  auto fetch_rows = [&](int sl, uint32_t (&raw)[kRPH][RAW]) {
-    const uint4* op = reinterpret_cast<const uint4*>(&wo[sl][wave][hf * kRPH]);
-#pragma unroll
-    for (int j = 0; j < kRPH / 2; ++j) {
-      const uint4 o = op[j];
-      load_words<RAW>(vrs, o.x + vlane, raw[2 * j]);
-      load_words<RAW>(vrs, o.z + vlane, raw[2 * j + 1]);
-    }
+  // Value row of step r of the half-wave's ranks in table slot `sl`; rows are
+  // clamped into the sequence, so every offset stays in the slice.
+  auto fetch_row = [&](int sl, int r, uint32_t (&raw)[RAW]) {
+    load_words<RAW>(vrs, (uint32_t)wo[sl][wave][hf * kRPH + r] + vlane, raw);
   };
   // weight of step r of this half-wave's ranks in table slot `sl`
   auto a_of = [&](int sl, int r) -> double {
@@ -204,12 +200,12 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   };
 
   const int nch = (n + kCurveChunk - 1) / kCurveChunk;
-  for (int i = threadIdx.x; i < kLPR * NR; i += kCurveThreads) (&cR[(nch - 1) & 1][0][0])[i] = 0.0;
+  for (int i = threadIdx.x; i < kLPR * NR; i += kCurveThreads) (&cR[0][0])[i] = 0.0;
 
   uint32_t k_n1, k_n2;
   int p_n1, p_n2;
   bool ok_n1, ok_n2;
-  uint32_t vcur[kRPH][RAW], vnext[kRPH][RAW];
+  uint32_t vcur[kRPH][RAW];
   {
     uint32_t k0;
     int p0;
@@ -218,15 +214,22 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     fetch_meta(nch - 2, k_n1, p_n1, ok_n1);
     publish(nch - 1, k0, p0, ok0);
   }
-  fetch_rows((nch - 1) & 1, vcur);
+  // The first chunk's rows one by one in step order, the order in which the
+  // walk fetches them: with the same order on both paths into the loop, the
+  // compiler's count of outstanding loads lets phase 1 wait for each row
+  // separately rather than for all of them.
+#pragma unroll
+  for (int r = 0; r < kRPH; ++r) {
+    fetch_row((nch - 1) & 1, r, vcur[r]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
   for (int k = nch - 1; k >= 0; --k) {
     const int par = k & 1;
-    // pipeline: order entries two chunks ahead, value rows one chunk ahead
-    // (chunk k-1 uses table slot par ^ 1)
+    // pipeline: order entries two chunks ahead; the table of chunk k-1 (slot
+    // par ^ 1), whose rows the walk below fetches
     fetch_meta(k - 2, k_n2, p_n2, ok_n2);
     publish(k - 1, k_n1, p_n1, ok_n1);
-    fetch_rows(par ^ 1, vnext);
 
     // phase 1: totals of each half's rows; the wave's totals (both halves)
     // and the upper half's own totals (for the lower half's carry)
@@ -270,18 +273,19 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       if (threadIdx.x < C) {
         const int col = threadIdx.x;
         double* t = &tR[0][0][0];
-        double run = (&cR[par][0][0])[col];
+        // every total read first: one LDS round trip, then the additions
+        double x[kCurveWaves];
 #pragma unroll
-        for (int w0 = 0; w0 < kCurveWaves; w0 += 4) {
-          double x[4];
+        for (int w = 0; w < kCurveWaves; ++w) x[w] = t[w * C + col];
+        double* cc = &cR[0][0] + col;
+        double run = *cc;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) x[j] = t[(w0 + j) * C + col];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            t[(w0 + j) * C + col] = run;
-            run += x[j];
-          }
+        for (int w = 0; w < kCurveWaves; ++w) {
+          t[w * C + col] = run;
+          run += x[w];
         }
+        // the chunk carry plus every total: the carry of the next chunk
+        *cc = run;
       }
     }
     __syncthreads();
@@ -354,6 +358,8 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
         }
       }
       if (!placed) c2 = cur;
+      // this row is spent: fetch row r of the next chunk into its registers
+      fetch_row(par ^ 1, r, vcur[r]);
     }
     // the two lanes sharing a step: add their copies
     c2 += __shfl_xor(c2, 1, 64);
@@ -365,27 +371,14 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       if (!isfinite(c2)) report_nonfinite(g);
       curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
     }
-    // the last sub-range's final state carries into the next chunk
-    if (wave == kCurveWaves - 1 && hf == 1) {
-      double* c = cR[par ^ 1][li];
-#pragma unroll
-      for (int t = 0; t < DP; ++t) c[t] = W[t];
-      c[DP] = q;
-      c[DP + 1] = m;
-    }
-    __syncthreads();
-    // rotate the pipeline
-#pragma unroll
-    for (int r = 0; r < kRPH; ++r) {
-#pragma unroll
-      for (int e = 0; e < RAW; ++e) vcur[r][e] = vnext[r][e];
-    }
     k_n1 = k_n2;
     p_n1 = p_n2;
     ok_n1 = ok_n2;
   }
+  // the carry after the last chunk: the sums over every rank
+  __syncthreads();
   if (vsum && wave == 0) {
-    for (int i = lane; i < D; i += 64) vsum[u * D + i] = cR[1][i / DP][i % DP] * tot;
+    for (int i = lane; i < D; i += 64) vsum[u * D + i] = cR[i / DP][i % DP] * tot;
   }
 }
 
