@@ -9,7 +9,8 @@
 // Q is kept as per-lane parts (the lane's dims of sum a |v|^2), which add up
 // to Q without a cross-lane reduction.  Per chunk:
 //   phase 1  each half-wave forms the totals of its 16 rows: m, W (per dim)
-//            and the lane parts of Q;
+//            and the lane parts of Q (with bf16 rows, each row's lane part
+//            of |v|^2 stays in registers for phase 2);
 //   carry    sub-range s starts from the chunk carry plus the totals of the
 //            sub-ranges 0..s-1 (higher ranks), added in a fixed order
 //            (deterministic);
@@ -119,6 +120,9 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   constexpr int E = BF16 ? 2 : 4;              // bytes per element
   constexpr int RAW = DP * E / 4;              // 32-bit words per lane per row
   constexpr int NR = DP + 2;                   // per-lane record: W (its dims), q, m
+  // phase 1 keeps the lane parts of |v|^2 of its rows for the walk (bf16
+  // rows; with fp32 rows the registers are not there and the walk recomputes)
+  constexpr bool kKeepNorms = BF16;
   // Per lane of a half-wave: phase-1 totals of each wave (both halves), the
   // upper half's own totals, and the chunk carry (suffix sums above the
   // chunk; each column read and rewritten by one thread of the carry pass).
@@ -233,6 +237,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
 
     // phase 1: totals of each half's rows; the wave's totals (both halves)
     // and the upper half's own totals (for the lower half's carry)
+    double vvs[kKeepNorms ? kRPH : 1];
     {
       double sW[DP], sq = 0.0, sm = 0.0;
 #pragma unroll
@@ -251,6 +256,7 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
         }
         sq = fma(ar, vv, sq);
         sm += ar;
+        if constexpr (kKeepNorms) vvs[r] = vv;
       }
       double tp[NR], bt[NR];
 #pragma unroll
@@ -331,8 +337,9 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
         const double vd = (double)v[t];
         W[t] = fma(ar, vd, W[t]);
         w2 = fma(W[t], W[t], w2);
-        vv = fma(vd, vd, vv);
+        if constexpr (!kKeepNorms) vv = fma(vd, vd, vv);
       }
+      if constexpr (kKeepNorms) vv = vvs[r];
       m += ar;
       q = fma(ar, vv, q);
       // the lanes' parts sum to m Q - |W|^2 (centered), m Q (uncentered) or,
