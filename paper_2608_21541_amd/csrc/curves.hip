@@ -16,8 +16,9 @@
 //            (deterministic);
 //   phase 2  the half-wave walks its ranks top-down extending m, W and its
 //            lane parts q; per rank each lane forms m q - |W|^2 over its dims
-//            and a transpose-reduce over the 32 lanes, folded in as the ranks
-//            are produced, yields c^2 of all 16 ranks.
+//            (its part of c^2) and leaves it in a wave-private LDS row; after
+//            every 8 ranks each lane adds up one rank's parts of 8 lanes and
+//            two lane exchanges complete the sums over the 32 lanes.
 // The carry pass also forms the chunk carry plus every total, the carry of the
 // next chunk, so a chunk needs two barriers (after phase 1 and after the carry
 // pass) and a wave that finishes its walk early goes on to the next phase 1.
@@ -36,7 +37,6 @@ constexpr int kCurveThreads = 1024;
 constexpr int kCurveWaves = kCurveThreads / 64;
 constexpr int kLPR = 32;                       // lanes per rank (a half-wave)
 constexpr int kRPH = 16;                       // ranks per half-wave and chunk
-constexpr int kLev = 4;                        // log2(kRPH)
 constexpr int kSubs = 2 * kCurveWaves;         // sub-ranges per chunk
 constexpr int kCurveChunk = kSubs * kRPH;      // 512 ranks
 
@@ -74,15 +74,13 @@ __device__ __forceinline__ double join_f64(uint32_t lo, uint32_t hi) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// One transpose-reduce step over lane bit 4: lanes with the bit clear end
-// with lo + partner's lo, lanes with it set with hi + partner's hi.
-// v_permlane16_swap exchanges the odd rows of 16 lanes of its first operand
-// with the even rows of its second, which is exactly that exchange.
-__device__ __forceinline__ double combine_swap16(double lo, double hi) {
-  const uint64_t a = (uint64_t)__double_as_longlong(lo);
-  const uint64_t b = (uint64_t)__double_as_longlong(hi);
-  const auto r0 = __builtin_amdgcn_permlane16_swap((uint32_t)a, (uint32_t)b, false, false);
-  const auto r1 = __builtin_amdgcn_permlane16_swap((uint32_t)(a >> 32), (uint32_t)(b >> 32), false,
+// x plus x of the lane 16 places away in the same half-wave.
+// v_permlane16_swap of x with itself exchanges neighbouring rows of 16 lanes,
+// leaving the lane's own value in one result and its partner's in the other.
+__device__ __forceinline__ double sum_lane16(double x) {
+  const uint64_t a = (uint64_t)__double_as_longlong(x);
+  const auto r0 = __builtin_amdgcn_permlane16_swap((uint32_t)a, (uint32_t)a, false, false);
+  const auto r1 = __builtin_amdgcn_permlane16_swap((uint32_t)(a >> 32), (uint32_t)(a >> 32), false,
                                                    false);
   return join_f64(r0[0], r1[0]) + join_f64(r0[1], r1[1]);
 }
@@ -98,6 +96,14 @@ __device__ __forceinline__ void halves(double x, double& top, double& bot) {
       __builtin_amdgcn_permlane32_swap((uint32_t)(a >> 32), (uint32_t)(a >> 32), false, false);
   top = join_f64(r0[0], r1[0]);
   bot = join_f64(r0[1], r1[1]);
+}
+
+// x of the lane 8 places along in the lane's row of 16 (DPP row rotation).
+__device__ __forceinline__ double row_ror8(double x) {
+  const uint64_t a = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)a, 0x128, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(a >> 32), 0x128, 0xF, 0xF, false);
+  return join_f64(lo, hi);
 }
 
 // A wave-uniform double, moved to scalar registers.
@@ -134,6 +140,10 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
   // slots) of its 32 ranks, entries 16 h + r: half h, step r
   __shared__ __align__(16) double wa[2][kCurveWaves][2 * kRPH];
   __shared__ __align__(16) uint64_t wo[2][kCurveWaves][2 * kRPH];
+  // per lane: its parts of c^2 of 8 walk steps (rows padded to 9 doubles,
+  // so that the writes of a step and the group reads are free of bank
+  // conflicts)
+  __shared__ __align__(16) double red[kCurveWaves][64][9];
 
   const int h = blockIdx.x % g.H;
   const int bl = blockIdx.x / g.H;
@@ -319,13 +329,12 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
 #pragma unroll
       for (int e = 0; e < RAW; ++e) __asm__ volatile("" : "+v"(vcur[r][e]));
     }
-    // phase 2: walk the ranks top-down.  Streaming transpose-reduce of the
-    // per-lane values over lane bits 4, 3, ...: steps 2i and 2i+1 combine
-    // over lane bit 4 as soon as both exist, pairs of those over bit 3, and
-    // so on, so at most one pending value per level is live.  Lane bit 4 - j
-    // ends up naming step bit j.
-    double pend[kLev];
-    double c2 = 0.0;
+    // phase 2: walk the ranks top-down.  Each lane's part of c^2 of step r
+    // goes to slot r % 8 of its LDS row; after steps 7 and 15 the lanes with
+    // li % 8 = j add up the parts of step j of the 8 lanes of their group
+    // (li / 8), a row rotation by 8 lanes adds the neighbouring group and a
+    // swap of 16-lane rows the other two.  c2r[h]: step 8 h + li % 8.
+    double c2r[2];
 #pragma unroll
     for (int r = 0; r < kRPH; ++r) {
       const double ar = a_of(par, r);
@@ -347,34 +356,28 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
       // square root is m
       const int stat = STAT >= 0 ? STAT : g.stat;
       double cur = stat == 0 ? fma(m, q, -w2) : stat == 1 ? m * q : (m * m) * (1.0 / kLPR);
-      bool placed = false;
-#pragma unroll
-      for (int lev = 0; lev < kLev; ++lev) {
-        if (placed) continue;
-        if (((r >> lev) & 1) == 0) {
-          pend[lev] = cur;
-          placed = true;
-        } else if (lev == 0) {
-          cur = combine_swap16(pend[0], cur);
-        } else {
-          const int msk = (kLPR / 2) >> lev;
-          const bool up = (lane & msk) != 0;
-          const double keep = up ? cur : pend[lev];
-          const double send = up ? pend[lev] : cur;
-          cur = keep + __shfl_xor(send, msk, 64);
-        }
-      }
-      if (!placed) c2 = cur;
+      red[wave][lane][r & 7] = cur;
       // this row is spent: fetch row r of the next chunk into its registers
       fetch_row(par ^ 1, r, vcur[r]);
-    }
-    // the two lanes sharing a step: add their copies
-    c2 += __shfl_xor(c2, 1, 64);
-    int r_mine = 0;
+      if ((r & 7) == 7) {
+        // Compiler barriers only: a wave's LDS accesses execute in order, so
+        // the reads see every lane's writes of these 8 steps and the next
+        // steps' writes follow the reads.
+        __asm__ volatile("" ::: "memory");
+        const double* col = &red[wave][hf * kLPR + (li >> 3) * 8][li & 7];
+        double x[8];
 #pragma unroll
-    for (int lev = 0; lev < kLev; ++lev) r_mine |= ((li >> (kLev - lev)) & 1) << lev;
+        for (int i = 0; i < 8; ++i) x[i] = col[i * 9];
+        double s = ((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7]));
+        s += row_ror8(s);
+        c2r[r >> 3] = sum_lane16(s);
+        __asm__ volatile("" ::: "memory");
+      }
+    }
+    const int r_mine = li & (kRPH - 1);
+    const double c2 = (li & 8) ? c2r[1] : c2r[0];
     const int rk = rank_of(k, 2 * wave + hf, r_mine);
-    if ((li & 1) == 0 && rk < n) {
+    if (li < kRPH && rk < n) {
       if (!isfinite(c2)) report_nonfinite(g);
       curves[base + rk] = (float)sqrt(c2 > 0.0 ? c2 : 0.0);
     }
