@@ -66,18 +66,9 @@ __global__ __launch_bounds__(1024) void offsets_kernel(int64_t U, int32_t slot,
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kSelPer = 4;                        // consecutive positions per thread
-constexpr int kSelTile = kSelThreads * kSelPer;   // 4096 positions per iteration
-
-// Spread the 16 low bits of x to every fourth bit of a 64-bit word.
-__device__ __forceinline__ uint64_t spread4(uint64_t x) {
-  x &= 0xffffull;
-  x = (x | (x << 24)) & 0x000000ff000000ffull;
-  x = (x | (x << 12)) & 0x000f000f000f000full;
-  x = (x | (x << 6)) & 0x0303030303030303ull;
-  x = (x | (x << 3)) & 0x1111111111111111ull;
-  return x;
-}
+constexpr int kSelRounds = 8;                     // rounds of 1024 consecutive positions
+constexpr int kSelTile = kSelThreads * kSelRounds; // 8192 positions per iteration
+constexpr int kSelScanPer = kSelRounds * kSelWaves / 64;  // counts per lane of the scan
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Geo g, SeqTab st, const float* __restrict__ scores, const uint32_t* __restrict__ sorted_keys,
@@ -85,7 +76,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int64_t* __restrict__ kept_offsets, int32_t* __restrict__ kept_idx, int64_t capacity,
     double* __restrict__ evicted_sum, double* __restrict__ total_sum, uint64_t* __restrict__ bm,
     int32_t bm_stride) {
-  __shared__ int32_t wtot[2][kSelWaves];
+  // kept counts of each (round, wave) of a tile, then their exclusive prefix
+  // in position order (round-major); the tile's total at the end
+  __shared__ uint32_t kcnt[kSelRounds * kSelWaves + 1];
   __shared__ double dsum[2][kSelWaves];
   const int h = blockIdx.x % g.H;
   const int bl = blockIdx.x / g.H;
@@ -107,69 +100,81 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int64_t off = kept_offsets[u];
   int64_t run = 0;
   double se = 0.0, sa = 0.0;
-  // Positions past the end read the last score (clamped, so no branch sits
-  // around the loads and the next step's loads stay in flight while this
-  // step is tested); they are masked where used.
-  auto load = [&](int j0, float (&sv)[kSelPer]) {
+  // Round r of a tile: positions j0 + 1024 r + thread, so every load covers
+  // 256 consecutive bytes per wave.  Loads through a range-checked buffer:
+  // positions past the end read as zero, so no branch sits around them and
+  // the next tile's loads stay in flight while this one is tested; they are
+  // masked where used.
+  const BufRsrc srs = make_rsrc(scores + base, (uint32_t)n * 4u);
+  auto load = [&](int j0, float (&sv)[kSelRounds]) {
 #pragma unroll
-    for (int r = 0; r < kSelPer; ++r) {
-      const int j = j0 + kSelPer * threadIdx.x + r;
-      sv[r] = scores[base + min(j, n - 1)];
-    }
+    for (int r = 0; r < kSelRounds; ++r)
+      sv[r] = __uint_as_float(
+          buf_load_u32(srs, (uint32_t)(j0 + r * kSelThreads + (int)threadIdx.x) * 4u));
   };
-  float cur[kSelPer], nxt[kSelPer];
-  if (n > 0) load(0, cur);  // (an empty segment reads nothing)
-  for (int j0 = 0, it = 0; j0 < n; j0 += kSelTile, ++it) {
+  float cur[kSelRounds], nxt[kSelRounds];
+  load(0, cur);
+  for (int j0 = 0; j0 < n; j0 += kSelTile) {
     load(j0 + kSelTile, nxt);
-    const int jt = j0 + kSelPer * threadIdx.x;
-    bool keep[kSelPer];
-    uint64_t bal[kSelPer];
-    uint32_t below = 0, wsum = 0;
+    uint32_t kmask = 0;
+    uint64_t bal[kSelRounds];  // wave-uniform: scalar registers
 #pragma unroll
-    for (int r = 0; r < kSelPer; ++r) {
-      const int j = jt + r;
+    for (int r = 0; r < kSelRounds; ++r) {
+      const int j = j0 + r * kSelThreads + (int)threadIdx.x;
       const bool valid = j < n;
       const uint32_t key = desc_key(cur[r]);
       // kept window keys hold ranks 0..w-1 in position order; the others
       // are kept up to the threshold pair at rank bb-1
-      keep[r] = valid && (j >= wkeep ? (j - wkeep < bb)
-                                     : (bb > g.keep_w && (key < kthr || (key == kthr && j <= ithr))));
+      const bool keep = valid && (j >= wkeep ? (j - wkeep < bb)
+                                             : (bb > g.keep_w && (key < kthr || (key == kthr && j <= ithr))));
       const double sp = (valid && cur[r] > 0.f) ? (double)cur[r] : 0.0;
       sa += sp;
-      se += keep[r] ? 0.0 : sp;
-      bal[r] = __ballot(keep[r]);
-      below += __builtin_amdgcn_mbcnt_hi((uint32_t)(bal[r] >> 32),
-                                         __builtin_amdgcn_mbcnt_lo((uint32_t)bal[r], 0u));
-      wsum += (uint32_t)__popcll(bal[r]);
-    }
-    // kept bitmap: lanes 16q..16q+15 of the wave cover word q of its 256 positions
-    if (bm && lane < 4) {
-      uint64_t word = 0;
-#pragma unroll
-      for (int r = 0; r < kSelPer; ++r) word |= spread4(bal[r] >> (16 * lane)) << r;
-      const int widx = (j0 >> 6) + wave * 4 + lane;
-      if (widx < bm_stride) bm[u * bm_stride + widx] = word;
-    }
-    if (lane == 0) wtot[it & 1][wave] = (int32_t)wsum;
-    __syncthreads();
-    int64_t pre = run;
-    int64_t tile = 0;
-    for (int w = 0; w < kSelWaves; ++w) {
-      const int32_t c = wtot[it & 1][w];
-      if (w < wave) pre += c;
-      tile += c;
-    }
-    int64_t dst = off + pre + below;
-#pragma unroll
-    for (int r = 0; r < kSelPer; ++r) {
-      if (keep[r]) {
-        if (dst < capacity) kept_idx[dst] = jt + r;
-        ++dst;
+      se += keep ? 0.0 : sp;
+      bal[r] = __ballot(keep);
+      kmask |= (uint32_t)keep << r;
+      if (lane == 0) {
+        kcnt[r * kSelWaves + wave] = (uint32_t)__popcll(bal[r]);
+        // kept bitmap: the ballot is the word of the wave's 64 positions
+        const int widx = ((j0 + r * kSelThreads) >> 6) + wave;
+        if (bm && widx < bm_stride) bm[u * bm_stride + widx] = bal[r];
       }
     }
-    run += tile;
+    __syncthreads();
+    // exclusive prefix of the counts in position order (one wave)
+    if (wave == 0) {
+      uint32_t c[kSelScanPer], t = 0;
 #pragma unroll
-    for (int r = 0; r < kSelPer; ++r) cur[r] = nxt[r];
+      for (int i = 0; i < kSelScanPer; ++i) {
+        c[i] = kcnt[kSelScanPer * lane + i];
+        t += c[i];
+      }
+      uint32_t incl = t;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      uint32_t ex = incl - t;
+#pragma unroll
+      for (int i = 0; i < kSelScanPer; ++i) {
+        kcnt[kSelScanPer * lane + i] = ex;
+        ex += c[i];
+      }
+      if (lane == 63) kcnt[kSelRounds * kSelWaves] = incl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSelRounds; ++r) {
+      if ((kmask >> r) & 1u) {
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(bal[r] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal[r], 0u));
+        const int64_t dst = off + run + kcnt[r * kSelWaves + wave] + below;
+        if (dst < capacity) kept_idx[dst] = j0 + r * kSelThreads + (int)threadIdx.x;
+      }
+    }
+    run += kcnt[kSelRounds * kSelWaves];
+#pragma unroll
+    for (int r = 0; r < kSelRounds; ++r) cur[r] = nxt[r];
   }
   se = wave_sum(se);
   sa = wave_sum(sa);

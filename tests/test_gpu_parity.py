@@ -181,6 +181,29 @@ def test_keep_all_and_minimal_budgets():
                                    cache["v"][0, last, h].float().numpy(), rtol=1e-6, atol=1e-7)
 
 
+def test_keep_all_direct_tail_over_several_select_tiles():
+    # n_keep = n on segments spanning several selection tiles: the evicted
+    # set is the last-ranked key alone, so the tail summary takes its direct
+    # form, which skips the kept positions through the selection's bitmap.
+    lens = [40000, 17000]
+    cfg = synth.config("C2", seqlens=lens)
+    cache = synth.make_cache(cfg, "cpu")
+    cache["n_keep"] = list(lens)
+    spec, out, _, _ = run_gpu(cfg, cache)
+    H = cfg.kv_heads
+    bud = out["budgets"].numpy()
+    start = 0
+    for b, n in enumerate(lens):
+        assert (bud[b * H:(b + 1) * H] == n - 1).all()
+        for h in range(H):
+            u = unit_id(spec, 0, b, h)
+            last = out["perm"][0, h, start + n - 1].item()
+            np.testing.assert_allclose(out["v_star"][u].numpy(),
+                                       cache["v"][0, start + last, h].float().numpy(),
+                                       rtol=1e-6, atol=1e-7)
+        start += n
+
+
 def test_determinism_bitwise():
     cfg = synth.config("C2", seqlens=[5000, 3333])
     cache = synth.make_cache(cfg, "cpu")
