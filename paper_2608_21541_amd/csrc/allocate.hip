@@ -59,6 +59,18 @@ __device__ __forceinline__ uint32_t count_below64(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
+// A curve value as the block statistics and the repair read it: unchanged
+// when finite; NaN and +inf read as the largest finite float, -inf as its
+// negative.  The bisection's candidate scans read the curves as they are (a
+// NaN never wins a comparison), and a head left without an argmin starts the
+// repair from b_min.  So with non-finite curves (a caller's, or from
+// non-finite inputs) the budgets still lie in [b_min, n-1] and sum to B_real,
+// meaningless as they are, and the status word reports the values.
+__device__ __forceinline__ float cval(float x) {
+  constexpr float kMax = 3.40282347e38f;  // the largest finite float
+  return fmaxf(fminf(x, kMax), -kMax);
+}
+
 __device__ __forceinline__ bool lex_less(double f1, int b1, double f2, int b2) {
   return f1 < f2 || (f1 == f2 && b1 < b2);
 }
@@ -237,6 +249,17 @@ __global__ __launch_bounds__(256) void curve_blockstats_kernel(Geo g, SeqTab st,
 #pragma unroll
     for (int e = 0; e < 5; ++e) c[j][e] = ch[min(i0 + e, n - 1)];
   }
+  // a caller's non-finite curve values: reported, then read as cval() reads them
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < kBsBlocks; ++j) {
+#pragma unroll
+    for (int e = 0; e < 5; ++e) {
+      bad |= !isfinite(c[j][e]);
+      c[j][e] = cval(c[j][e]);
+    }
+  }
+  if (__ballot(bad) != 0ull && lane == 0) report_nonfinite(g);
 #pragma unroll
   for (int j = 0; j < kBsBlocks; ++j) {
     const int k = k0 + j;
@@ -868,6 +891,10 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     if (!have_bhi) evaluate(hi, bhi);
   }
   const uint64_t t_bisect = wall_clock64();
+  // A head whose curve holds no comparable value from b_min on (all NaN) has
+  // no argmin: it starts the repair from b_min.
+  if (tid < H && (bhi[tid] < bmin || bhi[tid] > n - 1)) bhi[tid] = bmin;
+  __syncthreads();
 
   int64_t sum0 = 0;
   for (int h = 0; h < H; ++h) sum0 += bhi[h];
@@ -908,7 +935,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
 #pragma unroll
       for (int m = 0; m < (kBlk + 32) / 32; ++m) {
         const int i = sub + 32 * m;
-        v[m] = i <= kBlk ? ch[min(lo_k * kBlk + i, n - 1)] : 0.f;
+        v[m] = i <= kBlk ? cval(ch[min(lo_k * kBlk + i, n - 1)]) : 0.f;
       }
 #pragma unroll
       for (int m = 0; m < (kBlk + 32) / 32; ++m) {
@@ -969,7 +996,8 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
         double dm = -INFINITY;
         if (s <= n - 2) {
           const int e1 = min(ks * kBlk + kBlk - 1, n - 2);
-          for (int i = s + sub; i <= e1; i += 32) dm = fmax(dm, (double)ch[i + 1] - (double)ch[i]);
+          for (int i = s + sub; i <= e1; i += 32)
+            dm = fmax(dm, (double)cval(ch[i + 1]) - (double)cval(ch[i]));
         }
 #pragma unroll
         for (int m = 16; m >= 1; m >>= 1) dm = fmax(dm, __shfl_xor(dm, m, 64));
@@ -1070,13 +1098,13 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     int64_t sum = sum0;
     int wbase = bh;  // win[lane][i] = c(wbase + i)
     if (act)
-      for (int i = 0; i <= kRepairWin && wbase + i < n; ++i) win[lane][i] = ch[wbase + i];
+      for (int i = 0; i <= kRepairWin && wbase + i < n; ++i) win[lane][i] = cval(ch[wbase + i]);
     while (sum < B_real) {
       double d = INFINITY;
       if (act && bh < n - 1) {
         if (bh + 1 - wbase > kRepairWin) {
           wbase = bh;
-          for (int i = 0; i <= kRepairWin && wbase + i < n; ++i) win[lane][i] = ch[wbase + i];
+          for (int i = 0; i <= kRepairWin && wbase + i < n; ++i) win[lane][i] = cval(ch[wbase + i]);
         }
         d = (double)win[lane][bh + 1 - wbase] - (double)win[lane][bh - wbase];
       }
@@ -1087,7 +1115,7 @@ __global__ __launch_bounds__(kAllocThreads) void allocate_kernel(
     }
     while (sum > B_real) {
       double d = INFINITY;
-      if (act && bh > bmin) d = (double)ch[bh - 1] - (double)ch[bh];
+      if (act && bh > bmin) d = (double)cval(ch[bh - 1]) - (double)cval(ch[bh]);
       const BestFB r = wave_lexmin(d, act ? lane : 0x7fffffff);
       if (r.f == INFINITY) break;  // unreachable: H b_min <= B_real
       if (lane == r.b) --bh;

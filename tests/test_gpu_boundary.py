@@ -139,6 +139,31 @@ def test_nonfinite_inputs_set_the_status_word(where):
     assert int(bufs.budgets.sum().item()) == br
 
 
+@pytest.mark.parametrize("H,n", [(8, 3000), (64, 40000)])
+def test_allocate_curves_with_nonfinite_values_keeps_the_budget_algebra(H, n):
+    # Caller curves holding NaN (a whole head, and scattered), +inf and -inf:
+    # the status word reports them and the budgets still obey the algebra
+    # (each in [b_min, n-1], summing to B_real).  H = 64 with n = 40000 takes
+    # the pruned scans and the sequential repair, 8 x 3000 the LDS paths.
+    rng = np.random.default_rng(n)
+    c = np.abs(np.cumsum(rng.standard_normal((H, n)), 1))[:, ::-1].astype(np.float32)
+    c[2, :] = np.nan
+    c[4, 100:200] = np.inf
+    c[5, 10] = -np.inf
+    c[6, ::7] = np.nan
+    dev = torch.device("cuda:0")
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    spec = ck.ProblemSpec(1, H, 2, 64, 16, [n], torch.bfloat16, status=status)
+    t = torch.from_numpy(np.ascontiguousarray(c)).reshape(1, H, n).to(dev)
+    for n_keep in (2, 97, n // 3):
+        status.zero_()
+        b = ck.allocate_curves(spec, t, [n_keep]).cpu().numpy().reshape(-1)
+        torch.cuda.synchronize()
+        assert status.item() == ck.CERTKV_ENONFINITE
+        br, bm = oracle.budget_params(H, n, n_keep)
+        assert int(b.sum()) == br and b.min() >= bm and b.max() <= n - 1, (n_keep, b)
+
+
 def test_keep_window_matches_oracle():
     # both lengths give b_min >= w = 64 (83 and 70)
     cfg = synth.config("C2", seqlens=[4173, 3500])
