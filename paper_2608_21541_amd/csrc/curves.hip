@@ -113,10 +113,9 @@ __device__ __forceinline__ double uniform_f64(double x) {
                   __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)));
 }
 
-// STAT: the curve statistic (0 centered, 1 uncentered, 2 tail mass) fixed at
-// compile time, so that the walk has no branch on it, or -1: read from
-// g.stat at run time (the ablation statistics: compiled with the statistic
-// fixed, their walks need more registers than the kernel has and spill).
+// STAT: the curve statistic (0 centered, 1 uncentered, 2 tail mass), fixed at
+// compile time so that the walk has no branch on it; -1 reads it from g.stat
+// at run time (not launched: each statistic has its own instantiation).
 template <int D, bool BF16, int STAT>
 __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
     Geo g, SeqTab st, const uint32_t* __restrict__ sorted_keys, const int32_t* __restrict__ perm,
@@ -395,14 +394,17 @@ __global__ __launch_bounds__(kCurveThreads) void curves_kernel(
 template <int D, bool BF16>
 static certkv_status launch_curves(const CurveArgs& a, const SeqTab& st, hipStream_t s) {
   const dim3 grid(a.g.H * st.count, a.g.L);
+#define CERTKV_CURVES(STAT)                                                                        \
+  CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, STAT>), grid, dim3(kCurveThreads), 0, s, a.g, st, \
+                a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,       \
+                a.curves, a.vsum)
   if (a.g.stat == 0)
-    CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, 0>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                  a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                  a.curves, a.vsum);
+    CERTKV_CURVES(0);
+  else if (a.g.stat == 1)
+    CERTKV_CURVES(1);
   else
-    CERTKV_LAUNCH("curves", (curves_kernel<D, BF16, -1>), grid, dim3(kCurveThreads), 0, s, a.g, st,
-                  a.sorted_keys, a.perm, a.ssum, a.v.ptr, a.v.s_layer, a.v.s_token, a.v.s_head,
-                  a.curves, a.vsum);
+    CERTKV_CURVES(2);
+#undef CERTKV_CURVES
   return CERTKV_OK;
 }
 

@@ -22,7 +22,8 @@ KERNELS = [
     ("score.hip", "_ZN6certkv22score_pass2_w16_kernelILi128ELi8ELb0E", 128),  # pass 2
     ("sort.hip", "_ZN6certkv15seg_sort_kernel", 128),
     ("curves.hip", "_ZN6certkv13curves_kernelILi128ELb1ELi0E", 128),         # centered
-    ("curves.hip", "_ZN6certkv13curves_kernelILi128ELb1ELin1E", 128),        # ablation statistics
+    ("curves.hip", "_ZN6certkv13curves_kernelILi128ELb1ELi1E", 128),         # uncentered
+    ("curves.hip", "_ZN6certkv13curves_kernelILi128ELb1ELi2E", 128),         # tail mass
     ("curves.hip", "_ZN6certkv13curves_kernelILi64ELb0ELi0E", 128),          # fp32, d = 64
     ("allocate.hip", "_ZN6certkv15allocate_kernel", 128),
     ("select.hip", "_ZN6certkv13select_kernel", 128),
